@@ -1,0 +1,101 @@
+"""CPU oracle for the fused multi-table lookup -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg import
+this package.  It wraps ``liboracle.so`` (plain C, fp64, see oracle.c) with
+numpy arrays and shares nothing with the GPU library.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+from .build import LIB, build
+
+OK, BAD_ARG, BAD_OFFSETS, BAD_ID = 0, 1, 5, 6
+FLAG_EXACT_SPLIT = 1 << 1
+
+_libs = {}
+
+
+def _load(path: Optional[str] = None):
+    path = path or LIB
+    if path not in _libs:
+        if path == LIB and not os.path.exists(LIB):
+            build()
+        lib = ctypes.CDLL(path)
+        p = ctypes.c_void_p
+        lib.oracle_lookup.argtypes = [ctypes.c_int32, ctypes.c_int64, p, p, p, p, p, p, p, p, p,
+                                      ctypes.c_int32]
+        lib.oracle_lookup.restype = ctypes.c_int
+        lib.oracle_plan.argtypes = [ctypes.c_int32, ctypes.c_int64, p, p, ctypes.c_int32, p,
+                                    ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                    ctypes.c_uint32, p, p, p, p, p, p]
+        lib.oracle_plan.restype = ctypes.c_int
+        _libs[path] = lib
+    return _libs[path]
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+class OracleError(RuntimeError):
+    def __init__(self, code: int):
+        super().__init__(f"oracle status {code}")
+        self.code = code
+
+
+def lookup(dims: Sequence[int], tables: Sequence[np.ndarray], ids: np.ndarray,
+           offsets: Optional[np.ndarray], pooling: Optional[Sequence[int]], batch: int,
+           with_mag: bool = True, nthreads: int = 0, lib_path: Optional[str] = None):
+    """Pooled [batch, sum(dims)] fp64 result (and its magnitude bound)."""
+    lib = _load(lib_path)
+    T = len(dims)
+    tabs = [np.ascontiguousarray(t) for t in tables]
+    dtypes = np.array([1 if t.dtype == np.float16 else 0 for t in tabs], dtype=np.int32)
+    for t in tabs:
+        if t.dtype not in (np.float16, np.float32):
+            raise TypeError(t.dtype)
+    dims_a = np.ascontiguousarray(dims, dtype=np.int32)
+    rows = np.array([t.shape[0] for t in tabs], dtype=np.int64)
+    ptrs = (ctypes.c_void_p * T)(*[t.ctypes.data for t in tabs])
+    ids_a = np.ascontiguousarray(ids, dtype=np.int32)
+    off_a = None if offsets is None else np.ascontiguousarray(offsets, dtype=np.int32)
+    pool = None if pooling is None else np.ascontiguousarray(pooling, dtype=np.int32)
+    total_d = int(dims_a.sum())
+    out = np.empty((batch, total_d), dtype=np.float64)
+    mag = np.empty_like(out) if with_mag else None
+    st = lib.oracle_lookup(T, batch, _ptr(rows), _ptr(dims_a), _ptr(dtypes),
+                           ctypes.cast(ptrs, ctypes.c_void_p), _ptr(ids_a), _ptr(off_a), _ptr(pool),
+                           _ptr(out), _ptr(mag), nthreads)
+    if st != OK:
+        raise OracleError(st)
+    return (out, mag) if with_mag else out
+
+
+def plan(dims: Sequence[int], dtypes: Sequence[int], out_dtype: int, offsets: Optional[np.ndarray],
+         batch: int, total_ids: int, chunk_rows: int, item_cost_k: int, waves_requested: int,
+         flags: int = 0, lib_path: Optional[str] = None):
+    """Integer work plan; returns a dict of int64 arrays."""
+    lib = _load(lib_path)
+    T = len(dims)
+    dims_a = np.ascontiguousarray(dims, dtype=np.int32)
+    dt_a = np.ascontiguousarray(dtypes, dtype=np.int32)
+    off_a = None if offsets is None else np.ascontiguousarray(offsets, dtype=np.int32)
+    hdr = np.zeros(16, dtype=np.int64)
+    col = np.zeros(T + 1, dtype=np.int64)
+    idb = np.zeros(T + 1, dtype=np.int64)
+    bib = np.zeros(T * batch + 1, dtype=np.int64)
+    bcb = np.zeros(T * batch + 1, dtype=np.int64)
+    wib = np.zeros(waves_requested + 1, dtype=np.int64)
+    st = lib.oracle_plan(T, batch, _ptr(dims_a), _ptr(dt_a), out_dtype, _ptr(off_a), total_ids,
+                         chunk_rows, item_cost_k, waves_requested, flags, _ptr(hdr), _ptr(col),
+                         _ptr(idb), _ptr(bib), _ptr(bcb), _ptr(wib))
+    if st != OK:
+        raise OracleError(st)
+    W = int(hdr[3])
+    return {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib,
+            "bag_cost_base": bcb, "wave_item_begin": wib[: W + 1]}

@@ -1,0 +1,85 @@
+"""Plant plausible mistakes in a copy of the oracle and check a pin catches each.
+
+The copy is compiled on the CPU into a temporary directory; the real oracle
+is untouched.  Each mutant must fail at least one pin of
+test_oracle_pins / test_plan_oracle.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle.build import HERE, build
+import test_oracle_pins as LP
+import test_plan_oracle as PP
+
+MUTANTS = {
+    "mean_divisor": ("o[c] /= (double)len;", "o[c] /= (double)(len + 1);"),
+    "always_mean": ("if (pooling && pooling[t] == 1 && len > 0)", "if (len > 0)"),
+    "ids_local_index": ("ids[id_base[t] + j]", "ids[id_base[t] + j - start]"),
+    "previous_col_base": ("out + b * total_d + col_base[t];", "out + b * total_d + col_base[t > 0 ? t - 1 : 0];"),
+    "half_bias": ("e - 25);", "e - 24);"),
+    "half_subnormal": ("ldexp((double)m, -24)", "ldexp((double)m, -23)"),
+    "half_sign": ("return sign ? -v : v;", "return v;"),
+    "onehot_index": ("start = b;\n      end = b + 1;", "start = (b + 1) % B;\n      end = start + 1;"),
+    "drop_last_id": ("for (int64_t j = start; j < end; ++j)", "for (int64_t j = start; j < end - 1; ++j)"),
+    "items_floor": ("int64_t n = (L + C - 1) / C;", "int64_t n = L / C;"),
+    "out_bytes_every_chunk": ("return rows * row_bytes + (j == 0 ? out_bytes : 0) + K;",
+                              "return rows * row_bytes + out_bytes + K;"),
+    "no_item_constant": ("return rows * row_bytes + (j == 0 ? out_bytes : 0) + K;",
+                         "return rows * row_bytes + (j == 0 ? out_bytes : 0) + (j == 0 ? K : 1);"),
+    "chunk_rows_shifted": ("int64_t lo = j * C, hi = (j + 1) * C;", "int64_t lo = j * C, hi = (j + 1) * C + 1;"),
+    "target_floor": ("(int64_t)((num + (uint64_t)W - 1) / (uint64_t)W)", "(int64_t)(num / (uint64_t)W)"),
+    "slack_wide": ("S / (2 * W)", "S / W"),
+    "snap_backward": ("begin = bag_item_base[bag + 1];", "begin = bag_item_base[bag];"),
+    "split_double_count": ("if (b0 > bag_item_base[bag] && bag != last_split)", "if (b0 > bag_item_base[bag])"),
+    "no_wave_clamp": ("waves_requested < N ? waves_requested : N", "waves_requested"),
+    "id_base_onehot": ("int64_t nnz = offsets ? offsets[t * (B + 1) + B] : B;",
+                       "int64_t nnz = offsets ? offsets[t * (B + 1) + B] : B - (t > 0);"),
+}
+
+
+def _pins():
+    yield lambda: LP.test_golden_lookup("lookup_fig5_onehot.txt")
+    yield lambda: LP.test_golden_lookup("lookup_multihot_mixed.txt")
+    yield lambda: LP.test_onehot_equals_algorithm1(1, None)
+    yield lambda: LP.test_pooled_equals_embedding_bag(5, 128, None)
+    yield LP.test_empty_bags_are_zero
+    yield LP.test_one_hot_bag_is_the_row
+    yield LP.test_mean_is_sum_over_length
+    yield LP.test_binary16_decode_all_patterns
+    for name in ("plan_small_w3.txt", "plan_small_w3_exact.txt", "plan_small_w8.txt"):
+        yield (lambda n: (lambda: PP.test_golden_plan(n)))(name)
+    for seed in range(8):
+        yield (lambda s: (lambda: PP.test_random_small_plans(s)))(seed)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path, monkeypatch):
+    old, new = MUTANTS[name]
+    src = open(os.path.join(HERE, "oracle.c")).read()
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found"
+    mutated = src.replace(old, new, 1)
+    path = tmp_path / "oracle_mutant.c"
+    path.write_text(mutated)
+    lib = build(source=str(path), out=str(tmp_path / f"liboracle_{name}.so"))
+    monkeypatch.setattr(oracle, "LIB", lib)
+    caught = []
+    for pin in _pins():
+        try:
+            pin()
+        except (AssertionError, oracle.OracleError, IndexError, ValueError):
+            caught.append(pin)
+            break
+    assert caught, f"no pin catches mutant {name}"
+
+
+def test_unmutated_copy_passes(tmp_path, monkeypatch):
+    src = open(os.path.join(HERE, "oracle.c")).read()
+    path = tmp_path / "oracle_copy.c"
+    path.write_text(src)
+    lib = build(source=str(path), out=str(tmp_path / "liboracle_copy.so"))
+    monkeypatch.setattr(oracle, "LIB", lib)
+    for pin in _pins():
+        pin()
