@@ -1,0 +1,173 @@
+/*
+ * dpi.h -- C ABI of the fused multi-table embedding lookup for MI355X (gfx950).
+ *
+ * What it computes (DPIFrame, §IV-B and §IV-C): every sparse field t has its
+ * own embedding table E_t (num_rows x dim, row-major).  For a batch of B
+ * samples, field t of sample b holds a bag of row ids; the bag's rows are
+ * gathered and pooled (sum, or mean over the bag length), and the pooled rows
+ * of all fields are written side by side, in field order, into one
+ * [B, sum_t dim_t] block -- the input of the interaction layers.  All fields
+ * and samples are processed by one launch driven by a work plan computed in
+ * advance from the bags' lengths (§III opportunity 2: the whole embedding
+ * workload is known before execution).  One-hot fields are bags of one id;
+ * multi-hot fields are delimited by offsets (last paragraph of §IV-B).
+ * Pooling, empty bags and accumulation precision are not defined by the
+ * paper; this library's reading: per-field sum or mean, an empty bag yields
+ * zeros, accumulation in fp32 for fp32 and fp16 tables, one round-to-
+ * nearest-even conversion to the output dtype.
+ *
+ * Memory and streams
+ *   - The caller owns every device buffer (tables, ids, offsets, out,
+ *     workspace).  The library allocates only the small host object behind
+ *     dpi_plan_t.  A plan borrows its workspace: the workspace must outlive
+ *     the plan and every lookup issued with it.
+ *   - dpi_plan and dpi_lookup validate host-visible arguments synchronously,
+ *     enqueue kernels on `stream` (a hipStream_t; NULL = default stream) and
+ *     return without synchronizing.  Device-detected errors (malformed
+ *     offsets, out-of-range ids) are latched into a status word in the
+ *     workspace and reported by dpi_plan_sync_status.
+ *   - One lookup in flight per plan: bags cut between two waves combine
+ *     their partial sums through workspace memory.  Distinct plans (distinct
+ *     workspaces) may run concurrently on distinct streams.
+ *   - Nothing aborts, exits or prints.  Identical inputs give bitwise
+ *     identical plans and outputs (no floating-point atomics; partial sums
+ *     are combined in a fixed order).
+ *
+ * Layouts
+ *   offsets: int32 [T][B+1]; row t is local to field t: offsets[t][0] == 0,
+ *            non-decreasing, offsets[t][B] = number of ids of field t
+ *            (< 2^31).  NULL means every bag holds exactly one id.
+ *   ids:     int32, the fields' id lists concatenated in field order; bag
+ *            (t, b) is ids[id_base[t] + offsets[t][b] .. id_base[t] +
+ *            offsets[t][b+1]) with id_base the exclusive prefix of the fields'
+ *            id counts.  With offsets == NULL bag (t, b) is {ids[t*B + b]}:
+ *            the transpose of the sample-major id matrix of Algorithm 1.
+ *            Ids outside [0, num_rows) contribute nothing and latch
+ *            DPI_ERR_BAD_ID.
+ *   tables:  host array [T] of device pointers, 16-byte aligned.
+ *   out:     device [B][sum_t dim_t] of the plan's out dtype; field t
+ *            occupies columns [col_base[t], col_base[t+1]), col_base the
+ *            exclusive prefix of the dims.  Every element is written.
+ */
+#ifndef DPI_H
+#define DPI_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DPI_ABI_VERSION 1
+#define DPI_MAX_TABLES 256      /* fields per plan */
+#define DPI_MAX_DIM 65536       /* elements per row */
+
+typedef enum {
+  DPI_OK = 0,
+  DPI_ERR_INVALID_ARG = 1,         /* null pointer, negative size, bad enum, table count */
+  DPI_ERR_UNSUPPORTED = 2,         /* dim * element size not a multiple of 4 bytes, dim too large */
+  DPI_ERR_MISALIGNED = 3,          /* table, out or workspace not 16-byte aligned */
+  DPI_ERR_WORKSPACE_TOO_SMALL = 4,
+  DPI_ERR_BAD_OFFSETS = 5,         /* offsets[t][0] != 0, decreasing, or ids != total_ids */
+  DPI_ERR_BAD_ID = 6,              /* an id outside [0, num_rows) was met by a lookup */
+  DPI_ERR_HIP = 7                  /* HIP runtime error; text in dpi_last_error() */
+} dpi_status;
+
+typedef enum { DPI_F32 = 0, DPI_F16 = 1 } dpi_dtype;
+typedef enum { DPI_POOL_SUM = 0, DPI_POOL_MEAN = 1 } dpi_pooling;
+
+/* plan flags */
+enum {
+  DPI_FLAG_EXACT_SPLIT = 1u << 1,  /* never move a wave boundary to a bag's end (many split bags) */
+  DPI_FLAG_XCD_AFFINE = 1u << 2    /* give each XCD a contiguous range of waves */
+};
+
+typedef struct {
+  int64_t num_rows;  /* rows of the table (ids must lie in [0, num_rows)) */
+  int32_t dim;       /* elements per row, 1..DPI_MAX_DIM */
+  int32_t dtype;     /* dpi_dtype of the table */
+} dpi_table_meta;
+
+typedef struct {
+  int32_t chunk_rows;   /* C: rows per work item; 0 -> 32 */
+  int32_t item_cost_k;  /* K: fixed cost per work item; 0 -> 64 */
+  int64_t num_waves;    /* requested waves; 0 -> dpi_default_waves(...) */
+  int32_t out_dtype;    /* dpi_dtype of the output */
+  uint32_t flags;       /* DPI_FLAG_* */
+} dpi_plan_opts;
+
+typedef struct dpi_plan_s* dpi_plan_t;
+
+/*
+ * Default wave count for a batch: max(8 * compute units of the current
+ * device, ceil((total_ids + T*B) / 512)).  The plan uses
+ * W = min(requested, number of work items).
+ */
+int64_t dpi_default_waves(int32_t num_tables, int64_t batch, int64_t total_ids);
+
+/*
+ * Bytes of device workspace dpi_plan needs for these sizes (0 on invalid
+ * arguments).  max_dim is the largest dim over the fields.
+ */
+size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total_ids,
+                                int32_t max_dim, const dpi_plan_opts* opts);
+
+/*
+ * Build the work plan of one batch (§III opportunity 2, §IV-B, §IV-C):
+ * the bags' item counts and costs, their exclusive prefix sums over all
+ * fields (field-major), and a partition of the items into W waves of nearly
+ * equal cost.  The plan's arrays are defined step by step in the oracle's
+ * documentation and exported by dpi_plan_export.
+ *   table_meta: host [num_tables]; offsets: device [T][B+1] or NULL;
+ *   total_ids:  number of ids (sum of offsets[t][B], or T*B);
+ *   opts:       NULL for defaults;
+ *   workspace:  device, 16-byte aligned, >= dpi_plan_workspace_bytes(...);
+ *   stream:     hipStream_t or NULL;  plan_out: receives the plan handle.
+ * Errors: INVALID_ARG, UNSUPPORTED, MISALIGNED, WORKSPACE_TOO_SMALL, HIP
+ * synchronously; BAD_OFFSETS later through dpi_plan_sync_status.
+ */
+dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const int32_t* offsets,
+                    int64_t batch, int64_t total_ids, const dpi_plan_opts* opts, void* workspace,
+                    size_t workspace_bytes, void* stream, dpi_plan_t* plan_out);
+
+/*
+ * Fused gather-pool of every field's bags into `out` (Algorithm 1 of §IV-B
+ * generalised to bags, heterogeneous dims and pooling; lanes of a wavefront
+ * cover the contiguous columns of one row, the output-first allocation of
+ * §IV-C).
+ *   tables:  host [T] of device pointers (16-byte aligned);
+ *   ids, offsets: the batch the plan was built from (same contents);
+ *   pooling: host [T] of dpi_pooling, NULL = all sum;
+ *   out:     device [B][sum dim] of the plan's out dtype.
+ * A plan whose offsets were rejected on the device makes the lookup a no-op.
+ */
+dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids,
+                      const int32_t* offsets, const int32_t* pooling, void* out, void* stream);
+
+/* Synchronize the plan's stream and report device-detected errors
+ * (BAD_OFFSETS before BAD_ID).  Lookups on other streams must be
+ * synchronized by the caller first. */
+dpi_status dpi_plan_sync_status(dpi_plan_t plan);
+
+/*
+ * Copy the plan to host arrays (synchronizes the plan's stream).  Any
+ * pointer may be NULL.  Sizes: header16[16], col_base[T+1], id_base[T+1],
+ * bag_item_base[T*B+1], bag_cost_base[T*B+1], wave_item_begin[W+1] with W =
+ * header16[3].  header16 = [abi, T, B, W, C, K, out_dtype, flags, total_dim,
+ * items N, total cost S, total_ids, split bags, requested waves, 0, 0].
+ */
+dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
+                           int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);
+
+/* Free the host object (not the workspace).  NULL is ignored. */
+void dpi_plan_destroy(dpi_plan_t plan);
+
+const char* dpi_status_str(dpi_status s);
+const char* dpi_last_error(void);   /* thread-local detail of the last error */
+int dpi_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DPI_H */

@@ -1,0 +1,394 @@
+// Host side of the C ABI declared in include/dpi.h: argument validation,
+// workspace layout, kernel launches on the caller's stream, plan export.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+
+#include "dpi_internal.h"
+
+using namespace dpi;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+dpi_status fail(dpi_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+dpi_status hip_fail(hipError_t e, const char* what) {
+  return fail(DPI_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+struct Layout {
+  size_t hdr, status, tinfo, col_base, id_base, block_sum, block_pre, bib, bcb, wib, wave_bag, head_first,
+      split_pieces, split_last, tickets, partial, total;
+};
+
+Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
+  Layout L{};
+  const int64_t TB = T * B;
+  const int64_t nblk = (TB + kScanTile - 1) / kScanTile;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align256(off + bytes);
+    return at;
+  };
+  L.hdr = take(16 * sizeof(int64_t));
+  L.status = take(sizeof(int32_t));
+  L.tinfo = take(T * sizeof(TableInfo));
+  L.col_base = take((T + 1) * sizeof(int64_t));
+  L.id_base = take((T + 1) * sizeof(int64_t));
+  L.block_sum = take(2 * std::max<int64_t>(nblk, 1) * sizeof(int64_t));
+  L.block_pre = take(2 * std::max<int64_t>(nblk, 1) * sizeof(int64_t));
+  L.bib = take((TB + 1) * sizeof(int64_t));
+  L.bcb = take((TB + 1) * sizeof(int64_t));
+  L.wib = take((waves_req + 1) * sizeof(int64_t));
+  L.wave_bag = take((waves_req + 1) * sizeof(int64_t));
+  L.head_first = take(waves_req * sizeof(int32_t));
+  L.split_pieces = take(waves_req * sizeof(int32_t));
+  L.split_last = take(waves_req * sizeof(int32_t));
+  L.tickets = take(waves_req * sizeof(int32_t));
+  L.partial = take(2 * waves_req * dmax * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 256;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+int ilog2(int x) {
+  int l = 0;
+  while ((1 << l) < x) ++l;
+  return l;
+}
+
+}  // namespace
+
+struct dpi_plan_s {
+  int32_t T;
+  int64_t B;
+  int64_t total_ids;
+  int64_t waves_req;
+  int32_t C, K, out_dtype;
+  uint32_t flags;
+  int32_t dmax;
+  int64_t total_d;
+  bool onehot;
+  hipStream_t stream;
+  char* ws;
+  Layout layout;
+  int32_t row_class[DPI_MAX_TABLES];
+};
+
+extern "C" {
+
+int dpi_abi_version(void) { return DPI_ABI_VERSION; }
+
+const char* dpi_last_error(void) { return g_last_error; }
+
+const char* dpi_status_str(dpi_status s) {
+  switch (s) {
+    case DPI_OK: return "ok";
+    case DPI_ERR_INVALID_ARG: return "invalid argument";
+    case DPI_ERR_UNSUPPORTED: return "unsupported table shape";
+    case DPI_ERR_MISALIGNED: return "misaligned pointer";
+    case DPI_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case DPI_ERR_BAD_OFFSETS: return "malformed offsets";
+    case DPI_ERR_BAD_ID: return "id out of range";
+    case DPI_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int64_t dpi_default_waves(int32_t num_tables, int64_t batch, int64_t total_ids) {
+  const int64_t units = total_ids + (int64_t)num_tables * batch;
+  const int64_t by_work = (units + kDefaultRowsPerWave - 1) / kDefaultRowsPerWave;
+  return std::max<int64_t>((int64_t)kDefaultWavesPerCU * device_cus(), by_work);
+}
+
+static dpi_status resolve_opts(const dpi_plan_opts* opts, int32_t T, int64_t B, int64_t total_ids,
+                               dpi_plan_opts& o) {
+  o = dpi_plan_opts{};
+  if (opts) o = *opts;
+  if (o.chunk_rows < 0 || o.item_cost_k < 0 || o.num_waves < 0)
+    return fail(DPI_ERR_INVALID_ARG, "negative plan option");
+  if (o.out_dtype != DPI_F32 && o.out_dtype != DPI_F16) return fail(DPI_ERR_INVALID_ARG, "bad out_dtype");
+  if (o.flags & ~(uint32_t)(DPI_FLAG_EXACT_SPLIT | DPI_FLAG_XCD_AFFINE))
+    return fail(DPI_ERR_INVALID_ARG, "unknown flag bits 0x%x", o.flags);
+  if (o.chunk_rows == 0) o.chunk_rows = kDefaultChunkRows;
+  if (o.item_cost_k == 0) o.item_cost_k = kDefaultItemCost;
+  if (o.num_waves == 0) o.num_waves = dpi_default_waves(T, B, total_ids);
+  if (o.num_waves > ((int64_t)1 << 31) - 2) return fail(DPI_ERR_UNSUPPORTED, "too many waves");
+  return DPI_OK;
+}
+
+size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total_ids, int32_t max_dim,
+                                const dpi_plan_opts* opts) {
+  if (num_tables < 1 || num_tables > DPI_MAX_TABLES || batch < 0 || total_ids < 0 || max_dim < 1 ||
+      max_dim > DPI_MAX_DIM)
+    return 0;
+  dpi_plan_opts o;
+  if (resolve_opts(opts, num_tables, batch, total_ids, o) != DPI_OK) return 0;
+  return make_layout(num_tables, batch, o.num_waves, max_dim).total;
+}
+
+dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const int32_t* offsets, int64_t batch,
+                    int64_t total_ids, const dpi_plan_opts* opts, void* workspace, size_t workspace_bytes,
+                    void* stream, dpi_plan_t* plan_out) {
+  if (!plan_out) return fail(DPI_ERR_INVALID_ARG, "plan_out is NULL");
+  *plan_out = nullptr;
+  if (!table_meta) return fail(DPI_ERR_INVALID_ARG, "table_meta is NULL");
+  if (num_tables < 1 || num_tables > DPI_MAX_TABLES)
+    return fail(DPI_ERR_INVALID_ARG, "num_tables %d outside [1, %d]", num_tables, DPI_MAX_TABLES);
+  if (batch < 0) return fail(DPI_ERR_INVALID_ARG, "negative batch");
+  if (batch > ((int64_t)1 << 31) - 2) return fail(DPI_ERR_UNSUPPORTED, "batch too large");
+  if (total_ids < 0) return fail(DPI_ERR_INVALID_ARG, "negative total_ids");
+  if (!offsets && total_ids != (int64_t)num_tables * batch)
+    return fail(DPI_ERR_INVALID_ARG, "one-hot batch needs total_ids == T*B");
+  if (offsets && (reinterpret_cast<uintptr_t>(offsets) & 3))
+    return fail(DPI_ERR_MISALIGNED, "offsets not 4-byte aligned");
+  dpi_plan_opts o;
+  dpi_status st = resolve_opts(opts, num_tables, batch, total_ids, o);
+  if (st != DPI_OK) return st;
+  const int osize = o.out_dtype == DPI_F16 ? 2 : 4;
+
+  int64_t col = 0;
+  int32_t dmax = 1;
+  MetaChunk chunk[(DPI_MAX_TABLES + kMetaChunk - 1) / kMetaChunk];
+  int32_t row_class[DPI_MAX_TABLES];
+  for (int t = 0; t < num_tables; ++t) {
+    const dpi_table_meta& m = table_meta[t];
+    if (m.dtype != DPI_F32 && m.dtype != DPI_F16) return fail(DPI_ERR_INVALID_ARG, "table %d: bad dtype", t);
+    if (m.dim < 1) return fail(DPI_ERR_INVALID_ARG, "table %d: dim < 1", t);
+    if (m.dim > DPI_MAX_DIM) return fail(DPI_ERR_UNSUPPORTED, "table %d: dim > %d", t, DPI_MAX_DIM);
+    if (m.num_rows < 0) return fail(DPI_ERR_INVALID_ARG, "table %d: negative num_rows", t);
+    const int esize = m.dtype == DPI_F16 ? 2 : 4;
+    const int64_t row_bytes = (int64_t)m.dim * esize;
+    if (row_bytes % 4) return fail(DPI_ERR_UNSUPPORTED, "table %d: row of %lld bytes is not a multiple of 4", t,
+                                   (long long)row_bytes);
+    int flags = m.dtype == DPI_F16 ? kTiF16 : 0;
+    if (row_bytes % 16 == 0 && row_bytes <= 1024) {
+      flags |= kTiFast;
+      flags |= ilog2((int)(row_bytes / 16)) << kTiLprShift;
+    }
+    row_class[t] = flags;
+    MetaChunk& c = chunk[t / kMetaChunk];
+    c.num_rows[t % kMetaChunk] = m.num_rows;
+    c.dim[t % kMetaChunk] = m.dim;
+    c.col_base[t % kMetaChunk] = (int32_t)col;
+    col += m.dim;
+    if (col > ((int64_t)1 << 31) - 1) return fail(DPI_ERR_UNSUPPORTED, "sum of dims too large");
+    dmax = std::max(dmax, m.dim);
+  }
+  const int64_t total_d = col;
+  // vector stores need every output row piece aligned to min(16, bytes per lane)
+  for (int t = 0; t < num_tables; ++t) {
+    MetaChunk& c = chunk[t / kMetaChunk];
+    int flags = row_class[t];
+    if (flags & kTiFast) {
+      const int epl = (flags & kTiF16) ? 8 : 4;
+      const int64_t a = std::min(16, epl * osize);
+      if ((total_d * osize) % a == 0 && ((int64_t)c.col_base[t % kMetaChunk] * osize) % a == 0)
+        flags |= kTiOutVec;
+    }
+    c.flags[t % kMetaChunk] = flags;
+    row_class[t] = flags;
+  }
+
+  const Layout L = make_layout(num_tables, batch, o.num_waves, dmax);
+  if (!workspace) return fail(DPI_ERR_INVALID_ARG, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) & 15) return fail(DPI_ERR_MISALIGNED, "workspace not 16-byte aligned");
+  if (workspace_bytes < L.total)
+    return fail(DPI_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, L.total);
+
+  dpi_plan_s* plan = new (std::nothrow) dpi_plan_s{};
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "out of host memory");
+  plan->T = num_tables;
+  plan->B = batch;
+  plan->total_ids = total_ids;
+  plan->waves_req = o.num_waves;
+  plan->C = o.chunk_rows;
+  plan->K = o.item_cost_k;
+  plan->out_dtype = o.out_dtype;
+  plan->flags = o.flags;
+  plan->dmax = dmax;
+  plan->total_d = total_d;
+  plan->onehot = offsets == nullptr;
+  plan->stream = reinterpret_cast<hipStream_t>(stream);
+  plan->ws = reinterpret_cast<char*>(workspace);
+  plan->layout = L;
+  std::memcpy(plan->row_class, row_class, sizeof(int32_t) * num_tables);
+
+  char* ws = plan->ws;
+  PlanDev d;
+  d.hdr = reinterpret_cast<int64_t*>(ws + L.hdr);
+  d.status = reinterpret_cast<int32_t*>(ws + L.status);
+  d.tinfo = reinterpret_cast<TableInfo*>(ws + L.tinfo);
+  d.col_base = reinterpret_cast<int64_t*>(ws + L.col_base);
+  d.id_base = reinterpret_cast<int64_t*>(ws + L.id_base);
+  d.block_sum = reinterpret_cast<int64_t*>(ws + L.block_sum);
+  d.block_pre = reinterpret_cast<int64_t*>(ws + L.block_pre);
+  d.bib = reinterpret_cast<int64_t*>(ws + L.bib);
+  d.bcb = reinterpret_cast<int64_t*>(ws + L.bcb);
+  d.wib = reinterpret_cast<int64_t*>(ws + L.wib);
+  d.wave_bag = reinterpret_cast<int64_t*>(ws + L.wave_bag);
+  d.head_first = reinterpret_cast<int32_t*>(ws + L.head_first);
+  d.split_pieces = reinterpret_cast<int32_t*>(ws + L.split_pieces);
+  d.split_last = reinterpret_cast<int32_t*>(ws + L.split_last);
+  d.tickets = reinterpret_cast<int32_t*>(ws + L.tickets);
+  d.partial = reinterpret_cast<float*>(ws + L.partial);
+
+  PlanParams p;
+  p.T = num_tables;
+  p.C = o.chunk_rows;
+  p.K = o.item_cost_k;
+  p.out_dtype = o.out_dtype;
+  p.flags = o.flags;
+  p.B = batch;
+  p.TB = (int64_t)num_tables * batch;
+  p.nblk = (int32_t)((p.TB + kScanTile - 1) / kScanTile);
+  p.total_ids = total_ids;
+  p.waves_req = o.num_waves;
+  p.total_d = total_d;
+  p.offsets = offsets;
+
+  hipStream_t s = plan->stream;
+  hipError_t e;
+  for (int first = 0; first < num_tables; first += kMetaChunk) {
+    const int count = std::min(kMetaChunk, num_tables - first);
+    e = launch_plan_meta(chunk[first / kMetaChunk], first, count, d, first == 0, osize, s);
+    if (e != hipSuccess) {
+      delete plan;
+      return hip_fail(e, "plan_meta launch");
+    }
+  }
+  if (p.TB > 0) {
+    e = launch_plan_reduce(p, d, s);
+    if (e != hipSuccess) {
+      delete plan;
+      return hip_fail(e, "plan_reduce launch");
+    }
+  }
+  e = launch_plan_totals(p, d, s);
+  if (e != hipSuccess) {
+    delete plan;
+    return hip_fail(e, "plan_totals launch");
+  }
+  if (p.TB > 0) {
+    e = launch_plan_scan_partition(p, d, s);
+    if (e != hipSuccess) {
+      delete plan;
+      return hip_fail(e, "plan_scan_partition launch");
+    }
+  }
+  *plan_out = plan;
+  return DPI_OK;
+}
+
+dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids, const int32_t* offsets,
+                      const int32_t* pooling, void* out, void* stream) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  if (!tables) return fail(DPI_ERR_INVALID_ARG, "tables is NULL");
+  if ((offsets == nullptr) != plan->onehot)
+    return fail(DPI_ERR_INVALID_ARG, "offsets must be NULL exactly when the plan was built without offsets");
+  if (plan->total_ids > 0 && !ids) return fail(DPI_ERR_INVALID_ARG, "ids is NULL");
+  if (ids && (reinterpret_cast<uintptr_t>(ids) & 3)) return fail(DPI_ERR_MISALIGNED, "ids not 4-byte aligned");
+  if (plan->B > 0 && !out) return fail(DPI_ERR_INVALID_ARG, "out is NULL");
+  LookupArgs a{};
+  for (int t = 0; t < plan->T; ++t) {
+    if (!tables[t]) return fail(DPI_ERR_INVALID_ARG, "tables[%d] is NULL", t);
+    if (reinterpret_cast<uintptr_t>(tables[t]) & 15) return fail(DPI_ERR_MISALIGNED, "tables[%d] not 16-byte aligned", t);
+    a.tables[t] = tables[t];
+    const int32_t pm = pooling ? pooling[t] : DPI_POOL_SUM;
+    if (pm != DPI_POOL_SUM && pm != DPI_POOL_MEAN) return fail(DPI_ERR_INVALID_ARG, "pooling[%d] invalid", t);
+    if (pm == DPI_POOL_MEAN) a.mean_bits[t >> 5] |= 1u << (t & 31);
+  }
+  if (out && (reinterpret_cast<uintptr_t>(out) & 15)) return fail(DPI_ERR_MISALIGNED, "out not 16-byte aligned");
+  if (plan->B == 0 || plan->waves_req == 0) return DPI_OK;
+  const Layout& L = plan->layout;
+  char* ws = plan->ws;
+  a.ids = ids;
+  a.offsets = offsets;
+  a.out = out;
+  a.hdr = reinterpret_cast<const int64_t*>(ws + L.hdr);
+  a.status = reinterpret_cast<int32_t*>(ws + L.status);
+  a.tinfo = reinterpret_cast<const TableInfo*>(ws + L.tinfo);
+  a.bib = reinterpret_cast<const int64_t*>(ws + L.bib);
+  a.wib = reinterpret_cast<const int64_t*>(ws + L.wib);
+  a.wave_bag = reinterpret_cast<const int64_t*>(ws + L.wave_bag);
+  a.head_first = reinterpret_cast<const int32_t*>(ws + L.head_first);
+  a.split_pieces = reinterpret_cast<const int32_t*>(ws + L.split_pieces);
+  a.split_last = reinterpret_cast<const int32_t*>(ws + L.split_last);
+  a.tickets = reinterpret_cast<int32_t*>(ws + L.tickets);
+  a.partial = reinterpret_cast<float*>(ws + L.partial);
+  a.B = plan->B;
+  a.total_d = plan->total_d;
+  a.T = plan->T;
+  a.C = plan->C;
+  a.dmax = plan->dmax;
+  a.out_f16 = plan->out_dtype == DPI_F16;
+  a.xcd_affine = (plan->flags & DPI_FLAG_XCD_AFFINE) ? 1 : 0;
+  a.grid_waves = plan->waves_req;
+  const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "lookup launch");
+  return DPI_OK;
+}
+
+dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  hipError_t e = hipStreamSynchronize(plan->stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  int32_t status = 0;
+  e = hipMemcpy(&status, plan->ws + plan->layout.status, sizeof(status), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+  if (status & kStatusBadOffsets) return fail(DPI_ERR_BAD_OFFSETS, "device rejected the offsets");
+  if (status & kStatusBadId) return fail(DPI_ERR_BAD_ID, "a lookup met an id outside its table");
+  return DPI_OK;
+}
+
+dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
+                           int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  hipError_t e = hipStreamSynchronize(plan->stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  const Layout& L = plan->layout;
+  int64_t hdr[16];
+  e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy header");
+  const int64_t T = plan->T, TB = (int64_t)plan->T * plan->B, W = hdr[kHdrW];
+  struct Part {
+    int64_t* dst;
+    size_t off;
+    int64_t count;
+  } parts[] = {{col_base, L.col_base, T + 1},       {id_base, L.id_base, T + 1},
+               {bag_item_base, L.bib, TB + 1},      {bag_cost_base, L.bcb, TB + 1},
+               {wave_item_begin, L.wib, W + 1}};
+  for (const Part& p : parts) {
+    if (!p.dst) continue;
+    e = hipMemcpy(p.dst, plan->ws + p.off, p.count * sizeof(int64_t), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy plan array");
+  }
+  if (header16) std::memcpy(header16, hdr, sizeof(hdr));
+  return DPI_OK;
+}
+
+void dpi_plan_destroy(dpi_plan_t plan) { delete plan; }
+
+}  // extern "C"

@@ -1,0 +1,131 @@
+// Internal definitions shared by the host API and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dpi.h"
+
+namespace dpi {
+
+constexpr int kWaveSize = 64;
+constexpr int kBlockThreads = 256;          // 4 independent waves per workgroup
+constexpr int kWavesPerBlock = kBlockThreads / kWaveSize;
+constexpr int kScanThreads = 256;           // plan scan: threads per block
+constexpr int kScanPerThread = 8;           // bags per thread
+constexpr int kScanTile = kScanThreads * kScanPerThread;
+constexpr int kMetaChunk = 64;              // tables per meta-upload launch
+constexpr int kDefaultChunkRows = 32;
+constexpr int kDefaultItemCost = 64;
+constexpr int kDefaultRowsPerWave = 512;
+constexpr int kDefaultWavesPerCU = 8;
+
+// status word bits (device-latched errors)
+constexpr int kStatusBadOffsets = 1;
+constexpr int kStatusBadId = 2;
+
+// header16 slots
+enum : int {
+  kHdrAbi = 0, kHdrT, kHdrB, kHdrW, kHdrC, kHdrK, kHdrOutDtype, kHdrFlags, kHdrTotalD,
+  kHdrItems, kHdrCost, kHdrTotalIds, kHdrSplit, kHdrWaveReq
+};
+
+// TableInfo.flags
+constexpr int kTiF16 = 1 << 0;              // table dtype is binary16
+constexpr int kTiFast = 1 << 1;             // row bytes multiple of 16 and <= 1024
+constexpr int kTiLprShift = 2;              // log2(lanes per row), 3 bits
+constexpr int kTiOutVec = 1 << 5;           // output rows allow vector stores
+
+// Static description of a field, written to the workspace by the plan.
+struct alignas(16) TableInfo {
+  int64_t num_rows;
+  int64_t id_base;     // first position of the field's ids
+  int64_t nnz;         // number of ids of the field
+  int32_t dim;
+  int32_t col_base;
+  int32_t row_bytes;
+  int32_t out_bytes;
+  int32_t flags;
+  int32_t pad;
+};
+
+// Host-side upload of up to kMetaChunk fields.
+struct MetaChunk {
+  int64_t num_rows[kMetaChunk];
+  int32_t dim[kMetaChunk];
+  int32_t col_base[kMetaChunk];
+  int32_t flags[kMetaChunk];
+};
+
+// Device pointers of a plan inside the caller's workspace.
+struct PlanDev {
+  int64_t* hdr;          // [16]
+  int32_t* status;       // [1]
+  TableInfo* tinfo;      // [T]
+  int64_t* col_base;     // [T+1]
+  int64_t* id_base;      // [T+1]
+  int64_t* block_sum;    // [2 * nblk]  (items, cost) per scan tile
+  int64_t* block_pre;    // [2 * nblk]  exclusive prefix of block_sum
+  int64_t* bib;          // bag_item_base [TB+1]
+  int64_t* bcb;          // bag_cost_base [TB+1]
+  int64_t* wib;          // wave_item_begin [Wreq+1]
+  int64_t* wave_bag;     // bag holding wib[w], [Wreq+1]
+  int32_t* head_first;   // [Wreq] first wave of the bag this wave starts inside, or -1
+  int32_t* split_pieces; // [Wreq] for the first wave of a split bag: nonempty waves covering it
+  int32_t* split_last;   // [Wreq] ... and the last of them
+  int32_t* tickets;      // [Wreq] arrival counters of split bags (zero between lookups)
+  float* partial;        // [2 * Wreq][dmax] fp32 partial sums of split bags
+};
+
+struct PlanParams {
+  int32_t T;
+  int32_t C;
+  int32_t K;
+  int32_t out_dtype;
+  uint32_t flags;
+  int32_t nblk;
+  int64_t B;
+  int64_t TB;
+  int64_t total_ids;
+  int64_t waves_req;
+  int64_t total_d;
+  const int32_t* offsets;  // device [T][B+1] or nullptr
+};
+
+struct LookupArgs {
+  const void* tables[DPI_MAX_TABLES];
+  uint32_t mean_bits[DPI_MAX_TABLES / 32];
+  const int32_t* ids;
+  const int32_t* offsets;
+  void* out;
+  const int64_t* hdr;
+  int32_t* status;
+  const TableInfo* tinfo;
+  const int64_t* bib;
+  const int64_t* wib;
+  const int64_t* wave_bag;
+  const int32_t* head_first;
+  const int32_t* split_pieces;
+  const int32_t* split_last;
+  int32_t* tickets;
+  float* partial;
+  int64_t B;
+  int64_t total_d;
+  int32_t T;
+  int32_t C;
+  int32_t dmax;
+  int32_t out_f16;
+  int32_t xcd_affine;
+  int32_t pad;
+  int64_t grid_waves;
+};
+
+// kernel launchers (plan.hip / lookup.hip); return the launch's hipError_t
+hipError_t launch_plan_meta(const MetaChunk& chunk, int first, int count, const PlanDev& d,
+                            bool clear_status, int osize, hipStream_t s);
+hipError_t launch_plan_reduce(const PlanParams& p, const PlanDev& d, hipStream_t s);
+hipError_t launch_plan_totals(const PlanParams& p, const PlanDev& d, hipStream_t s);
+hipError_t launch_plan_scan_partition(const PlanParams& p, const PlanDev& d, hipStream_t s);
+hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
+
+}  // namespace dpi

@@ -1,0 +1,209 @@
+"""Python binding of the C ABI in include/dpi.h (ctypes; argument marshalling only).
+
+Every step of the lookup runs in libdpi.so's HIP kernels.  torch tensors are
+accepted wherever the ABI takes device memory: only their data pointers are
+passed.  There is no fallback: if the library is not built, loading fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+
+from .build import LIB
+
+DPI_OK = 0
+DPI_ERR_INVALID_ARG = 1
+DPI_ERR_UNSUPPORTED = 2
+DPI_ERR_MISALIGNED = 3
+DPI_ERR_WORKSPACE_TOO_SMALL = 4
+DPI_ERR_BAD_OFFSETS = 5
+DPI_ERR_BAD_ID = 6
+DPI_ERR_HIP = 7
+
+DPI_F32 = 0
+DPI_F16 = 1
+DPI_POOL_SUM = 0
+DPI_POOL_MEAN = 1
+DPI_FLAG_EXACT_SPLIT = 1 << 1
+DPI_FLAG_XCD_AFFINE = 1 << 2
+DPI_MAX_TABLES = 256
+
+
+class dpi_table_meta(ctypes.Structure):
+    _fields_ = [("num_rows", ctypes.c_int64), ("dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class dpi_plan_opts(ctypes.Structure):
+    _fields_ = [("chunk_rows", ctypes.c_int32), ("item_cost_k", ctypes.c_int32), ("num_waves", ctypes.c_int64),
+                ("out_dtype", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+class DpiError(RuntimeError):
+    def __init__(self, status: int, detail: str = ""):
+        self.status = status
+        super().__init__(f"{dpi_status_str(status)} ({status}): {detail}")
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load the in-tree libdpi.so; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB):
+        raise ImportError(f"{LIB} is missing: build it with __graft_entry__.build() "
+                          "(hipcc --offload-arch=gfx950); there is no CPU fallback")
+    lib = ctypes.CDLL(LIB)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.dpi_abi_version.restype = ctypes.c_int
+    lib.dpi_last_error.restype = ctypes.c_char_p
+    lib.dpi_status_str.restype = ctypes.c_char_p
+    lib.dpi_status_str.argtypes = [ctypes.c_int]
+    lib.dpi_default_waves.restype = i64
+    lib.dpi_default_waves.argtypes = [i32, i64, i64]
+    lib.dpi_plan_workspace_bytes.restype = sz
+    lib.dpi_plan_workspace_bytes.argtypes = [i32, i64, i64, i32, ctypes.POINTER(dpi_plan_opts)]
+    lib.dpi_plan.restype = ctypes.c_int
+    lib.dpi_plan.argtypes = [ctypes.POINTER(dpi_table_meta), i32, vp, i64, i64, ctypes.POINTER(dpi_plan_opts),
+                             vp, sz, vp, ctypes.POINTER(vp)]
+    lib.dpi_lookup.restype = ctypes.c_int
+    lib.dpi_lookup.argtypes = [vp, ctypes.POINTER(vp), vp, vp, ctypes.POINTER(i32), vp, vp]
+    lib.dpi_plan_sync_status.restype = ctypes.c_int
+    lib.dpi_plan_sync_status.argtypes = [vp]
+    p64 = ctypes.POINTER(i64)
+    lib.dpi_plan_export.restype = ctypes.c_int
+    lib.dpi_plan_export.argtypes = [vp, p64, p64, p64, p64, p64, p64]
+    lib.dpi_plan_destroy.restype = None
+    lib.dpi_plan_destroy.argtypes = [vp]
+    _lib = lib
+    return lib
+
+
+def _ptr(x) -> Optional[int]:
+    """Device (or host) address of a tensor, an int address, or None."""
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return int(x.data_ptr())
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return None
+    if isinstance(stream, int):
+        return stream
+    return int(stream.cuda_stream)
+
+
+def _check(status: int):
+    if status != DPI_OK:
+        raise DpiError(status, dpi_last_error())
+
+
+def dpi_abi_version() -> int:
+    return load().dpi_abi_version()
+
+
+def dpi_last_error() -> str:
+    return load().dpi_last_error().decode()
+
+
+def dpi_status_str(status: int) -> str:
+    return load().dpi_status_str(int(status)).decode()
+
+
+def dpi_default_waves(num_tables: int, batch: int, total_ids: int) -> int:
+    return int(load().dpi_default_waves(num_tables, batch, total_ids))
+
+
+def make_opts(chunk_rows: int = 0, item_cost_k: int = 0, num_waves: int = 0, out_dtype: int = DPI_F32,
+              flags: int = 0) -> dpi_plan_opts:
+    return dpi_plan_opts(chunk_rows, item_cost_k, num_waves, out_dtype, flags)
+
+
+def make_meta(num_rows: Sequence[int], dims: Sequence[int], dtypes: Sequence[int]):
+    T = len(dims)
+    arr = (dpi_table_meta * T)()
+    for t in range(T):
+        arr[t] = dpi_table_meta(int(num_rows[t]), int(dims[t]), int(dtypes[t]))
+    return arr
+
+
+def dpi_plan_workspace_bytes(num_tables: int, batch: int, total_ids: int, max_dim: int,
+                             opts: Optional[dpi_plan_opts] = None) -> int:
+    o = ctypes.byref(opts) if opts is not None else None
+    return int(load().dpi_plan_workspace_bytes(num_tables, batch, total_ids, max_dim, o))
+
+
+@dataclass
+class Plan:
+    """Handle of a device plan; keeps the borrowed buffers alive."""
+    handle: int
+    num_tables: int
+    batch: int
+    keep: tuple
+
+    def __del__(self):
+        if self.handle and _lib is not None:
+            _lib.dpi_plan_destroy(ctypes.c_void_p(self.handle))
+            self.handle = 0
+
+
+def dpi_plan(table_meta, offsets, batch: int, total_ids: int, opts: Optional[dpi_plan_opts], workspace,
+             workspace_bytes: Optional[int] = None, stream=None) -> Plan:
+    lib = load()
+    T = len(table_meta)
+    if workspace_bytes is None:
+        workspace_bytes = int(workspace.numel() * workspace.element_size())
+    out = ctypes.c_void_p()
+    st = lib.dpi_plan(table_meta, T, _ptr(offsets), batch, total_ids,
+                      ctypes.byref(opts) if opts is not None else None, _ptr(workspace), workspace_bytes,
+                      _stream(stream), ctypes.byref(out))
+    _check(st)
+    return Plan(out.value, T, batch, (workspace, offsets, table_meta))
+
+
+def dpi_lookup(plan: Plan, tables, ids, offsets, pooling: Optional[Sequence[int]], out, stream=None) -> None:
+    lib = load()
+    T = plan.num_tables
+    ptrs = (ctypes.c_void_p * T)(*[_ptr(t) for t in tables])
+    pool = None if pooling is None else (ctypes.c_int32 * T)(*[int(p) for p in pooling])
+    st = lib.dpi_lookup(ctypes.c_void_p(plan.handle), ptrs, _ptr(ids), _ptr(offsets), pool, _ptr(out),
+                        _stream(stream))
+    _check(st)
+
+
+def dpi_plan_sync_status(plan: Plan) -> int:
+    """Device-detected status (an int dpi_status; does not raise)."""
+    return int(load().dpi_plan_sync_status(ctypes.c_void_p(plan.handle)))
+
+
+def dpi_plan_export(plan: Plan) -> dict:
+    lib = load()
+    hdr = np.zeros(16, dtype=np.int64)
+    p64 = ctypes.POINTER(ctypes.c_int64)
+    _check(lib.dpi_plan_export(ctypes.c_void_p(plan.handle), hdr.ctypes.data_as(p64), None, None, None, None, None))
+    T, B, W = int(hdr[1]), int(hdr[2]), int(hdr[3])
+    col = np.zeros(T + 1, np.int64)
+    idb = np.zeros(T + 1, np.int64)
+    bib = np.zeros(T * B + 1, np.int64)
+    bcb = np.zeros(T * B + 1, np.int64)
+    wib = np.zeros(W + 1, np.int64)
+    _check(lib.dpi_plan_export(ctypes.c_void_p(plan.handle), hdr.ctypes.data_as(p64), col.ctypes.data_as(p64),
+                               idb.ctypes.data_as(p64), bib.ctypes.data_as(p64), bcb.ctypes.data_as(p64),
+                               wib.ctypes.data_as(p64)))
+    return {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib, "bag_cost_base": bcb,
+            "wave_item_begin": wib}
+
+
+def dpi_plan_destroy(plan: Plan) -> None:
+    if plan.handle:
+        load().dpi_plan_destroy(ctypes.c_void_p(plan.handle))
+        plan.handle = 0

@@ -1,0 +1,100 @@
+"""The C ABI library loads, exports every declared symbol and validates its
+host-visible arguments before touching the GPU (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_21101_amd import dpi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "dpi.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dpi_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    lib = dpi.load()
+    names = declared_functions()
+    assert len(names) >= 10
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_strings():
+    assert dpi.dpi_abi_version() == 1
+    for s in range(8):
+        assert dpi.dpi_status_str(s)
+    assert "unknown" in dpi.dpi_status_str(99)
+
+
+def _meta(dims=(16, 16), dtypes=(0, 0), rows=(10, 10)):
+    return dpi.make_meta(rows, dims, dtypes)
+
+
+def _plan(meta, T=None, offsets=None, B=4, total=None, opts=None, ws=0x10000, ws_bytes=1 << 30):
+    lib = dpi.load()
+    T = len(meta) if T is None else T
+    total = T * B if total is None else total
+    out = ctypes.c_void_p()
+    o = opts if opts is not None else dpi.make_opts(num_waves=64)
+    return lib.dpi_plan(meta, T, offsets, B, total, ctypes.byref(o), ws, ws_bytes, None, ctypes.byref(out))
+
+
+def test_plan_rejects_bad_arguments():
+    lib = dpi.load()
+    m = _meta()
+    assert lib.dpi_plan(m, 2, None, 4, 8, None, 0x10000, 1 << 30, None, None) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(None, T=2) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(m, T=0) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(_meta(dims=[4] * 257, dtypes=[0] * 257, rows=[1] * 257)) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(m, B=-1) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(m, total=7) == dpi.DPI_ERR_INVALID_ARG          # one-hot needs T*B ids
+    assert _plan(_meta(dtypes=(0, 2))) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(_meta(dims=(16, 0))) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(_meta(rows=(10, -1))) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(m, opts=dpi.make_opts(num_waves=64, out_dtype=3)) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(m, opts=dpi.make_opts(num_waves=64, flags=1 << 9)) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(m, opts=dpi.make_opts(chunk_rows=-1, num_waves=64)) == dpi.DPI_ERR_INVALID_ARG
+    assert "one-hot" in dpi.dpi_last_error() or dpi.dpi_last_error()
+
+
+def test_plan_rejects_unsupported_and_misaligned():
+    assert _plan(_meta(dims=(3, 16), dtypes=(1, 0))) == dpi.DPI_ERR_UNSUPPORTED   # 6-byte rows
+    assert _plan(_meta(dims=(70000, 16))) == dpi.DPI_ERR_UNSUPPORTED
+    assert _plan(_meta(), ws=0x10008) == dpi.DPI_ERR_MISALIGNED
+    assert _plan(_meta(), offsets=0x10002, total=3) == dpi.DPI_ERR_MISALIGNED
+    assert _plan(_meta(), ws=None) == dpi.DPI_ERR_INVALID_ARG
+    assert _plan(_meta(), ws_bytes=100) == dpi.DPI_ERR_WORKSPACE_TOO_SMALL
+    assert "need" in dpi.dpi_last_error()
+
+
+def test_workspace_size_query():
+    o = dpi.make_opts(num_waves=100)
+    a = dpi.dpi_plan_workspace_bytes(26, 16384, 4_000_000, 64, o)
+    b = dpi.dpi_plan_workspace_bytes(26, 16384, 4_000_000, 128, o)
+    assert 0 < a < b
+    assert dpi.dpi_plan_workspace_bytes(0, 1, 1, 16, o) == 0
+    assert dpi.dpi_plan_workspace_bytes(1, -1, 1, 16, o) == 0
+    assert dpi.dpi_plan_workspace_bytes(1, 1, 1, 0, o) == 0
+
+
+def test_lookup_rejects_null_plan_and_destroy_null():
+    lib = dpi.load()
+    ptrs = (ctypes.c_void_p * 1)(0x10000)
+    assert lib.dpi_lookup(None, ptrs, 0x10000, None, None, 0x10000, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_plan_sync_status(None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_plan_export(None, None, None, None, None, None, None) == dpi.DPI_ERR_INVALID_ARG
+    lib.dpi_plan_destroy(None)
+
+
+def test_default_waves_formula():
+    # max(8 * CUs, ceil((total_ids + T*B) / 512)); on a host without a GPU the
+    # CU count falls back to 256
+    w = dpi.dpi_default_waves(100, 65536, 176_805_878)
+    assert w == -(-(176_805_878 + 100 * 65536) // 512)
+    assert dpi.dpi_default_waves(8, 256, 2048) >= 2048

@@ -1,0 +1,135 @@
+"""Edge cases of the fused lookup on the GPU, each against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_21101_amd import dpi
+from paper_2606_21101_amd.lookup import FusedLookup
+from parity import check_outputs
+
+pytestmark = pytest.mark.gpu
+
+
+def random_problem(rng, dims, dtypes, B, max_len, rows=50, p_empty=0.1):
+    T = len(dims)
+    tables = []
+    for d, dt in zip(dims, dtypes):
+        v = rng.standard_normal((rows, d)) * 0.01
+        tables.append(v.astype(np.float16 if dt else np.float32))
+    lens = rng.integers(0, max_len + 1, size=(T, B))
+    lens[rng.random((T, B)) < p_empty] = 0
+    offs = np.zeros((T, B + 1), np.int32)
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    ids = np.concatenate([rng.integers(0, rows, size=int(offs[t, -1])) for t in range(T)]).astype(np.int32)
+    pool = [int(x) for x in rng.integers(0, 2, T)]
+    return tables, ids, offs, pool
+
+
+def run_case(tables, ids, offs, pool, B, out_dtype=torch.float32, **kw):
+    tt = [torch.from_numpy(t).cuda() for t in tables]
+    fl = FusedLookup(tt, pool, out_dtype, **{k: v for k, v in kw.items() if k in ("chunk_rows", "flags")})
+    ids_d = torch.from_numpy(ids).cuda()
+    offs_d = None if offs is None else torch.from_numpy(offs).cuda()
+    plan = fl.plan(offs_d, B, len(ids), num_waves=kw.get("num_waves", 0))
+    out = fl.lookup(plan, ids_d, offs_d)
+    st = dpi.dpi_plan_sync_status(plan)
+    return out, st, fl, plan
+
+
+def check(tables, ids, offs, pool, B, out, exact=False):
+    dims = [t.shape[1] for t in tables]
+    ref, mag = oracle.lookup(dims, tables, ids, offs, pool, B)
+    f16 = any(t.dtype == np.float16 for t in tables)
+    return check_outputs(out.double().cpu().numpy(), ref, mag, f16, out.dtype == torch.float16, exact=exact)
+
+
+@pytest.mark.parametrize("dims,dtypes", [
+    ([3, 5, 7], [0, 0, 0]),            # 12/20/28-byte rows: general path
+    ([6, 2, 10], [1, 1, 1]),           # fp16 rows of 12/4/20 bytes: general path
+    ([12, 48, 24], [0, 1, 1]),         # rows of 48/96/48 bytes: lanes rounded up to a power of two
+    ([300], [0]),                      # 1200-byte rows: several column passes
+    ([256, 512], [0, 1]),              # 1024-byte rows: 64 lanes per row
+    ([4, 8, 16, 32, 64, 128], [0, 1, 0, 1, 0, 1]),
+])
+def test_row_shapes(dims, dtypes):
+    rng = np.random.default_rng(sum(dims))
+    tables, ids, offs, pool = random_problem(rng, dims, dtypes, 37, 70)
+    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 53)):
+        for od in (torch.float32, torch.float16):
+            out, st, _, _ = run_case(tables, ids, offs, pool, 37, od, flags=flags, num_waves=W, chunk_rows=8)
+            assert st == dpi.DPI_OK
+            check(tables, ids, offs, pool, 37, out)
+
+
+def test_all_bags_empty_and_zero_batch():
+    rng = np.random.default_rng(1)
+    tables, _, _, pool = random_problem(rng, [16, 8], [0, 1], 20, 3)
+    offs = np.zeros((2, 21), np.int32)
+    ids = np.zeros(0, np.int32)
+    out, st, _, _ = run_case(tables, ids, offs, pool, 20)
+    assert st == dpi.DPI_OK
+    assert torch.all(out == 0)
+    out0, st0, _, _ = run_case(tables, ids, np.zeros((2, 1), np.int32), pool, 0)
+    assert st0 == dpi.DPI_OK and out0.shape == (0, 24)
+
+
+def test_single_long_bag_split_over_many_waves():
+    rng = np.random.default_rng(2)
+    tables, _, _, _ = random_problem(rng, [64], [1], 1, 1, rows=500)
+    ids = rng.integers(0, 500, size=256).astype(np.int32)
+    offs = np.array([[0, 256]], np.int32)
+    for pool in ([0], [1]):
+        for W, C in ((64, 4), (8, 32), (300, 1)):
+            out, st, fl, plan = run_case(tables, ids, offs, pool, 1, chunk_rows=C, num_waves=W,
+                                         flags=dpi.DPI_FLAG_EXACT_SPLIT)
+            hdr = dpi.dpi_plan_export(plan)["header"]
+            assert hdr[12] == 1              # the one bag is split
+            check(tables, ids, offs, pool, 1, out)
+
+
+def test_onehot_null_offsets_bit_exact():
+    rng = np.random.default_rng(4)
+    tables, _, _, pool = random_problem(rng, [16, 32, 8], [0, 0, 0], 300, 1)
+    ids = np.concatenate([rng.integers(0, 50, 300) for _ in range(3)]).astype(np.int32)
+    out, st, _, _ = run_case(tables, ids, None, pool, 300)
+    assert st == dpi.DPI_OK
+    check(tables, ids, None, pool, 300, out, exact=True)
+
+
+def test_out_of_range_ids_reported_and_skipped():
+    rng = np.random.default_rng(5)
+    tables, ids, offs, pool = random_problem(rng, [16, 8], [0, 0], 40, 6, p_empty=0.0)
+    bad_ids = ids.copy()
+    bad_ids[3] = -1
+    bad_ids[len(ids) - 2] = 50            # == num_rows
+    out, st, _, _ = run_case(tables, bad_ids, offs, pool, 40)
+    assert st == dpi.DPI_ERR_BAD_ID
+    # the oracle's view: out-of-range ids contribute nothing (its status is BAD_ID)
+    fixed = bad_ids.copy()
+    tables_z = [np.concatenate([t, np.zeros((1, t.shape[1]), t.dtype)]) for t in tables]
+    fixed[fixed < 0] = 50
+    ref, mag = oracle.lookup([16, 8], tables_z, fixed, offs, [0, 0], 40)
+    sums = out.double().cpu().numpy()
+    # compare only sum-pooled columns (mean divides by the full length in both)
+    out_s, _, _, _ = run_case(tables, bad_ids, offs, [0, 0], 40)
+    check_outputs(out_s.double().cpu().numpy(), ref, mag, False, False)
+
+
+def test_deterministic_and_stream():
+    rng = np.random.default_rng(6)
+    tables, ids, offs, pool = random_problem(rng, [64, 16], [1, 0], 500, 80)
+    kw = dict(flags=dpi.DPI_FLAG_EXACT_SPLIT, num_waves=97, chunk_rows=8)
+    a, _, _, _ = run_case(tables, ids, offs, pool, 500, **kw)
+    b, _, _, _ = run_case(tables, ids, offs, pool, 500, **kw)
+    assert torch.equal(a, b)
+    s = torch.cuda.Stream()
+    tt = [torch.from_numpy(t).cuda() for t in tables]
+    fl = FusedLookup(tt, pool, torch.float32, flags=kw["flags"], chunk_rows=8)
+    ids_d, offs_d = torch.from_numpy(ids).cuda(), torch.from_numpy(offs).cuda()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        c = fl(ids_d, offs_d, 500, num_waves=97, stream=s)
+    s.synchronize()
+    assert torch.equal(a, c)
+    check(tables, ids, offs, pool, 500, a)

@@ -1,0 +1,125 @@
+"""Fused gather-pool on the GPU vs the CPU oracle on the five workloads.
+
+Small workloads are compared element by element in full; the 100-table
+workload is compared on sampled contiguous sample ranges (all fields) that
+the oracle recomputes from regenerated rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_21101_amd import dpi
+from paper_2606_21101_amd.lookup import FusedLookup
+from parity import check_outputs, default_waves, gpu_tables, oracle_ref, out_torch_dtype, pooling_codes
+from synth import configs, generate as G
+
+pytestmark = pytest.mark.gpu
+
+
+def run_gpu(cfg, tables, batch, num_waves=0, flags=0, chunk_rows=0, out_dtype=None):
+    od = out_dtype or out_torch_dtype(cfg)
+    fl = FusedLookup(tables, pooling_codes(cfg), od, num_rows=G.table_sizes(cfg), flags=flags,
+                     chunk_rows=chunk_rows)
+    out = fl(batch.ids, batch.offsets, cfg.batch, num_waves=num_waves)
+    plan_status = None
+    torch.cuda.synchronize()
+    return out
+
+
+def compare(cfg, out, ranges=None, mapping="literal", out_f16=None, exact=False):
+    p, ref, mag = oracle_ref(cfg, ranges=ranges, mapping=mapping)
+    y = out[torch.from_numpy(p["samples"]).cuda()].double().cpu().numpy()
+    out_f16 = (out.dtype == torch.float16) if out_f16 is None else out_f16
+    stats = check_outputs(y, ref, mag, cfg.dtype == configs.F16, out_f16, exact=exact,
+                          where=f"cfg{cfg.key} B={cfg.batch}")
+    print(f"cfg{cfg.key} B={cfg.batch} out={out.dtype}: {stats}")
+    return stats
+
+
+def test_generator_same_on_gpu_and_cpu():
+    cfg = configs.get(3)
+    b_gpu = G.make_batch(cfg, device="cuda")
+    b_cpu = G.make_batch(cfg, device="cpu")
+    assert torch.equal(b_gpu.ids.cpu(), b_cpu.ids)
+    t = G.make_table(cfg, 5, "cuda")
+    rows = torch.tensor([0, 1, 17, t.shape[0] - 1])
+    assert torch.equal(t[rows.cuda()].cpu(), G.table_rows(cfg, 5, rows))
+
+
+@pytest.mark.parametrize("key", [1, 2])
+def test_onehot_bit_exact(key):
+    cfg = configs.get(key)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda")
+    out = run_gpu(cfg, tables, batch)
+    compare(cfg, out, exact=True)          # a one-hot lookup is a copy
+
+
+def test_multihot_full():
+    cfg = configs.get(3)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda")
+    out = run_gpu(cfg, tables, batch)
+    compare(cfg, out)
+    out32 = run_gpu(cfg, tables, batch, out_dtype=torch.float32)
+    compare(cfg, out32)
+
+
+def test_multihot_scattered_ids():
+    cfg = configs.get(3)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda", mapping="scattered")
+    out = run_gpu(cfg, tables, batch)
+    compare(cfg, out, ranges=[(0, 2048), (9000, 9100), (16000, 16384)], mapping="scattered")
+
+
+@pytest.mark.parametrize("batch_size", [1, 16, 128, 512, 4096])
+def test_hetero_sweep(batch_size):
+    cfg = configs.get(5, batch=batch_size)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda")
+    out = run_gpu(cfg, tables, batch)
+    compare(cfg, out)
+    # the same batch with wave boundaries inside bags (split bags combined across waves)
+    out2 = run_gpu(cfg, tables, batch, num_waves=max(3, batch.total_ids // 9), flags=dpi.DPI_FLAG_EXACT_SPLIT,
+                   chunk_rows=4)
+    compare(cfg, out2)
+
+
+@pytest.fixture(scope="module")
+def large():
+    cfg = configs.get(4)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda")
+    yield cfg, tables, batch
+    del tables, batch
+    torch.cuda.empty_cache()
+
+
+LARGE_RANGES = [(0, 96), (31000, 31064), (65440, 65536)]
+
+
+def test_large_sampled(large):
+    cfg, tables, batch = large
+    out = run_gpu(cfg, tables, batch)
+    compare(cfg, out, ranges=LARGE_RANGES)
+
+
+def test_large_sampled_fp32_out(large):
+    cfg, tables, batch = large
+    out = run_gpu(cfg, tables, batch, out_dtype=torch.float32)
+    compare(cfg, out, ranges=LARGE_RANGES)
+
+
+def test_large_every_row_written_and_finite(large):
+    cfg, tables, batch = large
+    out = torch.full((cfg.batch, cfg.num_tables * cfg.dim(0)), float("nan"), dtype=torch.float16, device="cuda")
+    fl = FusedLookup(tables, pooling_codes(cfg), torch.float16, num_rows=G.table_sizes(cfg))
+    fl(batch.ids, batch.offsets, cfg.batch, out=out)
+    torch.cuda.synchronize()
+    assert not torch.isnan(out).any()
+    # empty bags are exactly zero, mean pooling never exceeds the row range
+    L = torch.from_numpy(batch.lengths).cuda()
+    empty = (L == 0).nonzero()
+    for t, b in empty[:50].tolist():
+        assert torch.all(out[b, t * 128:(t + 1) * 128] == 0)

@@ -1,0 +1,104 @@
+"""Device plan == CPU plan oracle, bit for bit (all five workloads + edge cases)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_21101_amd import dpi
+from paper_2606_21101_amd.lookup import FusedLookup
+from parity import default_waves, plan_args
+from synth import configs, generate as G
+
+pytestmark = pytest.mark.gpu
+KEYS = ("header", "col_base", "id_base", "bag_item_base", "bag_cost_base", "wave_item_begin")
+
+
+def run_plan(dims, dtypes, out_dtype, rows, lengths, onehot, C=0, K=0, W=0, flags=0):
+    T, B = lengths.shape
+    offs_np = G.offsets_from_lengths(lengths) if B else np.zeros((T, 1), np.int32)
+    offs = None if onehot else torch.from_numpy(offs_np).cuda()
+    total = int(lengths.sum())
+    tabs = [torch.empty((1, d), dtype=torch.float16 if dt else torch.float32, device="cuda")
+            for d, dt in zip(dims, dtypes)]
+    fl = FusedLookup(tabs, None, torch.float16 if out_dtype else torch.float32, num_rows=rows,
+                     chunk_rows=C, item_cost_k=K, flags=flags)
+    plan = fl.plan(offs, B, total, num_waves=W)
+    got = dpi.dpi_plan_export(plan)
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_OK
+    ref = oracle.plan(dims, dtypes, out_dtype, None if onehot else offs_np, B, total, C or 32, K or 64, W,
+                      flags)
+    for k in KEYS:
+        assert np.array_equal(got[k], ref[k]), (k, got[k][:20], ref[k][:20])
+    return got
+
+
+@pytest.mark.parametrize("key,batch", [(1, None), (2, None), (3, None), (4, None),
+                                       (5, 1), (5, 16), (5, 128), (5, 512), (5, 4096)])
+def test_plan_parity_configs(key, batch):
+    cfg = configs.get(key, batch=batch)
+    lengths = G.bag_lengths(cfg)
+    dims, dtypes, out_dtype = plan_args(cfg)
+    rows = G.table_sizes(cfg)
+    W = default_waves(cfg, int(lengths.sum()))
+    got = run_plan(dims, dtypes, out_dtype, rows, lengths, cfg.all_onehot, W=W)
+    print(f"cfg{key} B={cfg.batch}: W={got['header'][3]} N={got['header'][9]} S={got['header'][10]} "
+          f"split={got['header'][12]}")
+    for W2, flags in ((7, 0), (1000, dpi.DPI_FLAG_EXACT_SPLIT)):
+        run_plan(dims, dtypes, out_dtype, rows, lengths, cfg.all_onehot, W=W2, flags=flags)
+
+
+@pytest.mark.parametrize("case", ["all_empty", "one_long_bag", "single_table", "w1", "w_over_n", "c1",
+                                  "mixed_dims", "zero_batch"])
+def test_plan_parity_edges(case):
+    rng = np.random.default_rng(3)
+    dims, dtypes, rows, lengths, kw = [16, 8], [0, 1], [100, 100], None, {}
+    if case == "all_empty":
+        lengths = np.zeros((2, 50), np.int64)
+    elif case == "one_long_bag":
+        lengths = np.array([[256], [0]], np.int64)
+        kw = dict(W=64, flags=dpi.DPI_FLAG_EXACT_SPLIT)
+    elif case == "single_table":
+        dims, dtypes, rows = [64], [1], [1000]
+        lengths = rng.integers(0, 90, size=(1, 333))
+    elif case == "w1":
+        lengths = rng.integers(0, 40, size=(2, 100))
+        kw = dict(W=1)
+    elif case == "w_over_n":
+        lengths = rng.integers(0, 3, size=(2, 10))
+        kw = dict(W=5000)
+    elif case == "c1":
+        lengths = rng.integers(0, 9, size=(2, 77))
+        kw = dict(C=1, K=1, W=37, flags=dpi.DPI_FLAG_EXACT_SPLIT)
+    elif case == "mixed_dims":
+        dims, dtypes, rows = [3, 12, 300, 256, 4], [0, 0, 0, 0, 1], [10, 10, 10, 10, 10]
+        lengths = rng.integers(0, 70, size=(5, 41))
+        kw = dict(W=19)
+    elif case == "zero_batch":
+        lengths = np.zeros((2, 0), np.int64)
+        kw = dict(W=8)
+    run_plan(dims, dtypes, 0, rows, lengths.astype(np.int64), False, **kw)
+
+
+def test_plan_onehot_null_offsets_equals_explicit():
+    cfg = configs.get(2)
+    lengths = G.bag_lengths(cfg)
+    dims, dtypes, out_dtype = plan_args(cfg)
+    rows = G.table_sizes(cfg)
+    a = run_plan(dims, dtypes, out_dtype, rows, lengths, True, W=3000)
+    b = run_plan(dims, dtypes, out_dtype, rows, lengths, False, W=3000)
+    for k in KEYS:
+        assert np.array_equal(a[k], b[k])
+
+
+def test_bad_offsets_detected():
+    tabs = [torch.zeros((10, 16), device="cuda")]
+    fl = FusedLookup(tabs)
+    for bad, total in (([1, 1, 3], 3), ([0, 3, 1], 3), ([0, 1, 3], 4)):
+        offs = torch.tensor([bad], dtype=torch.int32, device="cuda")
+        plan = fl.plan(offs, 2, total, num_waves=4)
+        assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_OFFSETS
+        out = torch.full((2, 16), 7.0, device="cuda")
+        ids = torch.zeros(total, dtype=torch.int32, device="cuda")
+        fl.lookup(plan, ids, offs, out)
+        torch.cuda.synchronize()
+        assert torch.all(out == 7.0)      # a rejected plan makes the lookup a no-op
