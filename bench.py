@@ -1,0 +1,263 @@
+"""Benchmark of the fused multi-table embedding lookup on one MI355X.
+
+A step is one pass of the whole hot path over one batch: dpi_plan (bag scan,
+wave partition) then dpi_lookup (fused gather-pool into the [B, sum dim]
+block), on resident inputs, rotating over R independently drawn batches.
+Prints one JSON line.
+
+  python bench.py [--config 4] [--steps K] [--warmup W] [--gpus 1]
+
+Roofline: the lookup kernel is bound by HBM bandwidth.  Its algorithmic bytes
+per batch are the distinct table rows the batch touches times their row
+bytes, plus 4 bytes per id, 4 bytes per offset and the output block; the
+achieved rate divides them by the lookup kernel's mean duration measured with
+HIP events on the stream it runs on.  HBM traffic measured by rocprofv3
+counters (FETCH_SIZE, WRITE_SIZE) is read from profiles/ when it was taken on
+the current kernel source, else reported as null.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+WORKLOAD_TEXT = {
+    1: "tiny one-hot: 8 tables x 1000 rows, D=16 fp32, B=256, uniform ids, sum",
+    2: "CTR one-hot: 26 tables, rows logU[10,1e6], D=16 fp32, B=4096, Zipf(1.05) ids, sum",
+    3: "multi-hot: 26 tables, rows logU[1e3,5e6], D=64 fp16 -> fp16, B=16384, bags Poisson(10) clip [1,64], "
+       "Zipf(1.05) ids, sum",
+    4: "large: 100 tables, rows logU[1e5,1e7] (59.3 GB fp16), D=128 fp16 -> fp16, B=65536, bags "
+       "floor(LogNormal(ln 20, 0.8)) clip [0,256], Zipf(1.1) ids, even fields sum / odd fields mean",
+    5: "heterogeneous: 39 fields, D in {8,16,32,64} fp32, 13 one-hot + 26 multi-hot, rows logU[10,1e7], "
+       "Zipf(1.2) ids, sum",
+}
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for name in ("lookup.hip", "plan.hip", "dpi_internal.h"):
+        with open(os.path.join(ROOT, "paper_2606_21101_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(config_key: int):
+    """Counter-measured HBM bytes per lookup launch from profiles/, if current."""
+    path = os.path.join(ROOT, "profiles", f"lookup_traffic_config{config_key}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(cfg, samples: int):
+    """Time the CPU oracle on samples [0, samples) of rotation 0, all fields."""
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    import oracle
+    from cases import sub_problem
+    cores = len(os.sched_getaffinity(0))
+    if os.environ.get("OMP_NUM_THREADS", "").isdigit():
+        cores = min(cores, int(os.environ["OMP_NUM_THREADS"]))
+    samples = min(samples, cfg.batch)
+    p = sub_problem(cfg, ranges=[(0, samples)])
+    nnz = int(len(p["ids"]))
+    t0 = time.perf_counter()
+    oracle.lookup(p["dims"], p["tables"], p["ids"], p["offsets"], p["pooling"], p["B"], with_mag=False,
+                  nthreads=cores)
+    dt = time.perf_counter() - t0
+    return {"value": nnz / dt, "unit": "rows/s", "cores": cores, "kind": "oracle",
+            "sample": f"samples [0, {samples}) of batch rotation 0, all {cfg.num_tables} fields: {nnz} pooled ids "
+                      f"in {dt:.3f} s ({dt * cores:.1f} thread-seconds), fp64 sequential per bag"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--batch", type=int, default=None, help="override the batch size (heterogeneous sweep)")
+    ap.add_argument("--rotations", type=int, default=4)
+    ap.add_argument("--out-dtype", choices=["f16", "f32"], default=None)
+    ap.add_argument("--mapping", choices=["literal", "scattered"], default="literal")
+    ap.add_argument("--flags", type=int, default=0)
+    ap.add_argument("--num-waves", type=int, default=0)
+    ap.add_argument("--cpu-samples", type=int, default=2048)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-gib", type=float, default=0.0,
+                    help="only run a plain device copy of this size (counter calibration)")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the lookup is a single-GPU "
+              "path here. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_21101_amd import dpi
+    from paper_2606_21101_amd.lookup import FusedLookup
+    from synth import configs, generate as G
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    if args.copy_probe_gib > 0:
+        n = int(args.copy_probe_gib * (1 << 30)) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 3}))
+        return
+
+    cfg = configs.get(args.config, batch=args.batch, out_dtype=args.out_dtype)
+    t_setup = time.perf_counter()
+    tables = [G.make_table(cfg, t, dev) for t in range(cfg.num_tables)]
+    batches = G.make_batches(cfg, range(args.rotations), dev, mapping=args.mapping)
+    out_dt = torch.float16 if cfg.out_dtype == configs.F16 else torch.float32
+    pool = [1 if p == configs.MEAN else 0 for p in G.table_pooling(cfg)]
+    fl = FusedLookup(tables, pool, out_dt, num_rows=G.table_sizes(cfg), flags=args.flags)
+    osize = 2 if out_dt == torch.float16 else 4
+    esize = 2 if cfg.dtype == configs.F16 else 4
+    total_d = fl.total_dim
+
+    # algorithmic bytes of each batch: distinct rows + ids + offsets + output
+    alg_bytes, nnz_list = [], []
+    for bt in batches:
+        base = bt.id_base
+        uniq_bytes = 0
+        for t in range(cfg.num_tables):
+            seg = bt.ids[int(base[t]):int(base[t + 1])]
+            if seg.numel():
+                uniq_bytes += int(torch.unique(seg).numel()) * cfg.dim(t) * esize
+        offs_bytes = 4 * cfg.num_tables * (cfg.batch + 1) if bt.offsets is not None else 0
+        alg_bytes.append(uniq_bytes + 4 * bt.total_ids + offs_bytes + cfg.batch * total_d * osize)
+        nnz_list.append(bt.total_ids)
+    gathered = [4 * n + (4 * cfg.num_tables * (cfg.batch + 1)) + cfg.batch * total_d * osize
+                + int(sum(int(bt.nnz[t]) * cfg.dim(t) * esize for t in range(cfg.num_tables)))
+                for n, bt in zip(nnz_list, batches)]
+
+    stream = torch.cuda.current_stream()
+    out = torch.empty((cfg.batch, total_d), dtype=out_dt, device=dev)
+    max_total = max(nnz_list)
+    opts = fl.opts(args.num_waves)
+    ws_bytes = dpi.dpi_plan_workspace_bytes(cfg.num_tables, cfg.batch, max_total, max(fl.dims), opts)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    setup_s = time.perf_counter() - t_setup
+
+    def step(i, ev=None):
+        bt = batches[i % len(batches)]
+        if ev is not None:
+            ev[0].record(stream)
+        plan = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, fl.opts(args.num_waves), ws,
+                            ws_bytes, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        dpi.dpi_lookup(plan, tables, bt.ids, bt.offsets, pool, out, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        return plan
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    plans = []
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        plans.append(step(args.warmup + i, evs[i]))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    status = dpi.dpi_plan_sync_status(plans[-1])
+    if status != dpi.DPI_OK:
+        raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
+    plan_ms = np.array([evs[i][0].elapsed_time(evs[i][1]) for i in range(args.steps)])
+    look_ms = np.array([evs[i][1].elapsed_time(evs[i][2]) for i in range(args.steps)])
+    span_ms = evs[0][0].elapsed_time(evs[-1][2])
+    rot = [(args.warmup + i) % len(batches) for i in range(args.steps)]
+    steps_nnz = sum(nnz_list[r] for r in rot)
+    steps_alg = np.array([alg_bytes[r] for r in rot], dtype=np.float64)
+    steps_gath = np.array([gathered[r] for r in rot], dtype=np.float64)
+    ms_per_step = span_ms / args.steps
+    value = steps_nnz / (span_ms / 1e3)
+    look_mean_s = float(look_ms.mean()) / 1e3
+    achieved = float(steps_alg.mean()) / look_mean_s / 1e9
+    hdr = dpi.dpi_plan_export(plans[-1])["header"]
+    traffic = read_traffic(cfg.key)
+
+    line = {
+        "metric": "pooled embedding rows/s",
+        "value": value,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded generator; stands in for Criteo-scale CTR fields)",
+        "config": {
+            "workload": f"config {cfg.key} " + WORKLOAD_TEXT[cfg.key]
+                        + (f" [B={cfg.batch}]" if args.batch else ""),
+            "global_batch": cfg.batch,
+            "fields": cfg.num_tables,
+            "table_dtype": cfg.dtype,
+            "out_dtype": cfg.out_dtype,
+            "id_mapping": args.mapping,
+            "rotating_batches": len(batches),
+            "waves": int(hdr[3]),
+            "items": int(hdr[9]),
+            "split_bags": int(hdr[12]),
+            "parallelism": "single GPU",
+        },
+        "p50_lookup_ms": float(np.median(look_ms)),
+        "p90_lookup_ms": float(np.percentile(look_ms, 90)),
+        "p50_plan_ms": float(np.median(plan_ms)),
+        "p50_step_ms": float(np.median(plan_ms + look_ms)),
+        "wall_ms_per_step": wall * 1e3 / args.steps,
+        "pooled_ids_per_batch": float(np.mean(nnz_list)),
+        "algorithmic_bytes_per_batch": float(np.mean(alg_bytes)),
+        "gathered_bytes_per_batch": float(np.mean(gathered)),
+        "hbm_gbs": achieved,
+        "hbm_frac": achieved / HBM_PEAK_GBS,
+        "gathered_gbs": float(steps_gath.mean()) / look_mean_s / 1e9,
+        "roofline": {
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic,
+        },
+        "setup_s": setup_s,
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_samples)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

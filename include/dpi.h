@@ -100,8 +100,8 @@ typedef struct {
 typedef struct dpi_plan_s* dpi_plan_t;
 
 /*
- * Default wave count for a batch: max(8 * compute units of the current
- * device, ceil((total_ids + T*B) / 512)).  The plan uses
+ * Default wave count for a batch: max(16 * compute units of the current
+ * device, ceil((total_ids + T*B) / 2048)).  The plan uses
  * W = min(requested, number of work items).
  */
 int64_t dpi_default_waves(int32_t num_tables, int64_t batch, int64_t total_ids);

@@ -91,6 +91,7 @@ struct dpi_plan_s {
   int32_t dmax;
   int64_t total_d;
   bool onehot;
+  int32_t uniform_class;   // shared row class of every field, or -1
   hipStream_t stream;
   char* ws;
   Layout layout;
@@ -212,6 +213,16 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
     row_class[t] = flags;
   }
 
+  // one specialised kernel serves batches whose fields share a row class and
+  // fit a buffer descriptor (< 2 GiB each)
+  const int class_mask = kTiF16 | kTiFast | (7 << kTiLprShift);
+  int32_t uniform_class = row_class[0] & class_mask;
+  for (int t = 0; t < num_tables; ++t) {
+    const int64_t bytes = table_meta[t].num_rows * (int64_t)table_meta[t].dim * (table_meta[t].dtype == DPI_F16 ? 2 : 4);
+    if (!(row_class[t] & kTiFast) || (row_class[t] & class_mask) != uniform_class || bytes >= ((int64_t)1 << 31))
+      uniform_class = -1;
+  }
+
   const Layout L = make_layout(num_tables, batch, o.num_waves, dmax);
   if (!workspace) return fail(DPI_ERR_INVALID_ARG, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 15) return fail(DPI_ERR_MISALIGNED, "workspace not 16-byte aligned");
@@ -231,6 +242,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   plan->dmax = dmax;
   plan->total_d = total_d;
   plan->onehot = offsets == nullptr;
+  plan->uniform_class = uniform_class;
   plan->stream = reinterpret_cast<hipStream_t>(stream);
   plan->ws = reinterpret_cast<char*>(workspace);
   plan->layout = L;
@@ -345,6 +357,7 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   a.dmax = plan->dmax;
   a.out_f16 = plan->out_dtype == DPI_F16;
   a.xcd_affine = (plan->flags & DPI_FLAG_XCD_AFFINE) ? 1 : 0;
+  a.uniform_class = plan->uniform_class;
   a.grid_waves = plan->waves_req;
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lookup launch");

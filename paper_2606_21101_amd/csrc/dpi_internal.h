@@ -17,8 +17,8 @@ constexpr int kScanTile = kScanThreads * kScanPerThread;
 constexpr int kMetaChunk = 64;              // tables per meta-upload launch
 constexpr int kDefaultChunkRows = 32;
 constexpr int kDefaultItemCost = 64;
-constexpr int kDefaultRowsPerWave = 512;
-constexpr int kDefaultWavesPerCU = 8;
+constexpr int kDefaultRowsPerWave = 2048;
+constexpr int kDefaultWavesPerCU = 16;
 
 // status word bits (device-latched errors)
 constexpr int kStatusBadOffsets = 1;
@@ -116,7 +116,7 @@ struct LookupArgs {
   int32_t dmax;
   int32_t out_f16;
   int32_t xcd_affine;
-  int32_t pad;
+  int32_t uniform_class;   // TableInfo class bits shared by every field, or -1
   int64_t grid_waves;
 };
 

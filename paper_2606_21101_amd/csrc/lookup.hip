@@ -10,13 +10,21 @@
 // Mapping (the output-first allocation of §IV-C, restated for wave64): the
 // lanes of a wavefront are split into row slots of LPR lanes; the LPR lanes of
 // a slot read one table row as consecutive 16-byte pieces (coalesced along
-// the row) and later write the pooled row as consecutive pieces of the
-// output row.  Interior bags are dealt to slots (a slot pools a whole bag,
-// fp32 accumulation, rows in bag order).  A bag split between waves is pooled
-// cooperatively by all slots of each wave (rows dealt round-robin to slots, a
-// fixed xor-butterfly across slots), its fp32 partial goes to the workspace,
-// and the last wave to arrive (agent-scope ticket) adds the partials in wave
-// order and writes the row -- deterministic, no floating-point atomics.
+// the row) and write the pooled row as consecutive pieces of the output row.
+//   * Interior bags: the wave stages the bags' offsets in LDS, gives each slot
+//     a contiguous run of whole bags holding about the same number of rows,
+//     and each slot walks its rows as one stream (ids prefetched one step
+//     ahead, kUnroll rows in flight), closing a bag whenever the stream
+//     crosses the bag's end (fp32 accumulation, rows in bag order).
+//   * Few or long bags: all slots of the wave pool one bag together (rows
+//     dealt round-robin to slots, then a fixed xor-butterfly across slots).
+//   * A bag split between waves is pooled cooperatively by each wave holding
+//     a piece; its fp32 partial goes to the workspace and the last wave to
+//     arrive (agent-scope ticket) adds the partials in wave order and writes
+//     the row -- deterministic, no floating-point atomics.
+// Rows are read with buffer loads (32-bit offsets, range-checked by the
+// descriptor) when the table is below 2 GiB, with 64-bit global loads
+// otherwise.
 //
 // Pooling: sum, or mean = fp32 sum / bag length (IEEE division); an empty bag
 // gives zeros; one round-to-nearest-even conversion to the output dtype.
@@ -30,25 +38,76 @@ typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
-constexpr int kUnroll = 4;      // rows in flight per slot
+constexpr int kUnroll = 8;        // rows in flight per slot
+constexpr int kTileBags = 256;    // bags whose offsets a wave stages in LDS at once
+constexpr uint32_t kBufferWord3 = 0x00020000;   // raw buffer descriptor, gfx9 family
 
 // Kernel arguments are read in place from the constant kernarg segment
 // (scalar loads); a by-value copy would go to private memory because the
 // table-pointer array is indexed at run time.
 typedef const __attribute__((address_space(4))) LookupArgs* KA;
 
+// Values known to be equal across the wave; out-of-line functions receive
+// them in vector registers, so they are re-read from the first lane to let
+// the compiler keep them (and what derives from them) in scalar registers.
+__device__ __forceinline__ int64_t uni(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+__device__ __forceinline__ KA uni(KA p) {
+  return (KA)(uint64_t)uni((int64_t)(uint64_t)p);
+}
+
+__device__ __forceinline__ int32_t uni(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+// A field's static info, held in scalar registers.
+__device__ __forceinline__ TableInfo table_info(KA a, int64_t t) {
+  const TableInfo x = a->tinfo[t];
+  TableInfo u;
+  u.num_rows = uni(x.num_rows);
+  u.id_base = uni(x.id_base);
+  u.nnz = uni(x.nnz);
+  u.dim = uni(x.dim);
+  u.col_base = uni(x.col_base);
+  u.row_bytes = uni(x.row_bytes);
+  u.out_bytes = uni(x.out_bytes);
+  u.flags = uni(x.flags);
+  u.pad = 0;
+  return u;
+}
+
+// ids are valid in [0, min(num_rows, 2^31)): one unsigned 32-bit compare
+__device__ __forceinline__ uint32_t id_limit(const TableInfo& ti) {
+  return (uint32_t)(ti.num_rows < ((int64_t)1 << 31) ? ti.num_rows : ((int64_t)1 << 31));
+}
+
+// per-wave staging of bag offsets
+__shared__ int32_t g_bag_off[kWavesPerBlock][kTileBags + 1];
+
 template <typename TIN> struct In;
 template <> struct In<float> { static constexpr int EPL = 4; };       // elements per 16 B
 template <> struct In<_Float16> { static constexpr int EPL = 8; };
 
 __device__ __forceinline__ void unpack(const raw16_t r, float* v, float) {
+  // bit-cast the whole vector: a bit-cast of one vector element reads element 0
+  const float4_t f = __builtin_bit_cast(float4_t, r);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) v[i] = __builtin_bit_cast(float, r[i]);
+  for (int i = 0; i < 4; ++i) v[i] = f[i];
 }
 __device__ __forceinline__ void unpack(const raw16_t r, float* v, _Float16) {
   const half8_t h = __builtin_bit_cast(half8_t, r);
 #pragma unroll
   for (int i = 0; i < 8; ++i) v[i] = (float)h[i];
+}
+
+template <typename TIN, int EPL>
+__device__ __forceinline__ void accumulate(float* acc, const raw16_t r) {
+  float v[EPL];
+  unpack(r, v, TIN());
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) acc[i] += v[i];
 }
 
 // Store EPL pooled values of one lane: one vector store when allowed.
@@ -87,112 +146,78 @@ __device__ __forceinline__ bool is_mean(KA a, int64_t t) {
   return (a->mean_bits[t >> 5] >> (t & 31)) & 1u;
 }
 
-// Positions [s, e) of bag b inside its field's id list, clamped to the list.
-__device__ __forceinline__ void bag_span(KA a, const TableInfo& ti, int64_t t, int64_t b,
-                                         int64_t& s, int64_t& e) {
-  if (a->offsets) {
-    const int32_t* o = a->offsets + t * (a->B + 1);
-    s = o[b];
-    e = o[b + 1];
-    s = s < 0 ? 0 : (s > ti.nnz ? ti.nnz : s);
-    e = e < s ? s : (e > ti.nnz ? ti.nnz : e);
-  } else {
-    s = b;
-    e = b + 1;
-  }
+// Position of bag boundary b (0..B) in field t's id list, clamped to the list.
+__device__ __forceinline__ int32_t bag_offset(KA a, const TableInfo& ti, int64_t t, int64_t b) {
+  int64_t v = a->offsets ? (int64_t)a->offsets[t * (a->B + 1) + b] : b;
+  v = v < 0 ? 0 : (v > ti.nnz ? ti.nnz : v);
+  return (int32_t)v;
 }
+
+__device__ __forceinline__ void bag_span(KA a, const TableInfo& ti, int64_t t, int64_t b, int64_t& s, int64_t& e) {
+  s = bag_offset(a, ti, t, b);
+  e = bag_offset(a, ti, t, b + 1);
+  if (e < s) e = s;
+}
+
+// 16-byte piece k of row `id` of a table.
+template <bool BUF> struct RowReader;
+template <> struct RowReader<true> {
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t row_bytes, koff;
+  __device__ RowReader(const void* table, const TableInfo& ti, int k)
+      : rsrc(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(table), (short)0,
+                                               (int)(ti.num_rows * (int64_t)ti.row_bytes), kBufferWord3)),
+        row_bytes((uint32_t)ti.row_bytes), koff((uint32_t)k * 16u) {}
+  __device__ __forceinline__ raw16_t load(int32_t id) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)((uint32_t)id * row_bytes + koff), 0, 0);
+  }
+};
+template <> struct RowReader<false> {
+  const char* base;
+  uint32_t row_bytes, koff;
+  __device__ RowReader(const void* table, const TableInfo& ti, int k)
+      : base(reinterpret_cast<const char*>(table)), row_bytes((uint32_t)ti.row_bytes), koff((uint32_t)k * 16u) {}
+  __device__ __forceinline__ raw16_t load(int32_t id) const {
+    return *reinterpret_cast<const raw16_t*>(base + (uint64_t)(uint32_t)id * row_bytes + koff);
+  }
+};
 
 // ---------------------------------------------------------------------------
 // Fast path: row bytes a multiple of 16 and at most 1024; LPR lanes per row.
 // ---------------------------------------------------------------------------
 
-// Whole bags [b_lo, b_hi) of field t, one bag per slot at a time.
-template <typename TIN, typename TOUT, int LPR>
-__device__ __attribute__((noinline)) int pool_bags_per_slot(KA a, int64_t t, int64_t b_lo, int64_t b_hi,
-                                                            int lane) {
-  constexpr int EPL = In<TIN>::EPL;
-  const TableInfo ti = a->tinfo[t];
-  int bad = 0;
-  constexpr int G = kWaveSize / LPR;
-  const int g = lane / LPR, k = lane % LPR;
-  const TIN* __restrict__ table = reinterpret_cast<const TIN*>(a->tables[t]);
-  const int32_t* __restrict__ ids = a->ids + ti.id_base;
-  const int64_t dim = ti.dim, nrows = ti.num_rows;
-  const bool col = k * EPL < dim;
-  const bool mean = is_mean(a, t);
-  const bool vec = (ti.flags & kTiOutVec) != 0;
-  for (int64_t b = b_lo + g; b < b_hi; b += G) {
-    int64_t s, e;
-    bag_span(a, ti, t, b, s, e);
-    float acc[EPL];
-#pragma unroll
-    for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
-    for (int64_t p = s; p < e; p += kUnroll) {
-      int32_t id[kUnroll];
-      raw16_t raw[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) id[u] = (p + u < e) ? ids[p + u] : -1;
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        raw[u] = raw16_t{0, 0, 0, 0};
-        const bool in_bag = p + u < e;
-        const bool ok = in_bag && id[u] >= 0 && id[u] < nrows;
-        bad |= (in_bag && !ok);
-        if (ok && col)
-          raw[u] = *reinterpret_cast<const raw16_t*>(table + (int64_t)id[u] * dim + k * EPL);
-      }
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        float v[EPL];
-        unpack(raw[u], v, TIN());
-#pragma unroll
-        for (int i = 0; i < EPL; ++i) acc[i] += v[i];
-      }
-    }
-    if (mean && e > s) {
-      const float L = (float)(e - s);
-#pragma unroll
-      for (int i = 0; i < EPL; ++i) acc[i] = acc[i] / L;
-    }
-    if (col) store_lane<TOUT, EPL>(out_row<TOUT>(a, ti, b) + k * EPL, acc, vec);
-  }
-  return bad;
-}
-
-// Rows [r0, r1) (positions in the field's id list) pooled by all slots of the
-// wave; on return every slot holds the total for its lane's columns.
-template <typename TIN, int LPR>
-__device__ __forceinline__ void pool_rows_coop(KA a, const TableInfo& ti, int64_t t, int64_t r0,
-                                               int64_t r1, int lane, float* acc, int& bad) {
+// Rows [r0, r1) of field t pooled by all slots of the wave; on return every
+// slot holds the total for its lane's columns.
+template <typename TIN, int LPR, bool BUF>
+__device__ __forceinline__ void pool_rows_coop(KA a, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1,
+                                               int lane, float* acc, int& bad) {
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
   const int g = lane / LPR, k = lane % LPR;
-  const TIN* __restrict__ table = reinterpret_cast<const TIN*>(a->tables[t]);
+  const RowReader<BUF> rows(a->tables[t], ti, k);
   const int32_t* __restrict__ ids = a->ids + ti.id_base;
-  const int64_t dim = ti.dim, nrows = ti.num_rows;
-  const bool col = k * EPL < dim;
+  const uint32_t nrows = id_limit(ti);
+  const bool col = k * EPL < ti.dim;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
-  for (int64_t r = r0 + g; r < r1; r += (int64_t)G * kUnroll) {
-    int32_t id[kUnroll];
-    raw16_t raw[kUnroll];
+  int32_t idn[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) id[u] = (r + u * G < r1) ? ids[r + u * G] : -1;
+  for (int u = 0; u < kUnroll; ++u) idn[u] = (r0 + g + u * G < r1) ? ids[r0 + g + u * G] : -1;
+  for (int64_t r = r0 + g; r < r1; r += (int64_t)G * kUnroll) {
+    raw16_t raw[kUnroll];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       raw[u] = raw16_t{0, 0, 0, 0};
       const bool in_bag = r + u * G < r1;
-      const bool ok = in_bag && id[u] >= 0 && id[u] < nrows;
+      const bool ok = in_bag && (uint32_t)idn[u] < nrows;
       bad |= (in_bag && !ok);
-      if (ok && col) raw[u] = *reinterpret_cast<const raw16_t*>(table + (int64_t)id[u] * dim + k * EPL);
+      if (ok && col) raw[u] = rows.load(idn[u]);
     }
+    const int64_t rn = r + (int64_t)G * kUnroll;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      float v[EPL];
-      unpack(raw[u], v, TIN());
+    for (int u = 0; u < kUnroll; ++u) idn[u] = (rn + u * G < r1) ? ids[rn + u * G] : -1;
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) acc[i] += v[i];
-    }
+    for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
   }
 #pragma unroll
   for (int m = LPR; m < kWaveSize; m <<= 1) {
@@ -201,44 +226,158 @@ __device__ __forceinline__ void pool_rows_coop(KA a, const TableInfo& ti, int64_
   }
 }
 
-// Whole bags, all slots on one bag at a time (few long bags).
-template <typename TIN, typename TOUT, int LPR>
-__device__ __attribute__((noinline)) int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
+// Whole bags [b_lo, b_hi) of field t, the wave pooling one bag at a time.
+template <typename TIN, typename TOUT, int LPR, bool BUF>
+__device__ __forceinline__ int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
   constexpr int EPL = In<TIN>::EPL;
-  const TableInfo ti = a->tinfo[t];
-  int bad = 0;
+  a = uni(a);
+  t = uni(t);
+  b_lo = uni(b_lo);
+  b_hi = uni(b_hi);
   const int g = lane / LPR, k = lane % LPR;
+  const TableInfo ti = table_info(a, t);
   const bool col = k * EPL < ti.dim;
   const bool mean = is_mean(a, t);
   const bool vec = (ti.flags & kTiOutVec) != 0;
+  int bad = 0;
   for (int64_t b = b_lo; b < b_hi; ++b) {
     int64_t s, e;
     bag_span(a, ti, t, b, s, e);
     float acc[EPL];
-    pool_rows_coop<TIN, LPR>(a, ti, t, s, e, lane, acc, bad);
+    pool_rows_coop<TIN, LPR, BUF>(a, ti, t, s, e, lane, acc, bad);
     if (mean && e > s) {
       const float L = (float)(e - s);
 #pragma unroll
-      for (int i = 0; i < EPL; ++i) acc[i] = acc[i] / L;
+      for (int q = 0; q < EPL; ++q) acc[q] = acc[q] / L;
     }
     if (g == 0 && col) store_lane<TOUT, EPL>(out_row<TOUT>(a, ti, b) + k * EPL, acc, vec);
   }
   return bad;
 }
 
-// Rows [row_lo, row_hi) of bag b (bag-relative), fp32 partial to `slot`.
-template <typename TIN, int LPR>
-__device__ __attribute__((noinline)) int partial_fast(KA a, int64_t t, int64_t b, int64_t row_lo, int64_t row_hi,
-                                                      int64_t slot, int lane) {
+// Whole bags [b_lo, b_hi) of field t.
+template <typename TIN, typename TOUT, int LPR, bool BUF>
+__device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
   constexpr int EPL = In<TIN>::EPL;
-  const TableInfo ti = a->tinfo[t];
-  int bad = 0;
+  constexpr int G = kWaveSize / LPR;
+  a = uni(a);
+  t = uni(t);
+  b_lo = uni(b_lo);
+  b_hi = uni(b_hi);
   const int g = lane / LPR, k = lane % LPR;
+  const TableInfo ti = table_info(a, t);
+  const RowReader<BUF> rows(a->tables[t], ti, k);
+  const int32_t* __restrict__ ids = a->ids + ti.id_base;
+  const uint32_t nrows = id_limit(ti);
+  const bool col = k * EPL < ti.dim;
+  const bool mean = is_mean(a, t);
+  const bool vec = (ti.flags & kTiOutVec) != 0;
+  TOUT* const out_lane = out_row<TOUT>(a, ti, 0) + k * EPL;
+  const int64_t ostride = a->total_d;
+  int32_t* const off = g_bag_off[threadIdx.x / kWaveSize];
+  int bad = 0;
+
+  for (int64_t tb0 = b_lo; tb0 < b_hi; tb0 += kTileBags) {
+    const int nb = (int)min((int64_t)kTileBags, b_hi - tb0);
+    if (nb * 2 <= G) {
+      // few bags: the whole wave pools one bag at a time
+      bad |= pool_bags_coop<TIN, TOUT, LPR, BUF>(a, t, tb0, tb0 + nb, lane);
+      continue;
+    }
+    // stage the tile's bag boundaries (wave-private LDS; LDS operations of
+    // one wave complete in order, so no barrier is needed)
+    for (int i = lane; i <= nb; i += kWaveSize) off[i] = bag_offset(a, ti, t, tb0 + i);
+    const int32_t P0 = off[0], R = off[nb] - P0;
+    // slot g owns the bags whose first row lies at or after P0 + ceil(g*R/G)
+    // and before the next slot's start
+    auto first_bag_at = [&](int slot) -> int {
+      if (slot <= 0) return 0;
+      if (slot >= G) return nb;
+      const int32_t target = P0 + (int32_t)(((int64_t)slot * R + G - 1) / G);
+      int lo = 0, hi = nb;   // smallest i in [0, nb] with off[i] >= target
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (off[mid] < target) lo = mid + 1; else hi = mid;
+      }
+      return lo;
+    };
+    int cur = first_bag_at(g);
+    const int endb = first_bag_at(g + 1);
+    int32_t r = off[cur];
+    const int32_t r_end = off[endb];
+    int32_t bstart = r;
+    int32_t bend = cur < endb ? off[cur + 1] : r;
+    float acc[EPL];
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
+
+    // close the current bag (pool, store, reset) and every empty bag after it
+    // until the stream position r lies inside a bag; the bound on cur only
+    // matters for offsets other than the non-decreasing ones the plan checked
+    auto close_bags = [&]() {
+      while (cur < endb && r >= bend) {
+        const int32_t L = bend - bstart;
+        if (mean && L > 0) {
+          const float fl = (float)L;
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) acc[q] = acc[q] / fl;
+        }
+        if (col) store_lane<TOUT, EPL>(out_lane + (tb0 + cur) * ostride, acc, vec);
+#pragma unroll
+        for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
+        ++cur;
+        bstart = bend;
+        if (cur < endb) bend = off[cur + 1];
+      }
+    };
+
+    close_bags();   // leading empty bags
+    int32_t idn[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) idn[u] = (r + u < r_end) ? ids[r + u] : -1;
+    while (cur < endb) {
+      // one group of up to kUnroll rows of the current bag
+      const int32_t ge = min(r + kUnroll, bend);
+      raw16_t raw[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        raw[u] = raw16_t{0, 0, 0, 0};
+        const bool in_group = r + u < ge;
+        const bool ok = in_group && (uint32_t)idn[u] < nrows;
+        bad |= (in_group && !ok);
+        if (ok && col) raw[u] = rows.load(idn[u]);
+      }
+      // the next group starts at ge: prefetch its ids
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) idn[u] = (ge + u < r_end) ? ids[ge + u] : -1;
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
+      r = ge;
+      close_bags();
+    }
+  }
+  return bad;
+}
+
+// Rows [row_lo, row_hi) of bag b (bag-relative), fp32 partial to `slot`.
+template <typename TIN, int LPR, bool BUF>
+__device__ __forceinline__ int partial_fast(KA a, int64_t t, int64_t b, int64_t row_lo, int64_t row_hi,
+                                           int64_t slot, int lane) {
+  constexpr int EPL = In<TIN>::EPL;
+  a = uni(a);
+  t = uni(t);
+  b = uni(b);
+  row_lo = uni(row_lo);
+  row_hi = uni(row_hi);
+  slot = uni(slot);
+  const int g = lane / LPR, k = lane % LPR;
+  const TableInfo ti = table_info(a, t);
+  int bad = 0;
   int64_t s, e;
   bag_span(a, ti, t, b, s, e);
   const int64_t r0 = min(e, s + row_lo), r1 = min(e, s + row_hi);
   float acc[EPL];
-  pool_rows_coop<TIN, LPR>(a, ti, t, r0, r1, lane, acc, bad);
+  pool_rows_coop<TIN, LPR, BUF>(a, ti, t, r0, r1, lane, acc, bad);
   if (g == 0 && k * EPL < ti.dim) {
     float* dst = a->partial + slot * a->dmax + k * EPL;
 #pragma unroll
@@ -254,7 +393,13 @@ template <typename TIN, typename TOUT>
 __device__ __attribute__((noinline)) int pool_general(KA a, int64_t t, int64_t b, int64_t row_lo, int64_t row_hi,
                                                       bool complete, int64_t slot, int lane) {
   constexpr int EPW = 4 / sizeof(TIN);   // elements per 4-byte word
-  const TableInfo ti = a->tinfo[t];
+  a = uni(a);
+  t = uni(t);
+  b = uni(b);
+  row_lo = uni(row_lo);
+  row_hi = uni(row_hi);
+  slot = uni(slot);
+  const TableInfo ti = table_info(a, t);
   int bad = 0;
   const int64_t words = ti.row_bytes / 4;
   int lpr = 1;
@@ -312,7 +457,10 @@ __device__ __attribute__((noinline)) int pool_general(KA a, int64_t t, int64_t b
 // Split bags: publish this wave's partial; the last arrival combines.
 // ---------------------------------------------------------------------------
 template <typename TOUT>
-__device__ __attribute__((noinline)) void finish_piece(KA a, int64_t w_first, int64_t bag, int lane) {
+__device__ __forceinline__ void finish_piece(KA a, int64_t w_first, int64_t bag, int lane) {
+  a = uni(a);
+  w_first = uni(w_first);
+  bag = uni(bag);
   if (w_first < 0 || w_first >= min(a->hdr[kHdrW], a->grid_waves)) return;   // malformed plan
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   int old = 0;
@@ -323,7 +471,7 @@ __device__ __attribute__((noinline)) void finish_piece(KA a, int64_t w_first, in
   if (old != pieces - 1) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
   const int64_t t = bag / a->B, b = bag - t * a->B;
-  const TableInfo ti = a->tinfo[t];
+  const TableInfo ti = table_info(a, t);
   int64_t s, e;
   bag_span(a, ti, t, b, s, e);
   const bool mean = is_mean(a, t);
@@ -340,81 +488,123 @@ __device__ __attribute__((noinline)) void finish_piece(KA a, int64_t w_first, in
 }
 
 // ---------------------------------------------------------------------------
-// Dispatch on the field's row class (wave-uniform).
+// Work of one wave, parameterised by how a field's rows are pooled.
+//   Uniform<TIN, TOUT, LPR>: every field has the same row class and fits a
+//     buffer descriptor; everything is inlined into one lean kernel.
+//   Mixed<TOUT>: fields of different classes; a wave-uniform switch calls
+//     out-of-line routines per class (including the general path).
 // ---------------------------------------------------------------------------
 #define DPI_FOR_LPR(MACRO) \
   MACRO(0, 1) MACRO(1, 2) MACRO(2, 4) MACRO(3, 8) MACRO(4, 16) MACRO(5, 32) MACRO(6, 64)
 
-template <typename TIN, typename TOUT>
-__device__ int pool_segment_typed(KA a, int flags, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
-  const int lg = (flags >> kTiLprShift) & 7;
-  const int64_t slots = kWaveSize >> lg;
-  const bool coop = (b_hi - b_lo) * 2 <= slots;
-  switch (lg) {
-#define DPI_CASE(L, LPR)                                                      \
-  case L:                                                                     \
-    return coop ? pool_bags_coop<TIN, TOUT, LPR>(a, t, b_lo, b_hi, lane)      \
-                : pool_bags_per_slot<TIN, TOUT, LPR>(a, t, b_lo, b_hi, lane);
-    DPI_FOR_LPR(DPI_CASE)
-#undef DPI_CASE
-    default:
-      return 0;
+template <typename TIN, typename TOUT, int LPR>
+struct Uniform {
+  static __device__ __forceinline__ int segment(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
+    return pool_segment_fast<TIN, TOUT, LPR, true>(a, t, b_lo, b_hi, lane);
   }
+  static __device__ __forceinline__ int partial(KA a, int64_t t, int64_t b, int64_t lo, int64_t hi, int64_t slot,
+                                                int lane) {
+    return partial_fast<TIN, LPR, true>(a, t, b, lo, hi, slot, lane);
+  }
+  static __device__ __forceinline__ void finish(KA a, int64_t w_first, int64_t bag, int lane) {
+    finish_piece<TOUT>(a, w_first, bag, lane);
+  }
+};
+
+template <typename TIN, typename TOUT, int LPR, bool BUF>
+__device__ __attribute__((noinline)) int segment_call(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
+  return pool_segment_fast<TIN, TOUT, LPR, BUF>(a, t, b_lo, b_hi, lane);
+}
+template <typename TIN, int LPR>
+__device__ __attribute__((noinline)) int partial_call(KA a, int64_t t, int64_t b, int64_t lo, int64_t hi,
+                                                      int64_t slot, int lane) {
+  return partial_fast<TIN, LPR, false>(a, t, b, lo, hi, slot, lane);
+}
+template <typename TOUT>
+__device__ __attribute__((noinline)) void finish_call(KA a, int64_t w_first, int64_t bag, int lane) {
+  finish_piece<TOUT>(a, w_first, bag, lane);
+}
+
+// buffer descriptors hold a 32-bit byte range; offsets are formed as signed
+// 32-bit values, so tables below 2 GiB use them
+__device__ __forceinline__ bool use_buffer(const TableInfo& ti) {
+  return ti.num_rows * (int64_t)ti.row_bytes < ((int64_t)1 << 31);
 }
 
 template <typename TOUT>
-__device__ int pool_bag_range(KA a, int64_t lA, int64_t lB, int lane) {
-  int bad = 0;
-  while (lA < lB) {
-    const int64_t t = __builtin_amdgcn_readfirstlane((int)(lA / a->B));
-    const int64_t seg_end = min(lB, (t + 1) * a->B);
-    const int flags = a->tinfo[t].flags;
-    const int64_t b_lo = lA - t * a->B, b_hi = seg_end - t * a->B;
-    if (flags & kTiFast) {
-      if (flags & kTiF16)
-        bad |= pool_segment_typed<_Float16, TOUT>(a, flags, t, b_lo, b_hi, lane);
-      else
-        bad |= pool_segment_typed<float, TOUT>(a, flags, t, b_lo, b_hi, lane);
-    } else {
+struct Mixed {
+  static __device__ int segment(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
+    const TableInfo ti = table_info(a, t);
+    const int flags = ti.flags;
+    if (!(flags & kTiFast)) {
+      int bad = 0;
       for (int64_t b = b_lo; b < b_hi; ++b) {
         if (flags & kTiF16)
           bad |= pool_general<_Float16, TOUT>(a, t, b, 0, INT64_MAX / 2, true, 0, lane);
         else
           bad |= pool_general<float, TOUT>(a, t, b, 0, INT64_MAX / 2, true, 0, lane);
       }
+      return bad;
     }
+    const bool buf = use_buffer(ti), f16 = (flags & kTiF16) != 0;
+    switch ((flags >> kTiLprShift) & 7) {
+#define DPI_CASE(L, LPR)                                                                   \
+  case L:                                                                                  \
+    if (f16)                                                                               \
+      return buf ? segment_call<_Float16, TOUT, LPR, true>(a, t, b_lo, b_hi, lane)         \
+                 : segment_call<_Float16, TOUT, LPR, false>(a, t, b_lo, b_hi, lane);       \
+    return buf ? segment_call<float, TOUT, LPR, true>(a, t, b_lo, b_hi, lane)              \
+               : segment_call<float, TOUT, LPR, false>(a, t, b_lo, b_hi, lane);
+      DPI_FOR_LPR(DPI_CASE)
+#undef DPI_CASE
+      default:
+        return 0;
+    }
+  }
+  static __device__ int partial(KA a, int64_t t, int64_t b, int64_t lo, int64_t hi, int64_t slot, int lane) {
+    const int flags = table_info(a, t).flags;
+    if (!(flags & kTiFast)) {
+      return (flags & kTiF16) ? pool_general<_Float16, TOUT>(a, t, b, lo, hi, false, slot, lane)
+                              : pool_general<float, TOUT>(a, t, b, lo, hi, false, slot, lane);
+    }
+    const bool f16 = (flags & kTiF16) != 0;
+    switch ((flags >> kTiLprShift) & 7) {
+#define DPI_CASE(L, LPR)                                                                          \
+  case L:                                                                                         \
+    return f16 ? partial_call<_Float16, LPR>(a, t, b, lo, hi, slot, lane)                         \
+               : partial_call<float, LPR>(a, t, b, lo, hi, slot, lane);
+      DPI_FOR_LPR(DPI_CASE)
+#undef DPI_CASE
+      default:
+        return 0;
+    }
+  }
+  static __device__ void finish(KA a, int64_t w_first, int64_t bag, int lane) {
+    finish_call<TOUT>(a, w_first, bag, lane);
+  }
+};
+
+// Bags [lA, lB) (global bag numbers, field-major), split at field ends.
+template <typename P>
+__device__ __forceinline__ int pool_bag_range(KA a, int64_t lA, int64_t lB, int lane) {
+  int bad = 0;
+  while (lA < lB) {
+    const int64_t t = __builtin_amdgcn_readfirstlane((int)(lA / a->B));
+    const int64_t seg_end = min(lB, (t + 1) * a->B);
+    bad |= P::segment(a, t, lA - t * a->B, seg_end - t * a->B, lane);
     lA = seg_end;
   }
   return bad;
 }
 
-template <typename TOUT>
-__device__ int pool_partial(KA a, int64_t bag, int64_t row_lo, int64_t row_hi, int64_t slot, int64_t w_first,
-                            int lane) {
+// Rows [row_lo, row_hi) of a bag shared with other waves: partial, then the
+// arrival protocol.
+template <typename P>
+__device__ __forceinline__ int pool_partial(KA a, int64_t bag, int64_t row_lo, int64_t row_hi, int64_t slot,
+                                            int64_t w_first, int lane) {
   const int64_t t = __builtin_amdgcn_readfirstlane((int)(bag / a->B));
-  const int64_t b = bag - t * a->B;
-  const int flags = a->tinfo[t].flags;
-  int bad = 0;
-  if (flags & kTiFast) {
-    const int lg = (flags >> kTiLprShift) & 7;
-    const bool f16 = (flags & kTiF16) != 0;
-    switch (lg) {
-#define DPI_CASE(L, LPR)                                                              \
-  case L:                                                                             \
-    bad = f16 ? partial_fast<_Float16, LPR>(a, t, b, row_lo, row_hi, slot, lane)      \
-              : partial_fast<float, LPR>(a, t, b, row_lo, row_hi, slot, lane);        \
-    break;
-      DPI_FOR_LPR(DPI_CASE)
-#undef DPI_CASE
-      default:
-        break;
-    }
-  } else if (flags & kTiF16) {
-    bad = pool_general<_Float16, TOUT>(a, t, b, row_lo, row_hi, false, slot, lane);
-  } else {
-    bad = pool_general<float, TOUT>(a, t, b, row_lo, row_hi, false, slot, lane);
-  }
-  finish_piece<TOUT>(a, w_first, bag, lane);
+  const int bad = P::partial(a, t, bag - t * a->B, row_lo, row_hi, slot, lane);
+  P::finish(a, w_first, bag, lane);
   return bad;
 }
 
@@ -425,10 +615,8 @@ __device__ __forceinline__ int64_t xcd_affine_block(int64_t g, int64_t n) {
   return x < r ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
 }
 
-template <typename TOUT>
-__global__ __launch_bounds__(kBlockThreads) void lookup_kernel(const LookupArgs args) {
-  (void)args;
-  const KA a = (KA)__builtin_amdgcn_kernarg_segment_ptr();
+template <typename P>
+__device__ __forceinline__ void wave_body(KA a) {
   const int lane = threadIdx.x & (kWaveSize - 1);
   int64_t blk = blockIdx.x;
   if (a->xcd_affine) blk = xcd_affine_block(blk, gridDim.x);
@@ -450,19 +638,31 @@ __global__ __launch_bounds__(kBlockThreads) void lookup_kernel(const LookupArgs 
   if (la == lb && (head || tail)) {
     const int64_t slot = head ? 2 * w : 2 * w + 1;
     const int64_t w_first = head ? (int64_t)a->head_first[w] : w;
-    bad |= pool_partial<TOUT>(a, la, (i0 - la_base) * C, (i1 - la_base) * C, slot, w_first, lane);
+    bad |= pool_partial<P>(a, la, (i0 - la_base) * C, (i1 - la_base) * C, slot, w_first, lane);
   } else {
     int64_t lA = la, lB = lb + 1;
     if (head) {
-      bad |= pool_partial<TOUT>(a, la, (i0 - la_base) * C, INT64_MAX / 2, 2 * w, a->head_first[w], lane);
+      bad |= pool_partial<P>(a, la, (i0 - la_base) * C, INT64_MAX / 2, 2 * w, a->head_first[w], lane);
       lA = la + 1;
     }
     if (tail) lB = lb;
-    bad |= pool_bag_range<TOUT>(a, lA, lB, lane);
-    if (tail) bad |= pool_partial<TOUT>(a, lb, 0, (i1 - lb_base) * C, 2 * w + 1, w, lane);
+    bad |= pool_bag_range<P>(a, lA, lB, lane);
+    if (tail) bad |= pool_partial<P>(a, lb, 0, (i1 - lb_base) * C, 2 * w + 1, w, lane);
   }
   if (__any(bad) && lane == 0)
     __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename TIN, typename TOUT, int LPR>
+__global__ __launch_bounds__(kBlockThreads) void lookup_uniform_kernel(const LookupArgs args) {
+  (void)args;
+  wave_body<Uniform<TIN, TOUT, LPR>>((KA)__builtin_amdgcn_kernarg_segment_ptr());
+}
+
+template <typename TOUT>
+__global__ __launch_bounds__(kBlockThreads) void lookup_mixed_kernel(const LookupArgs args) {
+  (void)args;
+  wave_body<Mixed<TOUT>>((KA)__builtin_amdgcn_kernarg_segment_ptr());
 }
 
 }  // namespace
@@ -470,10 +670,32 @@ __global__ __launch_bounds__(kBlockThreads) void lookup_kernel(const LookupArgs 
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s) {
   const int64_t blocks = (a.grid_waves + kWavesPerBlock - 1) / kWavesPerBlock;
   if (blocks <= 0) return hipSuccess;
-  if (a.out_f16)
-    hipLaunchKernelGGL(lookup_kernel<_Float16>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(lookup_kernel<float>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+  const dim3 grid((unsigned)blocks), block(kBlockThreads);
+  if (a.uniform_class < 0) {
+    if (a.out_f16)
+      hipLaunchKernelGGL(lookup_mixed_kernel<_Float16>, grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL(lookup_mixed_kernel<float>, grid, block, 0, s, a);
+    return hipGetLastError();
+  }
+  const bool f16 = (a.uniform_class & kTiF16) != 0;
+  switch ((a.uniform_class >> kTiLprShift) & 7) {
+#define DPI_CASE(L, LPR)                                                                               \
+  case L:                                                                                              \
+    if (f16 && a.out_f16)                                                                              \
+      hipLaunchKernelGGL((lookup_uniform_kernel<_Float16, _Float16, LPR>), grid, block, 0, s, a);      \
+    else if (f16)                                                                                      \
+      hipLaunchKernelGGL((lookup_uniform_kernel<_Float16, float, LPR>), grid, block, 0, s, a);         \
+    else if (a.out_f16)                                                                                \
+      hipLaunchKernelGGL((lookup_uniform_kernel<float, _Float16, LPR>), grid, block, 0, s, a);         \
+    else                                                                                               \
+      hipLaunchKernelGGL((lookup_uniform_kernel<float, float, LPR>), grid, block, 0, s, a);            \
+    break;
+    DPI_FOR_LPR(DPI_CASE)
+#undef DPI_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

@@ -64,9 +64,9 @@ def plan_args(cfg):
 
 
 def default_waves(cfg, total_ids):
-    """The library's documented default: max(8 * CUs, ceil((ids + T*B) / 512))."""
+    """The library's documented default: max(16 * CUs, ceil((ids + T*B) / 2048))."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    return max(8 * cus, -(-(total_ids + cfg.num_tables * cfg.batch) // 512))
+    return max(16 * cus, -(-(total_ids + cfg.num_tables * cfg.batch) // 2048))
 
 
 __all__ = ["check_outputs", "oracle_ref", "gpu_tables", "out_torch_dtype", "plan_args", "default_waves",

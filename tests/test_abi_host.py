@@ -93,8 +93,8 @@ def test_lookup_rejects_null_plan_and_destroy_null():
 
 
 def test_default_waves_formula():
-    # max(8 * CUs, ceil((total_ids + T*B) / 512)); on a host without a GPU the
-    # CU count falls back to 256
+    # max(16 * CUs, ceil((total_ids + T*B) / 2048)); on a host without a GPU
+    # the CU count falls back to 256
     w = dpi.dpi_default_waves(100, 65536, 176_805_878)
-    assert w == -(-(176_805_878 + 100 * 65536) // 512)
-    assert dpi.dpi_default_waves(8, 256, 2048) >= 2048
+    assert w == -(-(176_805_878 + 100 * 65536) // 2048)
+    assert dpi.dpi_default_waves(8, 256, 2048) == 16 * 256

@@ -89,8 +89,13 @@ def test_hetero_sweep(batch_size):
 @pytest.fixture(scope="module")
 def large():
     cfg = configs.get(4)
-    tables = gpu_tables(cfg)
+    tables = []
+    for t in range(cfg.num_tables):
+        tables.append(G.make_table(cfg, t, "cuda"))
+        if t % 20 == 19:
+            print(f"  large workload: {t + 1} tables generated", flush=True)
     batch = G.make_batch(cfg, device="cuda")
+    print(f"  large workload: batch of {batch.total_ids} ids generated", flush=True)
     yield cfg, tables, batch
     del tables, batch
     torch.cuda.empty_cache()
@@ -99,18 +104,21 @@ def large():
 LARGE_RANGES = [(0, 96), (31000, 31064), (65440, 65536)]
 
 
+@pytest.mark.timeout(900)
 def test_large_sampled(large):
     cfg, tables, batch = large
     out = run_gpu(cfg, tables, batch)
     compare(cfg, out, ranges=LARGE_RANGES)
 
 
+@pytest.mark.timeout(600)
 def test_large_sampled_fp32_out(large):
     cfg, tables, batch = large
     out = run_gpu(cfg, tables, batch, out_dtype=torch.float32)
     compare(cfg, out, ranges=LARGE_RANGES)
 
 
+@pytest.mark.timeout(600)
 def test_large_every_row_written_and_finite(large):
     cfg, tables, batch = large
     out = torch.full((cfg.batch, cfg.num_tables * cfg.dim(0)), float("nan"), dtype=torch.float16, device="cuda")

@@ -22,6 +22,10 @@ def run_plan(dims, dtypes, out_dtype, rows, lengths, onehot, C=0, K=0, W=0, flag
             for d, dt in zip(dims, dtypes)]
     fl = FusedLookup(tabs, None, torch.float16 if out_dtype else torch.float32, num_rows=rows,
                      chunk_rows=C, item_cost_k=K, flags=flags)
+    if W == 0:
+        # the library's documented default, computed here from the device's CU count
+        cus = torch.cuda.get_device_properties(0).multi_processor_count
+        W = max(16 * cus, -(-(total + T * B) // 2048))
     plan = fl.plan(offs, B, total, num_waves=W)
     got = dpi.dpi_plan_export(plan)
     assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_OK
