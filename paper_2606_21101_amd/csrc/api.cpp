@@ -31,8 +31,8 @@ dpi_status hip_fail(hipError_t e, const char* what) {
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t hdr, status, tinfo, col_base, id_base, block_sum, block_pre, bib, bcb, wib, wave_bag, head_first,
-      split_pieces, split_last, tickets, partial, total;
+  size_t hdr, status, tinfo, col_base, id_base, block_sum, bib, bcb, wib, wave_bag, head_first, split_pieces,
+      split_last, tickets, partial, total;
 };
 
 Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
@@ -50,8 +50,7 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
   L.tinfo = take(T * sizeof(TableInfo));
   L.col_base = take((T + 1) * sizeof(int64_t));
   L.id_base = take((T + 1) * sizeof(int64_t));
-  L.block_sum = take(2 * std::max<int64_t>(nblk, 1) * sizeof(int64_t));
-  L.block_pre = take(2 * std::max<int64_t>(nblk, 1) * sizeof(int64_t));
+  L.block_sum = take(3 * std::max<int64_t>(nblk, 1) * sizeof(int64_t));
   L.bib = take((TB + 1) * sizeof(int64_t));
   L.bcb = take((TB + 1) * sizeof(int64_t));
   L.wib = take((waves_req + 1) * sizeof(int64_t));
@@ -172,7 +171,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
 
   int64_t col = 0;
   int32_t dmax = 1;
-  MetaChunk chunk[(DPI_MAX_TABLES + kMetaChunk - 1) / kMetaChunk];
+  int64_t col_base[DPI_MAX_TABLES];
   int32_t row_class[DPI_MAX_TABLES];
   for (int t = 0; t < num_tables; ++t) {
     const dpi_table_meta& m = table_meta[t];
@@ -190,10 +189,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
       flags |= ilog2((int)(row_bytes / 16)) << kTiLprShift;
     }
     row_class[t] = flags;
-    MetaChunk& c = chunk[t / kMetaChunk];
-    c.num_rows[t % kMetaChunk] = m.num_rows;
-    c.dim[t % kMetaChunk] = m.dim;
-    c.col_base[t % kMetaChunk] = (int32_t)col;
+    col_base[t] = col;
     col += m.dim;
     if (col > ((int64_t)1 << 31) - 1) return fail(DPI_ERR_UNSUPPORTED, "sum of dims too large");
     dmax = std::max(dmax, m.dim);
@@ -201,15 +197,12 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   const int64_t total_d = col;
   // vector stores need every output row piece aligned to min(16, bytes per lane)
   for (int t = 0; t < num_tables; ++t) {
-    MetaChunk& c = chunk[t / kMetaChunk];
     int flags = row_class[t];
     if (flags & kTiFast) {
       const int epl = (flags & kTiF16) ? 8 : 4;
       const int64_t a = std::min(16, epl * osize);
-      if ((total_d * osize) % a == 0 && ((int64_t)c.col_base[t % kMetaChunk] * osize) % a == 0)
-        flags |= kTiOutVec;
+      if ((total_d * osize) % a == 0 && (col_base[t] * osize) % a == 0) flags |= kTiOutVec;
     }
-    c.flags[t % kMetaChunk] = flags;
     row_class[t] = flags;
   }
 
@@ -256,7 +249,6 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   d.col_base = reinterpret_cast<int64_t*>(ws + L.col_base);
   d.id_base = reinterpret_cast<int64_t*>(ws + L.id_base);
   d.block_sum = reinterpret_cast<int64_t*>(ws + L.block_sum);
-  d.block_pre = reinterpret_cast<int64_t*>(ws + L.block_pre);
   d.bib = reinterpret_cast<int64_t*>(ws + L.bib);
   d.bcb = reinterpret_cast<int64_t*>(ws + L.bcb);
   d.wib = reinterpret_cast<int64_t*>(ws + L.wib);
@@ -267,7 +259,9 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   d.tickets = reinterpret_cast<int32_t*>(ws + L.tickets);
   d.partial = reinterpret_cast<float*>(ws + L.partial);
 
-  PlanParams p;
+  PlanArgs pa;
+  std::memset(&pa, 0, sizeof(pa));
+  PlanParams& p = pa.p;
   p.T = num_tables;
   p.C = o.chunk_rows;
   p.K = o.item_cost_k;
@@ -280,35 +274,15 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   p.waves_req = o.num_waves;
   p.total_d = total_d;
   p.offsets = offsets;
-
-  hipStream_t s = plan->stream;
-  hipError_t e;
-  for (int first = 0; first < num_tables; first += kMetaChunk) {
-    const int count = std::min(kMetaChunk, num_tables - first);
-    e = launch_plan_meta(chunk[first / kMetaChunk], first, count, d, first == 0, osize, s);
-    if (e != hipSuccess) {
-      delete plan;
-      return hip_fail(e, "plan_meta launch");
-    }
+  pa.d = d;
+  for (int t = 0; t < num_tables; ++t) {
+    pa.packed[t] = (uint32_t)table_meta[t].dim | ((uint32_t)row_class[t] << 17);
+    pa.num_rows[t] = table_meta[t].num_rows;
   }
-  if (p.TB > 0) {
-    e = launch_plan_reduce(p, d, s);
-    if (e != hipSuccess) {
-      delete plan;
-      return hip_fail(e, "plan_reduce launch");
-    }
-  }
-  e = launch_plan_totals(p, d, s);
+  const hipError_t e = launch_plan(pa, plan->stream);
   if (e != hipSuccess) {
     delete plan;
-    return hip_fail(e, "plan_totals launch");
-  }
-  if (p.TB > 0) {
-    e = launch_plan_scan_partition(p, d, s);
-    if (e != hipSuccess) {
-      delete plan;
-      return hip_fail(e, "plan_scan_partition launch");
-    }
+    return hip_fail(e, "plan launch");
   }
   *plan_out = plan;
   return DPI_OK;

@@ -14,7 +14,6 @@ constexpr int kWavesPerBlock = kBlockThreads / kWaveSize;
 constexpr int kScanThreads = 256;           // plan scan: threads per block
 constexpr int kScanPerThread = 8;           // bags per thread
 constexpr int kScanTile = kScanThreads * kScanPerThread;
-constexpr int kMetaChunk = 64;              // tables per meta-upload launch
 constexpr int kDefaultChunkRows = 32;
 constexpr int kDefaultItemCost = 64;
 constexpr int kDefaultRowsPerWave = 2048;
@@ -49,14 +48,6 @@ struct alignas(16) TableInfo {
   int32_t pad;
 };
 
-// Host-side upload of up to kMetaChunk fields.
-struct MetaChunk {
-  int64_t num_rows[kMetaChunk];
-  int32_t dim[kMetaChunk];
-  int32_t col_base[kMetaChunk];
-  int32_t flags[kMetaChunk];
-};
-
 // Device pointers of a plan inside the caller's workspace.
 struct PlanDev {
   int64_t* hdr;          // [16]
@@ -64,8 +55,7 @@ struct PlanDev {
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
-  int64_t* block_sum;    // [2 * nblk]  (items, cost) per scan tile
-  int64_t* block_pre;    // [2 * nblk]  exclusive prefix of block_sum
+  int64_t* block_sum;    // [3 * nblk]  (items, cost, offsets rejected) per scan tile
   int64_t* bib;          // bag_item_base [TB+1]
   int64_t* bcb;          // bag_cost_base [TB+1]
   int64_t* wib;          // wave_item_begin [Wreq+1]
@@ -90,6 +80,15 @@ struct PlanParams {
   int64_t waves_req;
   int64_t total_d;
   const int32_t* offsets;  // device [T][B+1] or nullptr
+};
+
+// Kernel arguments of both planning launches.  packed[t] = dim | flags << 17
+// (flags as in TableInfo).
+struct PlanArgs {
+  PlanParams p;
+  PlanDev d;
+  uint32_t packed[DPI_MAX_TABLES];
+  int64_t num_rows[DPI_MAX_TABLES];
 };
 
 struct LookupArgs {
@@ -121,11 +120,7 @@ struct LookupArgs {
 };
 
 // kernel launchers (plan.hip / lookup.hip); return the launch's hipError_t
-hipError_t launch_plan_meta(const MetaChunk& chunk, int first, int count, const PlanDev& d,
-                            bool clear_status, int osize, hipStream_t s);
-hipError_t launch_plan_reduce(const PlanParams& p, const PlanDev& d, hipStream_t s);
-hipError_t launch_plan_totals(const PlanParams& p, const PlanDev& d, hipStream_t s);
-hipError_t launch_plan_scan_partition(const PlanParams& p, const PlanDev& d, hipStream_t s);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
 
 }  // namespace dpi

@@ -4,66 +4,88 @@
 // is known before it runs (§III, opportunity 2) and fuses every field's
 // lookup into one pass whose output size is fixed in advance (§IV-B), with
 // the work spread over threads afterwards (§IV-C).  This file computes that
-// plan on the device from the per-field offsets:
-//   1. field metadata (dims, row/output bytes, column bases)     plan_meta
-//   2. per scan tile: sum of item counts and costs of its bags    plan_reduce
-//   3. exclusive prefix of the tiles, per-field id bases, totals  plan_totals
-//   4. per bag: exclusive prefixes of items and cost, and the
-//      wave boundaries that fall in the bag's cost interval       plan_scan_partition
+// plan on the device from the per-field offsets, in two launches:
+//   plan_reduce    per tile of bags: sum of item counts and costs, offset
+//                  validation; tile 0 also writes the per-field table info,
+//                  column bases and id bases, and resets the per-wave arrays.
+//   plan_scan      per tile: its exclusive prefix (sum of the preceding tile
+//                  sums), the per-bag exclusive prefixes of items and cost,
+//                  and every wave boundary that falls in a bag's cost interval.
 //
-// Definitions (also the contract checked bit-for-bit against the CPU plan):
+// Definitions (the contract checked bit-for-bit against the CPU plan):
 //   bag (t, b) is number t*B + b (field-major); it holds L ids, has
 //   n = max(1, ceil(L/C)) items, item j costs rows_j*row_bytes_t
 //   + (j == 0) * out_bytes_t + K.  W = min(requested, N).  Wave w starts at
 //   the first item whose cost prefix reaches ceil(w*S/W); unless the exact
 //   flag is set, a start strictly inside a bag moves to the bag's end when
 //   the bag's cost beyond the target is at most floor(S/(2W)).
+// All target arithmetic is exact: comparisons of 128-bit products, with
+// floating point used only for first guesses that are then corrected.
 #include "dpi_internal.h"
 
 namespace dpi {
 namespace {
 
 typedef unsigned __int128 u128;
+// Kernel arguments are read in place from the constant kernarg segment
+// (scalar loads); the per-field arrays are indexed at run time.
+typedef const __attribute__((address_space(4))) PlanArgs* PA;
+typedef const __attribute__((address_space(4))) PlanParams& PPR;
+typedef const __attribute__((address_space(4))) PlanDev& PDR;
 
-__device__ __forceinline__ int64_t ceil_div_mul(int64_t w, int64_t S, int64_t W) {
-  // ceil(w * S / W) with a 128-bit intermediate
-  const u128 num = (u128)(uint64_t)w * (uint64_t)S;
-  return (int64_t)((num + (uint64_t)W - 1) / (uint64_t)W);
+__device__ __forceinline__ u128 mul128(int64_t a, int64_t b) { return (u128)(uint64_t)a * (uint64_t)b; }
+
+// smallest q >= 0 with q * den >= num (den > 0; the result fits int64)
+__device__ __forceinline__ int64_t ceil_div128(u128 num, int64_t den) {
+  int64_t q = (int64_t)((double)num / (double)den);
+  if (q < 0) q = 0;
+  while (q > 0 && mul128(q - 1, den) >= num) --q;
+  while (mul128(q, den) < num) ++q;
+  return q;
 }
 
-__device__ __forceinline__ void latch_status(int32_t* status, int bits) {
-  __hip_atomic_fetch_or(status, bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+// field of bag l: floor(l / B), exact
+__device__ __forceinline__ int64_t field_of(int64_t l, int64_t B, double inv_b) {
+  int64_t t = (int64_t)((double)l * inv_b);
+  while (t > 0 && t * B > l) --t;
+  while ((t + 1) * B <= l) ++t;
+  return t;
 }
 
-// Length of bag (t, b); validates the offsets it reads.
-__device__ __forceinline__ int64_t bag_length(const int32_t* offsets, int64_t B, int64_t t, int64_t b,
-                                              int32_t* status) {
-  if (!offsets) return 1;
-  const int32_t* o = offsets + t * (B + 1);
-  const int64_t lo = o[b], hi = o[b + 1];
-  if ((b == 0 && lo != 0) || hi < lo) {
-    latch_status(status, kStatusBadOffsets);
-    return 0;
-  }
-  return hi - lo;
-}
+__device__ __forceinline__ int32_t packed_dim(uint32_t pk) { return (int32_t)(pk & 0x1ffffu); }
+__device__ __forceinline__ int32_t packed_flags(uint32_t pk) { return (int32_t)(pk >> 17); }
 
 struct BagCost {
   int64_t items;
   int64_t cost;
 };
 
-__device__ __forceinline__ BagCost bag_cost(int64_t L, int64_t C, int64_t K, int64_t row_bytes,
-                                            int64_t out_bytes) {
-  int64_t n = (L + C - 1) / C;
+__device__ __forceinline__ BagCost bag_cost(int64_t L, PPR p, uint32_t pk) {
+  const int64_t dim = packed_dim(pk);
+  const int64_t row_bytes = dim * ((packed_flags(pk) & kTiF16) ? 2 : 4);
+  const int64_t out_bytes = dim * (p.out_dtype == DPI_F16 ? 2 : 4);
+  const uint32_t C = (uint32_t)p.C;
+  int64_t n = (int64_t)(((uint32_t)L + C - 1u) / C);   // L < 2^31, C < 2^31
   if (n < 1) n = 1;
   // every item pays K; rows sum to L; the first item also pays the output row
-  return BagCost{n, L * row_bytes + out_bytes + n * K};
+  return BagCost{n, L * row_bytes + out_bytes + n * (int64_t)p.K};
 }
 
-// Block-wide exclusive scan of a pair of int64 values (256 threads = 4 waves).
-__device__ __forceinline__ void block_scan_pair(int64_t a, int64_t b, int64_t& ea, int64_t& eb,
-                                                int64_t& ta, int64_t& tb) {
+// Length of bag (t, b) and whether its offsets are well formed.
+__device__ __forceinline__ int64_t bag_length(PPR p, int64_t t, int64_t b, bool& bad) {
+  if (!p.offsets) return 1;
+  const int32_t* o = p.offsets + t * (p.B + 1);
+  const int64_t lo = o[b], hi = o[b + 1];
+  if ((b == 0 && lo != 0) || hi < lo) {
+    bad = true;
+    return 0;
+  }
+  return hi - lo;
+}
+
+// Block-wide exclusive scan of a pair of int64 values (kScanThreads threads).
+__device__ __forceinline__ void block_scan_pair(int64_t a, int64_t b, int64_t& ea, int64_t& eb, int64_t& ta,
+                                                int64_t& tb) {
   __shared__ int64_t wsum[2][kScanThreads / kWaveSize];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   int64_t ia = a, ib = b;
@@ -96,112 +118,126 @@ __device__ __forceinline__ void block_scan_pair(int64_t a, int64_t b, int64_t& e
   __syncthreads();
 }
 
-__global__ void plan_meta_kernel(const MetaChunk chunk, int first, int count, PlanDev d,
-                                 int clear_status, int osize) {
-  const int i = threadIdx.x;
-  if (clear_status && i == 0) *d.status = 0;
-  if (i >= count) return;
-  TableInfo ti;
-  ti.num_rows = chunk.num_rows[i];
-  ti.id_base = 0;
-  ti.nnz = 0;
-  ti.dim = chunk.dim[i];
-  ti.col_base = chunk.col_base[i];
-  ti.row_bytes = chunk.dim[i] * ((chunk.flags[i] & kTiF16) ? 2 : 4);
-  ti.out_bytes = chunk.dim[i] * osize;
-  ti.flags = chunk.flags[i];
-  ti.pad = 0;
-  d.tinfo[first + i] = ti;
-  d.col_base[first + i] = chunk.col_base[i];
+__device__ __forceinline__ int64_t block_sum_i64(int64_t v) {
+  int64_t e, d0, tot, d1;
+  block_scan_pair(v, 0, e, d0, tot, d1);
+  return tot;
 }
 
-// Tile sums of (items, cost); also resets the per-wave arrays.
-__global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanParams p, PlanDev d) {
-  const int64_t tid = threadIdx.x;
+// ---------------------------------------------------------------------------
+// Launch 1: tile sums, validation, field info, wave-array reset.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x;
   const int64_t blk = blockIdx.x;
-  // per-wave arrays for the coming partition
+  const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
+
   for (int64_t w = blk * kScanThreads + tid; w < p.waves_req; w += (int64_t)gridDim.x * kScanThreads) {
     d.head_first[w] = -1;
     d.split_pieces[w] = 0;
     d.split_last[w] = -1;
     d.tickets[w] = 0;
   }
-  const int64_t first = blk * kScanTile + tid * kScanPerThread;
+
+  bool bad = false;
   int64_t items = 0, cost = 0;
-  if (first < p.TB) {
-    int64_t t = first / p.B, b = first - t * p.B;
-    const int64_t last = min(first + kScanPerThread, p.TB);
-    for (int64_t bag = first; bag < last; ++bag) {
-      const TableInfo& ti = d.tinfo[t];
-      const int64_t L = bag_length(p.offsets, p.B, t, b, d.status);
-      const BagCost bc = bag_cost(L, p.C, p.K, ti.row_bytes, ti.out_bytes);
-      items += bc.items;
-      cost += bc.cost;
-      if (++b == p.B) {
-        b = 0;
-        ++t;
+  const int64_t tile0 = blk * kScanTile;
+  for (int k = 0; k < kScanPerThread; ++k) {
+    const int64_t l = tile0 + (int64_t)k * kScanThreads + tid;   // coalesced over threads
+    if (l >= p.TB) break;
+    const int64_t t = field_of(l, p.B, inv_b);
+    const int64_t L = bag_length(p, t, l - t * p.B, bad);
+    const BagCost bc = bag_cost(L, p, pa->packed[t]);
+    items += bc.items;
+    cost += bc.cost;
+  }
+
+  if (blk == 0) {
+    // per-field info: dims -> column bases, id counts -> id bases
+    int64_t dim = 0, nnz = 0;
+    if (tid < p.T) {
+      dim = packed_dim(pa->packed[tid]);
+      nnz = p.offsets ? (int64_t)p.offsets[(int64_t)tid * (p.B + 1) + p.B] : p.B;
+      if (nnz < 0) {
+        bad = true;
+        nnz = 0;
       }
     }
+    int64_t col, idb, tot_d, tot_ids;
+    block_scan_pair(dim, nnz, col, idb, tot_d, tot_ids);
+    if (tid < p.T) {
+      TableInfo ti;
+      ti.num_rows = pa->num_rows[tid];
+      ti.id_base = idb;
+      ti.nnz = nnz;
+      ti.dim = (int32_t)dim;
+      ti.col_base = (int32_t)col;
+      ti.flags = packed_flags(pa->packed[tid]);
+      ti.row_bytes = (int32_t)dim * ((ti.flags & kTiF16) ? 2 : 4);
+      ti.out_bytes = (int32_t)dim * (p.out_dtype == DPI_F16 ? 2 : 4);
+      ti.pad = 0;
+      d.tinfo[tid] = ti;
+      d.col_base[tid] = col;
+      d.id_base[tid] = idb;
+    }
+    if (tid == 0) {
+      d.col_base[p.T] = tot_d;
+      d.id_base[p.T] = tot_ids;
+      if (tot_ids != p.total_ids) bad = true;
+    }
+    if (tid < 16) d.hdr[tid] = 0;
   }
+
   int64_t ea, eb, ta, tb;
   block_scan_pair(items, cost, ea, eb, ta, tb);
+  const int64_t any_bad = block_sum_i64(bad ? 1 : 0);
   if (tid == 0) {
-    d.block_sum[2 * blk] = ta;
-    d.block_sum[2 * blk + 1] = tb;
+    d.block_sum[3 * blk] = ta;
+    d.block_sum[3 * blk + 1] = tb;
+    d.block_sum[3 * blk + 2] = any_bad;
   }
 }
 
-// One block: prefix of the tile sums, per-field id bases, header.
-__global__ __launch_bounds__(kScanThreads) void plan_totals_kernel(const PlanParams p, PlanDev d) {
+// ---------------------------------------------------------------------------
+// Launch 2: prefixes and partition.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  PPR p = pa->p;
+  PDR d = pa->d;
   const int tid = threadIdx.x;
-  __shared__ int64_t carry[2];
-  if (tid == 0) {
-    carry[0] = 0;
-    carry[1] = 0;
-  }
-  __syncthreads();
-  for (int64_t base = 0; base < p.nblk; base += kScanThreads) {
-    const int64_t i = base + tid;
-    const int64_t a = i < p.nblk ? d.block_sum[2 * i] : 0;
-    const int64_t b = i < p.nblk ? d.block_sum[2 * i + 1] : 0;
-    int64_t ea, eb, ta, tb;
-    block_scan_pair(a, b, ea, eb, ta, tb);
-    if (i < p.nblk) {
-      d.block_pre[2 * i] = carry[0] + ea;
-      d.block_pre[2 * i + 1] = carry[1] + eb;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      carry[0] += ta;
-      carry[1] += tb;
-    }
-    __syncthreads();
-  }
-  const int64_t N = carry[0], S = carry[1];
+  const int64_t blk = blockIdx.x;
+  const int64_t nblk = p.nblk;
 
-  // per-field id bases (T <= DPI_MAX_TABLES = 256 = one value per thread)
-  int64_t nnz = 0;
-  if (tid < p.T) {
-    nnz = p.offsets ? (int64_t)p.offsets[(int64_t)tid * (p.B + 1) + p.B] : p.B;
-    if (nnz < 0) {
-      latch_status(d.status, kStatusBadOffsets);
-      nnz = 0;
+  // this tile's exclusive prefix and the totals, from the tile sums
+  int64_t pre_i = 0, pre_c = 0, tot_i = 0, tot_c = 0, err = 0;
+  for (int64_t i = tid; i < nblk; i += kScanThreads) {
+    const int64_t si = d.block_sum[3 * i], sc = d.block_sum[3 * i + 1];
+    if (i < blk) {
+      pre_i += si;
+      pre_c += sc;
     }
+    tot_i += si;
+    tot_c += sc;
+    err |= d.block_sum[3 * i + 2];
   }
-  int64_t ebase, dummy, total, dummy2;
-  block_scan_pair(nnz, 0, ebase, dummy, total, dummy2);
-  if (tid < p.T) {
-    d.id_base[tid] = ebase;
-    d.tinfo[tid].id_base = ebase;
-    d.tinfo[tid].nnz = nnz;
-  }
-  if (tid == 0) {
-    d.id_base[p.T] = total;
-    d.col_base[p.T] = p.total_d;
-    if (total != p.total_ids) latch_status(d.status, kStatusBadOffsets);
-    const int64_t W = p.waves_req < N ? p.waves_req : N;
+  int64_t e0, e1, s0, s1;
+  block_scan_pair(pre_i, pre_c, e0, e1, s0, s1);
+  pre_i = s0;
+  pre_c = s1;
+  block_scan_pair(tot_i, tot_c, e0, e1, s0, s1);
+  const int64_t N = s0, S = s1;
+  err = block_sum_i64(err);
+  const int64_t W = p.waves_req < N ? p.waves_req : N;
+
+  if (blk == 0 && tid == 0) {
+    // the split counter was zeroed by plan_reduce; other blocks add to it
     int64_t* h = d.hdr;
-    for (int k = 0; k < 16; ++k) h[k] = 0;
     h[kHdrAbi] = DPI_ABI_VERSION;
     h[kHdrT] = p.T;
     h[kHdrB] = p.B;
@@ -214,136 +250,123 @@ __global__ __launch_bounds__(kScanThreads) void plan_totals_kernel(const PlanPar
     h[kHdrItems] = N;
     h[kHdrCost] = S;
     h[kHdrTotalIds] = p.total_ids;
-    h[kHdrSplit] = 0;
     h[kHdrWaveReq] = p.waves_req;
     d.bib[p.TB] = N;
     d.bcb[p.TB] = S;
     d.wib[0] = 0;
     d.wave_bag[0] = 0;
+    // the only writer of the status word during planning; lookups latch later
+    *d.status = err ? kStatusBadOffsets : 0;
   }
-}
+  if (p.TB == 0) return;
 
-// Per bag: exclusive prefixes, then the wave starts whose targets fall in the
-// bag's cost interval (E_lo, E_hi].
-__global__ __launch_bounds__(kScanThreads) void plan_scan_partition_kernel(const PlanParams p, PlanDev d) {
-  const int64_t tid = threadIdx.x;
-  const int64_t blk = blockIdx.x;
-  const int64_t first = blk * kScanTile + tid * kScanPerThread;
-  const int64_t last = first < p.TB ? min(first + kScanPerThread, p.TB) : first;
-  int64_t t0 = 0, b0 = 0;
-  int64_t items = 0, cost = 0;
-  if (first < p.TB) {
-    t0 = first / p.B;
-    b0 = first - t0 * p.B;
-    int64_t t = t0, b = b0;
-    for (int64_t bag = first; bag < last; ++bag) {
-      const TableInfo& ti = d.tinfo[t];
-      // validation already latched by plan_reduce; lengths recomputed quietly
-      int64_t L = 1;
-      if (p.offsets) {
-        const int32_t* o = p.offsets + t * (p.B + 1);
-        L = (int64_t)o[b + 1] - o[b];
-        if (L < 0) L = 0;
-      }
-      const BagCost bc = bag_cost(L, p.C, p.K, ti.row_bytes, ti.out_bytes);
-      items += bc.items;
-      cost += bc.cost;
-      if (++b == p.B) {
-        b = 0;
-        ++t;
-      }
-    }
+  // bag costs of the tile, computed coalesced, then each thread scans
+  // kScanPerThread consecutive bags
+  __shared__ int32_t s_items[kScanTile];
+  __shared__ int64_t s_cost[kScanTile];
+  __shared__ int64_t s_pre_items[kScanTile];
+  __shared__ int64_t s_pre_cost[kScanTile];
+  const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
+  const int64_t tile0 = blk * kScanTile;
+  const int tile_n = (int)min((int64_t)kScanTile, p.TB - tile0);
+  for (int k = 0; k < kScanPerThread; ++k) {
+    const int i = k * kScanThreads + tid;
+    if (i >= tile_n) break;
+    const int64_t l = tile0 + i;
+    const int64_t t = field_of(l, p.B, inv_b);
+    bool ignored = false;   // validation was done by plan_reduce
+    const BagCost bc = bag_cost(bag_length(p, t, l - t * p.B, ignored), p, pa->packed[t]);
+    s_items[i] = (int32_t)bc.items;
+    s_cost[i] = bc.cost;
   }
-  int64_t ea, eb, ta, tb;
-  block_scan_pair(items, cost, ea, eb, ta, tb);
-  if (first >= p.TB) return;
+  __syncthreads();
+  const int first = tid * kScanPerThread;
+  int64_t ti = 0, tc = 0;
+  for (int k = 0; k < kScanPerThread && first + k < tile_n; ++k) {
+    ti += s_items[first + k];
+    tc += s_cost[first + k];
+  }
+  int64_t xi, xc, dtot0, dtot1;
+  block_scan_pair(ti, tc, xi, xc, dtot0, dtot1);
+  int64_t ib = pre_i + xi, cb = pre_c + xc;
+  for (int k = 0; k < kScanPerThread && first + k < tile_n; ++k) {
+    s_pre_items[first + k] = ib;
+    s_pre_cost[first + k] = cb;
+    ib += s_items[first + k];
+    cb += s_cost[first + k];
+  }
+  __syncthreads();
+  for (int k = 0; k < kScanPerThread; ++k) {
+    const int i = k * kScanThreads + tid;
+    if (i >= tile_n) break;
+    d.bib[tile0 + i] = s_pre_items[i];
+    d.bcb[tile0 + i] = s_pre_cost[i];
+  }
+  if (W == 0) return;
 
-  const int64_t W = d.hdr[kHdrW];
-  const int64_t S = d.hdr[kHdrCost];
+  // wave boundaries whose targets fall in each bag's cost interval
   const bool exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
-  const int64_t slack = W > 0 ? S / (2 * W) : 0;
-  int64_t ib = d.block_pre[2 * blk] + ea;
-  int64_t cb = d.block_pre[2 * blk + 1] + eb;
-  int64_t t = t0, b = b0;
-  for (int64_t bag = first; bag < last; ++bag) {
-    const TableInfo& ti = d.tinfo[t];
-    int64_t L = 1;
-    if (p.offsets) {
-      const int32_t* o = p.offsets + t * (p.B + 1);
-      L = (int64_t)o[b + 1] - o[b];
-      if (L < 0) L = 0;
-    }
-    const BagCost bc = bag_cost(L, p.C, p.K, ti.row_bytes, ti.out_bytes);
-    d.bib[bag] = ib;
-    d.bcb[bag] = cb;
-    const int64_t E_lo = cb, E_hi = cb + bc.cost;
-    if (W > 0) {
-      // first w >= 1 with ceil(w*S/W) > E_lo
-      int64_t w = (int64_t)(((u128)(uint64_t)E_lo * (uint64_t)W) / (uint64_t)S) + 1;
-      const int64_t per_item = (int64_t)p.C * ti.row_bytes + p.K;
-      int64_t w_first = -1, w_prev = -1, begin_prev = -1, pieces = 1, w_last = -1;
-      for (; w <= W; ++w) {
-        const int64_t c = ceil_div_mul(w, S, W);
-        if (c > E_hi) break;
-        // smallest j in [1, n] whose cost prefix reaches c
-        const int64_t num = c - E_lo - ti.out_bytes;
-        int64_t j = num <= 0 ? 1 : (num + per_item - 1) / per_item;
-        if (j < 1) j = 1;
-        if (j > bc.items - 1) j = bc.items;
-        bool inside = j < bc.items;
-        int64_t begin = ib + j;
-        if (inside && !exact && E_hi - c <= slack) {
-          inside = false;
-          begin = ib + bc.items;
-        }
-        d.wib[w] = begin;
-        d.wave_bag[w] = inside ? bag : bag + 1;
-        if (inside && w < W) {
-          if (w_first < 0) w_first = w - 1;   // the wave holding the bag's first item
-          d.head_first[w] = (int32_t)w_first;
-          if (w_prev >= 0 && begin_prev < begin) ++pieces;   // previous inside wave was nonempty
-          w_prev = w;
-          begin_prev = begin;
-          w_last = w;
-        }
+  const int64_t slack = S / (2 * W);
+  for (int k = 0; k < kScanPerThread && first + k < tile_n; ++k) {
+    const int i = first + k;
+    const int64_t bag = tile0 + i;
+    const int64_t n = s_items[i];
+    const int64_t E_lo = s_pre_cost[i], E_hi = E_lo + s_cost[i];
+    const int64_t ibase = s_pre_items[i];
+    // first w >= 1 with w*S > E_lo*W, i.e. ceil(w*S/W) > E_lo
+    const u128 lo_w = mul128(E_lo, W), hi_w = mul128(E_hi, W);
+    int64_t w = (int64_t)((double)lo_w / (double)S);
+    if (w < 0) w = 0;
+    while (w > 0 && mul128(w, S) > lo_w) --w;
+    while (mul128(w, S) <= lo_w) ++w;
+    if (w > W || mul128(w, S) > hi_w) continue;   // no target in this bag (the common case)
+    const int64_t t = field_of(bag, p.B, inv_b);
+    const uint32_t pk = pa->packed[t];
+    const int64_t dim = packed_dim(pk);
+    const int64_t row_bytes = dim * ((packed_flags(pk) & kTiF16) ? 2 : 4);
+    const int64_t out_bytes = dim * (p.out_dtype == DPI_F16 ? 2 : 4);
+    const int64_t per_item = (int64_t)p.C * row_bytes + p.K;
+    int64_t w_first = -1, begin_prev = -1, pieces = 1, w_last = -1;
+    for (; w <= W && mul128(w, S) <= hi_w; ++w) {
+      const int64_t c = ceil_div128(mul128(w, S), W);   // ceil(w*S/W), in (E_lo, E_hi]
+      // smallest j in [1, n] whose cost prefix reaches c
+      const int64_t num = c - E_lo - out_bytes;
+      int64_t j = num <= 0 ? 1 : ceil_div128((u128)(uint64_t)num, per_item);
+      if (j < 1) j = 1;
+      if (j > n - 1) j = n;
+      bool inside = j < n;
+      int64_t begin = ibase + j;
+      if (inside && !exact && E_hi - c <= slack) {
+        inside = false;
+        begin = ibase + n;
       }
-      if (w_first >= 0) {
-        ++pieces;   // the last inside wave always holds the bag's remaining items
-        d.split_pieces[w_first] = (int32_t)pieces;
-        d.split_last[w_first] = (int32_t)w_last;
-        atomicAdd((unsigned long long*)&d.hdr[kHdrSplit], 1ull);
+      d.wib[w] = begin;
+      d.wave_bag[w] = inside ? bag : bag + 1;
+      if (inside && w < W) {
+        if (w_first < 0) w_first = w - 1;   // the wave holding the bag's first item
+        d.head_first[w] = (int32_t)w_first;
+        if (begin_prev >= 0 && begin_prev < begin) ++pieces;   // previous inside wave was nonempty
+        begin_prev = begin;
+        w_last = w;
       }
     }
-    ib += bc.items;
-    cb += bc.cost;
-    if (++b == p.B) {
-      b = 0;
-      ++t;
+    if (w_first >= 0) {
+      ++pieces;   // the last inside wave always holds the bag's remaining items
+      d.split_pieces[w_first] = (int32_t)pieces;
+      d.split_last[w_first] = (int32_t)w_last;
+      atomicAdd((unsigned long long*)&d.hdr[kHdrSplit], 1ull);
     }
   }
 }
 
 }  // namespace
 
-hipError_t launch_plan_meta(const MetaChunk& chunk, int first, int count, const PlanDev& d,
-                            bool clear_status, int osize, hipStream_t s) {
-  hipLaunchKernelGGL(plan_meta_kernel, dim3(1), dim3(kMetaChunk), 0, s, chunk, first, count, d,
-                     clear_status ? 1 : 0, osize);
-  return hipGetLastError();
-}
-
-hipError_t launch_plan_reduce(const PlanParams& p, const PlanDev& d, hipStream_t s) {
-  hipLaunchKernelGGL(plan_reduce_kernel, dim3(p.nblk), dim3(kScanThreads), 0, s, p, d);
-  return hipGetLastError();
-}
-
-hipError_t launch_plan_totals(const PlanParams& p, const PlanDev& d, hipStream_t s) {
-  hipLaunchKernelGGL(plan_totals_kernel, dim3(1), dim3(kScanThreads), 0, s, p, d);
-  return hipGetLastError();
-}
-
-hipError_t launch_plan_scan_partition(const PlanParams& p, const PlanDev& d, hipStream_t s) {
-  hipLaunchKernelGGL(plan_scan_partition_kernel, dim3(p.nblk), dim3(kScanThreads), 0, s, p, d);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
+  const unsigned blocks = (unsigned)(a.p.nblk > 0 ? a.p.nblk : 1);
+  hipLaunchKernelGGL(plan_reduce_kernel, dim3(blocks), dim3(kScanThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(plan_scan_kernel, dim3(blocks), dim3(kScanThreads), 0, s, a);
   return hipGetLastError();
 }
 
