@@ -67,6 +67,73 @@ def read_traffic(config_key: int):
         return None
 
 
+def _counter_per_dispatch(csv_path: str, counter: str, kernel_regex: str) -> float:
+    """Mean over dispatches of a rocprofv3 counter (summed over its instances)."""
+    import csv
+    import re
+    per = {}
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter and re.search(kernel_regex, r["Kernel_Name"]):
+                per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    if not per:
+        raise SystemExit(f"no {counter} rows for /{kernel_regex}/ in {csv_path}")
+    return sum(per.values()) / len(per)
+
+
+def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_fetch_csv: str,
+                          copy_write_csv: str, copy_gib: float, commands: str, out_dir: str):
+    """HBM bytes per lookup launch from FETCH_SIZE / WRITE_SIZE passes, each scaled by
+    what the same counter reads for a plain device copy of known size."""
+    fetch = _counter_per_dispatch(fetch_csv, "FETCH_SIZE", "lookup_")
+    write = _counter_per_dispatch(write_csv, "WRITE_SIZE", "lookup_")
+    copy_bytes = copy_gib * (1 << 30)
+    cf = _counter_per_dispatch(copy_fetch_csv, "FETCH_SIZE", "copy|Copy")
+    cw = _counter_per_dispatch(copy_write_csv, "WRITE_SIZE", "copy|Copy")
+    f_scale = copy_bytes / (cf * 1024.0)
+    w_scale = copy_bytes / (cw * 1024.0)
+    hbm = fetch * 1024.0 * f_scale + write * 1024.0 * w_scale
+    path = os.path.join(out_dir, f"lookup_traffic_config{config_key}.txt")
+    with open(path, "w") as f:
+        f.write(f"# HBM traffic of the fused lookup kernel, workload config {config_key}\n")
+        f.write(f"# {WORKLOAD_TEXT[config_key]}\n")
+        f.write("# commands (run from /tmp, repository at $R):\n")
+        for line in commands.strip().splitlines():
+            f.write(f"#   {line.strip()}\n")
+        f.write("# FETCH_SIZE / WRITE_SIZE are KiB per dispatch; each is scaled by the ratio of the\n")
+        f.write("# known bytes of a plain device copy to what the same counter reads for it.\n")
+        f.write(f"kernel_source_hash: {kernel_source_hash()}\n")
+        f.write(f"fetch_kib_per_dispatch: {fetch:.1f}\n")
+        f.write(f"write_kib_per_dispatch: {write:.1f}\n")
+        f.write(f"copy_probe_bytes: {copy_bytes:.0f}\n")
+        f.write(f"copy_fetch_kib_per_dispatch: {cf:.1f}\n")
+        f.write(f"copy_write_kib_per_dispatch: {cw:.1f}\n")
+        f.write(f"fetch_scale: {f_scale:.4f}\n")
+        f.write(f"write_scale: {w_scale:.4f}\n")
+        f.write(f"hbm_read_bytes_per_launch: {fetch * 1024.0 * f_scale:.0f}\n")
+        f.write(f"hbm_write_bytes_per_launch: {write * 1024.0 * w_scale:.0f}\n")
+        f.write(f"hbm_bytes_per_launch: {hbm:.0f}\n")
+    print(path)
+
+
+def summarize_kernel_stats(stats_csv: str, out_path: str, commands: str):
+    """Condense a rocprofv3 --stats kernel_stats.csv to the library's kernels."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    keep = [r for r in rows if any(k in r["Name"] for k in ("lookup_", "plan_"))]
+    with open(out_path, "w") as f:
+        f.write("# rocprofv3 kernel statistics of the library's kernels (durations in ns)\n")
+        f.write("# commands (run from /tmp, repository at $R):\n")
+        for line in commands.strip().splitlines():
+            f.write(f"#   {line.strip()}\n")
+        f.write(f"# kernel_source_hash: {kernel_source_hash()}\n")
+        cols = [c for c in ("Calls", "TotalDurationNs", "AverageNs", "MinNs", "MaxNs", "Percentage") if c in rows[0]]
+        f.write("name | " + " | ".join(cols) + "\n")
+        for r in keep:
+            f.write(r["Name"][:90] + " | " + " | ".join(r[c] for c in cols) + "\n")
+    print(out_path)
+
+
 def cpu_baseline(cfg, samples: int):
     """Time the CPU oracle on samples [0, samples) of rotation 0, all fields."""
     sys.path.insert(0, os.path.join(ROOT, "tests"))
@@ -99,11 +166,25 @@ def main():
     ap.add_argument("--mapping", choices=["literal", "scattered"], default="literal")
     ap.add_argument("--flags", type=int, default=0)
     ap.add_argument("--num-waves", type=int, default=0)
-    ap.add_argument("--cpu-samples", type=int, default=2048)
+    ap.add_argument("--cpu-samples", type=int, default=6144)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="only run a plain device copy of this size (counter calibration)")
+    ap.add_argument("--write-traffic-profile", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                                  "COPY_WRITE_CSV"),
+                    help="write profiles/lookup_traffic_config<N>.txt from rocprofv3 counter CSVs")
+    ap.add_argument("--summarize-kernel-stats", nargs=2, metavar=("STATS_CSV", "OUT"))
+    ap.add_argument("--commands", default="", help="command lines recorded in a written profile")
+    ap.add_argument("--profile-dir", default=os.path.join(ROOT, "profiles"))
     args = ap.parse_args()
+
+    if args.write_traffic_profile:
+        write_traffic_profile(args.config, *args.write_traffic_profile, copy_gib=args.copy_probe_gib or 1.0,
+                              commands=args.commands, out_dir=args.profile_dir)
+        return
+    if args.summarize_kernel_stats:
+        summarize_kernel_stats(*args.summarize_kernel_stats, commands=args.commands)
+        return
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the lookup is a single-GPU "

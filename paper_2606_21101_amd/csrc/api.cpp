@@ -207,12 +207,12 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   }
 
   // one specialised kernel serves batches whose fields share a row class and
-  // fit a buffer descriptor (< 2 GiB each)
+  // fit a buffer descriptor (at most 4 GiB - 1 bytes each)
   const int class_mask = kTiF16 | kTiFast | (7 << kTiLprShift);
   int32_t uniform_class = row_class[0] & class_mask;
   for (int t = 0; t < num_tables; ++t) {
     const int64_t bytes = table_meta[t].num_rows * (int64_t)table_meta[t].dim * (table_meta[t].dtype == DPI_F16 ? 2 : 4);
-    if (!(row_class[t] & kTiFast) || (row_class[t] & class_mask) != uniform_class || bytes >= ((int64_t)1 << 31))
+    if (!(row_class[t] & kTiFast) || (row_class[t] & class_mask) != uniform_class || bytes > (int64_t)0xffffffffLL)
       uniform_class = -1;
   }
 

@@ -23,7 +23,7 @@
 //     arrive (agent-scope ticket) adds the partials in wave order and writes
 //     the row -- deterministic, no floating-point atomics.
 // Rows are read with buffer loads (32-bit offsets, range-checked by the
-// descriptor) when the table is below 2 GiB, with 64-bit global loads
+// descriptor) when the table is below 4 GiB, with 64-bit global loads
 // otherwise.
 //
 // Pooling: sum, or mean = fp32 sum / bag length (IEEE division); an empty bag
@@ -162,11 +162,13 @@ __device__ __forceinline__ void bag_span(KA a, const TableInfo& ti, int64_t t, i
 // 16-byte piece k of row `id` of a table.
 template <bool BUF> struct RowReader;
 template <> struct RowReader<true> {
+  // raw buffer: the descriptor's record count and the per-lane offset are
+  // unsigned 32-bit byte values, so tables up to 4 GiB - 1 bytes qualify
   __amdgpu_buffer_rsrc_t rsrc;
   uint32_t row_bytes, koff;
   __device__ RowReader(const void* table, const TableInfo& ti, int k)
       : rsrc(__builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(table), (short)0,
-                                               (int)(ti.num_rows * (int64_t)ti.row_bytes), kBufferWord3)),
+                                               (int)(uint32_t)(ti.num_rows * (int64_t)ti.row_bytes), kBufferWord3)),
         row_bytes((uint32_t)ti.row_bytes), koff((uint32_t)k * 16u) {}
   __device__ __forceinline__ raw16_t load(int32_t id) const {
     return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)((uint32_t)id * row_bytes + koff), 0, 0);
@@ -525,10 +527,9 @@ __device__ __attribute__((noinline)) void finish_call(KA a, int64_t w_first, int
   finish_piece<TOUT>(a, w_first, bag, lane);
 }
 
-// buffer descriptors hold a 32-bit byte range; offsets are formed as signed
-// 32-bit values, so tables below 2 GiB use them
+// buffer descriptors hold an unsigned 32-bit byte range
 __device__ __forceinline__ bool use_buffer(const TableInfo& ti) {
-  return ti.num_rows * (int64_t)ti.row_bytes < ((int64_t)1 << 31);
+  return ti.num_rows * (int64_t)ti.row_bytes <= (int64_t)0xffffffffLL;
 }
 
 template <typename TOUT>

@@ -133,3 +133,34 @@ def test_deterministic_and_stream():
     s.synchronize()
     assert torch.equal(a, c)
     check(tables, ids, offs, pool, 500, a)
+
+
+def test_rows_beyond_2gib_of_a_table():
+    """Rows whose byte offset exceeds 2^31 (buffer-descriptor range up to 4 GiB)
+    and a table above 4 GiB (64-bit addressing) are read correctly."""
+    rng = np.random.default_rng(9)
+    for rows, dim, dtype in ((9_000_000, 128, torch.float16), (4_500_000, 256, torch.float32)):
+        big = torch.empty((rows, dim), dtype=dtype, device="cuda")
+        hi = torch.arange(rows - 3000, rows, device="cuda")
+        lo = torch.arange(0, 3000, device="cuda")
+        vals_hi = torch.from_numpy((rng.integers(-64, 64, size=(3000, dim)) / 64.0)).to(dtype).cuda()
+        vals_lo = torch.from_numpy((rng.integers(-64, 64, size=(3000, dim)) / 64.0)).to(dtype).cuda()
+        big[hi] = vals_hi
+        big[lo] = vals_lo
+        B = 500
+        ids_np = np.concatenate([rng.integers(rows - 3000, rows, size=6 * B // 2), rng.integers(0, 3000, size=6 * B // 2)])
+        rng.shuffle(ids_np)
+        ids = torch.from_numpy(ids_np.astype(np.int32)).cuda()
+        offs = torch.arange(0, 6 * B + 1, 6, dtype=torch.int32, device="cuda").view(1, -1)
+        fl = FusedLookup([big], [0], torch.float32)
+        out = fl(ids, offs, B)
+        # reference from the two populated slices only
+        table_np = np.zeros((6000, dim), dtype=np.float32)
+        table_np[:3000] = vals_lo.float().cpu().numpy()
+        table_np[3000:] = vals_hi.float().cpu().numpy()
+        remap = np.where(ids_np >= rows - 3000, ids_np - (rows - 3000) + 3000, ids_np).astype(np.int32)
+        ref, mag = oracle.lookup([dim], [table_np.astype(np.float16 if dtype == torch.float16 else np.float32)],
+                                 remap, offs.cpu().numpy(), [0], B)
+        check_outputs(out.double().cpu().numpy(), ref, mag, dtype == torch.float16, False)
+        del big
+        torch.cuda.empty_cache()
