@@ -99,7 +99,7 @@ def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_
         f.write(f"# {WORKLOAD_TEXT[config_key]}\n")
         f.write("# commands (run from /tmp, repository at $R):\n")
         for line in commands.strip().splitlines():
-            f.write(f"#   {line.strip()}\n")
+            f.write(f"#   {_portable(line)}\n")
         f.write("# FETCH_SIZE / WRITE_SIZE are KiB per dispatch; each is scaled by the ratio of the\n")
         f.write("# known bytes of a plain device copy to what the same counter reads for it.\n")
         f.write(f"kernel_source_hash: {kernel_source_hash()}\n")
@@ -116,6 +116,12 @@ def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_
     print(path)
 
 
+def _portable(command: str) -> str:
+    """A recorded command with this checkout's absolute path written as $R."""
+    root = os.path.dirname(os.path.abspath(__file__))
+    return command.strip().replace(root, "$R")
+
+
 def summarize_kernel_stats(stats_csv: str, out_path: str, commands: str):
     """Condense a rocprofv3 --stats kernel_stats.csv to the library's kernels."""
     import csv
@@ -125,7 +131,7 @@ def summarize_kernel_stats(stats_csv: str, out_path: str, commands: str):
         f.write("# rocprofv3 kernel statistics of the library's kernels (durations in ns)\n")
         f.write("# commands (run from /tmp, repository at $R):\n")
         for line in commands.strip().splitlines():
-            f.write(f"#   {line.strip()}\n")
+            f.write(f"#   {_portable(line)}\n")
         f.write(f"# kernel_source_hash: {kernel_source_hash()}\n")
         cols = [c for c in ("Calls", "TotalDurationNs", "AverageNs", "MinNs", "MaxNs", "Percentage") if c in rows[0]]
         f.write("name | " + " | ".join(cols) + "\n")
