@@ -313,6 +313,7 @@ def main():
             "table_dtype": cfg.dtype,
             "out_dtype": cfg.out_dtype,
             "id_mapping": args.mapping,
+            "plan_flags": args.flags,
             "rotating_batches": len(batches),
             "waves": int(hdr[3]),
             "items": int(hdr[9]),

@@ -80,7 +80,9 @@ typedef enum { DPI_POOL_SUM = 0, DPI_POOL_MEAN = 1 } dpi_pooling;
 /* plan flags */
 enum {
   DPI_FLAG_EXACT_SPLIT = 1u << 1,  /* never move a wave boundary to a bag's end (many split bags) */
-  DPI_FLAG_XCD_AFFINE = 1u << 2    /* give each XCD a contiguous range of waves */
+  DPI_FLAG_LINEAR_BLOCKS = 1u << 2 /* workgroup i takes waves 4i..4i+3 (default: each XCD of the
+                                      chip takes a contiguous range of waves, so one field's rows
+                                      meet in one L2) */
 };
 
 typedef struct {

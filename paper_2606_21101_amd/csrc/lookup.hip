@@ -14,7 +14,8 @@
 //   * Interior bags: the wave stages the bags' offsets in LDS, gives each slot
 //     a contiguous run of whole bags holding about the same number of rows,
 //     and each slot walks its rows as one stream (ids prefetched one step
-//     ahead, kUnroll rows in flight), closing a bag whenever the stream
+//     ahead and shared across the slot's lanes by permutes, kUnroll rows in
+//     flight), closing a bag whenever the stream
 //     crosses the bag's end (fp32 accumulation, rows in bag order).
 //   * Few or long bags: all slots of the wave pool one bag together (rows
 //     dealt round-robin to slots, then a fixed xor-butterfly across slots).
@@ -334,11 +335,26 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
     };
 
     close_bags();   // leading empty bags
-    int32_t idn[kUnroll];
+    // ids of a group: lane k of a slot loads ids k, k + LPR, ... of the group
+    // and the slot's lanes exchange them by cross-lane permutes, so a group
+    // costs ceil(kUnroll / LPR) id loads per lane instead of kUnroll
+    constexpr int IPL = (kUnroll + LPR - 1) / LPR;
+    int32_t idm[IPL];
+    auto fetch_ids = [&](int32_t p) {
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) idn[u] = (r + u < r_end) ? ids[r + u] : -1;
+      for (int j = 0; j < IPL; ++j) {
+        const int q = k + j * LPR;
+        idm[j] = (q < kUnroll && p + q < r_end) ? ids[p + q] : -1;
+      }
+    };
+    fetch_ids(r);
     while (cur < endb) {
-      // one group of up to kUnroll rows of the current bag
+      // one group of up to kUnroll rows of the current bag; the lanes of a
+      // slot are active together, so every permute reads an active lane
+      int32_t idn[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+        idn[u] = LPR == 1 ? idm[u] : __shfl(idm[u / LPR], g * LPR + u % LPR, kWaveSize);
       const int32_t ge = min(r + kUnroll, bend);
       raw16_t raw[kUnroll];
 #pragma unroll
@@ -350,8 +366,7 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
         if (ok && col) raw[u] = rows.load(idn[u]);
       }
       // the next group starts at ge: prefetch its ids
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u) idn[u] = (ge + u < r_end) ? ids[ge + u] : -1;
+      fetch_ids(ge);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
       r = ge;
@@ -654,8 +669,10 @@ __device__ __forceinline__ void wave_body(KA a) {
     __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// five waves per SIMD: at most 96 VGPRs (512 per SIMD lane, granule 8)
 template <typename TIN, typename TOUT, int LPR>
-__global__ __launch_bounds__(kBlockThreads) void lookup_uniform_kernel(const LookupArgs args) {
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(5)))
+void lookup_uniform_kernel(const LookupArgs args) {
   (void)args;
   wave_body<Uniform<TIN, TOUT, LPR>>((KA)__builtin_amdgcn_kernarg_segment_ptr());
 }

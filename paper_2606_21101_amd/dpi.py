@@ -29,7 +29,7 @@ DPI_F16 = 1
 DPI_POOL_SUM = 0
 DPI_POOL_MEAN = 1
 DPI_FLAG_EXACT_SPLIT = 1 << 1
-DPI_FLAG_XCD_AFFINE = 1 << 2
+DPI_FLAG_LINEAR_BLOCKS = 1 << 2
 DPI_MAX_TABLES = 256
 
 

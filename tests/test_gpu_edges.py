@@ -55,7 +55,7 @@ def check(tables, ids, offs, pool, B, out, exact=False):
 def test_row_shapes(dims, dtypes):
     rng = np.random.default_rng(sum(dims))
     tables, ids, offs, pool = random_problem(rng, dims, dtypes, 37, 70)
-    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 53)):
+    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 53), (dpi.DPI_FLAG_LINEAR_BLOCKS, 0)):
         for od in (torch.float32, torch.float16):
             out, st, _, _ = run_case(tables, ids, offs, pool, 37, od, flags=flags, num_waves=W, chunk_rows=8)
             assert st == dpi.DPI_OK
@@ -133,6 +133,11 @@ def test_deterministic_and_stream():
     s.synchronize()
     assert torch.equal(a, c)
     check(tables, ids, offs, pool, 500, a)
+    # the block-to-wave order changes where waves run, not what they compute
+    kw_lin = dict(kw, flags=kw["flags"] | dpi.DPI_FLAG_LINEAR_BLOCKS)
+    d, st, _, _ = run_case(tables, ids, offs, pool, 500, **kw_lin)
+    assert st == dpi.DPI_OK
+    assert torch.equal(a, d)
 
 
 def test_rows_beyond_2gib_of_a_table():
