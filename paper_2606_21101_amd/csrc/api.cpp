@@ -38,7 +38,8 @@ struct Layout {
 Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
   Layout L{};
   const int64_t TB = T * B;
-  const int64_t nblk = (TB + kScanTile - 1) / kScanTile;
+  const int64_t tile = (int64_t)kScanThreads * plan_slabs(TB);
+  const int64_t nblk = (TB + tile - 1) / tile;
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -269,7 +270,8 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   p.flags = o.flags;
   p.B = batch;
   p.TB = (int64_t)num_tables * batch;
-  p.nblk = (int32_t)((p.TB + kScanTile - 1) / kScanTile);
+  p.slabs = plan_slabs(p.TB);
+  p.nblk = (int32_t)((p.TB + (int64_t)kScanThreads * p.slabs - 1) / ((int64_t)kScanThreads * p.slabs));
   p.total_ids = total_ids;
   p.waves_req = o.num_waves;
   p.total_d = total_d;

@@ -12,8 +12,9 @@ constexpr int kWaveSize = 64;
 constexpr int kBlockThreads = 256;          // 4 independent waves per workgroup
 constexpr int kWavesPerBlock = kBlockThreads / kWaveSize;
 constexpr int kScanThreads = 256;           // plan scan: threads per block
-constexpr int kScanPerThread = 8;           // bags per thread
-constexpr int kScanTile = kScanThreads * kScanPerThread;
+constexpr int kScanPerThread = 8;           // most bags per thread (slabs per tile)
+constexpr int kScanTile = kScanThreads * kScanPerThread;   // largest tile
+constexpr int kScanMaxTiles = 2048;          // tiles above which a tile grows to more slabs
 constexpr int kDefaultChunkRows = 32;
 constexpr int kDefaultItemCost = 64;
 constexpr int kDefaultRowsPerWave = 2048;
@@ -73,7 +74,8 @@ struct PlanParams {
   int32_t K;
   int32_t out_dtype;
   uint32_t flags;
-  int32_t nblk;
+  int32_t nblk;       // tiles of slabs * kScanThreads bags
+  int32_t slabs;      // 1, 2, 4 or 8: bags per thread
   int64_t B;
   int64_t TB;
   int64_t total_ids;
@@ -118,6 +120,15 @@ struct LookupArgs {
   int32_t uniform_class;   // TableInfo class bits shared by every field, or -1
   int64_t grid_waves;
 };
+
+// Bags per plan thread: the fewest slabs (1, 2, 4, 8) that keep the tile
+// count at most kScanMaxTiles, so small batches still spread over many blocks.
+inline int32_t plan_slabs(int64_t TB) {
+  int32_t s = 1;
+  while (s < kScanPerThread && (TB + (int64_t)kScanThreads * s - 1) / ((int64_t)kScanThreads * s) > kScanMaxTiles)
+    s <<= 1;
+  return s;
+}
 
 // kernel launchers (plan.hip / lookup.hip); return the launch's hipError_t
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);

@@ -145,15 +145,18 @@ __global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArg
 
   bool bad = false;
   int64_t items = 0, cost = 0;
-  const int64_t tile0 = blk * kScanTile;
+  const int64_t tile0 = blk * (int64_t)kScanThreads * p.slabs;
+#pragma unroll
   for (int k = 0; k < kScanPerThread; ++k) {
+    if (k >= p.slabs) break;
     const int64_t l = tile0 + (int64_t)k * kScanThreads + tid;   // coalesced over threads
-    if (l >= p.TB) break;
-    const int64_t t = field_of(l, p.B, inv_b);
-    const int64_t L = bag_length(p, t, l - t * p.B, bad);
-    const BagCost bc = bag_cost(L, p, pa->packed[t]);
-    items += bc.items;
-    cost += bc.cost;
+    if (l < p.TB) {
+      const int64_t t = field_of(l, p.B, inv_b);
+      const int64_t L = bag_length(p, t, l - t * p.B, bad);
+      const BagCost bc = bag_cost(L, p, pa->packed[t]);
+      items += bc.items;
+      cost += bc.cost;
+    }
   }
 
   if (blk == 0) {
@@ -216,6 +219,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs 
 
   // this tile's exclusive prefix and the totals, from the tile sums
   int64_t pre_i = 0, pre_c = 0, tot_i = 0, tot_c = 0, err = 0;
+#pragma unroll 4
   for (int64_t i = tid; i < nblk; i += kScanThreads) {
     const int64_t si = d.block_sum[3 * i], sc = d.block_sum[3 * i + 1];
     if (i < blk) {
@@ -260,62 +264,54 @@ __global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs 
   }
   if (p.TB == 0) return;
 
-  // bag costs of the tile, computed coalesced, then each thread scans
-  // kScanPerThread consecutive bags
-  __shared__ int32_t s_items[kScanTile];
-  __shared__ int64_t s_cost[kScanTile];
-  __shared__ int64_t s_pre_items[kScanTile];
-  __shared__ int64_t s_pre_cost[kScanTile];
+  // the tile's bags as p.slabs coalesced slabs, one after the other:
+  // thread tid holds bag tile0 + k*kScanThreads + tid of slab k; its
+  // exclusive prefix is the running total of the earlier slabs plus a block
+  // scan within the slab
   const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
-  const int64_t tile0 = blk * kScanTile;
-  const int tile_n = (int)min((int64_t)kScanTile, p.TB - tile0);
-  for (int k = 0; k < kScanPerThread; ++k) {
-    const int i = k * kScanThreads + tid;
-    if (i >= tile_n) break;
-    const int64_t l = tile0 + i;
-    const int64_t t = field_of(l, p.B, inv_b);
-    bool ignored = false;   // validation was done by plan_reduce
-    const BagCost bc = bag_cost(bag_length(p, t, l - t * p.B, ignored), p, pa->packed[t]);
-    s_items[i] = (int32_t)bc.items;
-    s_cost[i] = bc.cost;
-  }
-  __syncthreads();
-  const int first = tid * kScanPerThread;
-  int64_t ti = 0, tc = 0;
-  for (int k = 0; k < kScanPerThread && first + k < tile_n; ++k) {
-    ti += s_items[first + k];
-    tc += s_cost[first + k];
-  }
-  int64_t xi, xc, dtot0, dtot1;
-  block_scan_pair(ti, tc, xi, xc, dtot0, dtot1);
-  int64_t ib = pre_i + xi, cb = pre_c + xc;
-  for (int k = 0; k < kScanPerThread && first + k < tile_n; ++k) {
-    s_pre_items[first + k] = ib;
-    s_pre_cost[first + k] = cb;
-    ib += s_items[first + k];
-    cb += s_cost[first + k];
-  }
-  __syncthreads();
-  for (int k = 0; k < kScanPerThread; ++k) {
-    const int i = k * kScanThreads + tid;
-    if (i >= tile_n) break;
-    d.bib[tile0 + i] = s_pre_items[i];
-    d.bcb[tile0 + i] = s_pre_cost[i];
-  }
-  if (W == 0) return;
-
-  // wave boundaries whose targets fall in each bag's cost interval
+  const int64_t tile0 = blk * (int64_t)kScanThreads * p.slabs;
   const bool exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
-  const int64_t slack = S / (2 * W);
-  for (int k = 0; k < kScanPerThread && first + k < tile_n; ++k) {
-    const int i = first + k;
-    const int64_t bag = tile0 + i;
-    const int64_t n = s_items[i];
-    const int64_t E_lo = s_pre_cost[i], E_hi = E_lo + s_cost[i];
-    const int64_t ibase = s_pre_items[i];
-    // first w >= 1 with w*S > E_lo*W, i.e. ceil(w*S/W) > E_lo
+  const int64_t slack = W > 0 ? S / (2 * W) : 0;
+  const double w_per_cost = W > 0 ? (double)W / (double)S : 0.0;
+  // all slabs' bag costs first (their offset loads overlap), kept in LDS
+  __shared__ int32_t s_items[kScanPerThread][kScanThreads];
+  __shared__ int64_t s_cost[kScanPerThread][kScanThreads];
+#pragma unroll
+  for (int k = 0; k < kScanPerThread; ++k) {
+    if (k >= p.slabs) break;
+    const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
+    int64_t n = 0, bag_c = 0;
+    if (bag < p.TB) {
+      const int64_t t = field_of(bag, p.B, inv_b);
+      bool ignored = false;   // validation was done by plan_reduce
+      const BagCost bc = bag_cost(bag_length(p, t, bag - t * p.B, ignored), p, pa->packed[t]);
+      n = bc.items;
+      bag_c = bc.cost;
+    }
+    s_items[k][tid] = (int32_t)n;   // n <= max(1, L) < 2^31
+    s_cost[k][tid] = bag_c;
+  }
+  int64_t run_i = pre_i, run_c = pre_c;
+#pragma unroll 1
+  for (int k = 0; k < p.slabs; ++k) {
+    const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
+    const int64_t n = s_items[k][tid], bag_c = s_cost[k][tid];   // this thread's own entries
+    int64_t xi, xc, si, sc;
+    block_scan_pair(n, bag_c, xi, xc, si, sc);   // every thread takes part
+    const int64_t ibase = run_i + xi;
+    const int64_t E_lo = run_c + xc, E_hi = E_lo + bag_c;
+    run_i += si;
+    run_c += sc;
+    if (bag >= p.TB) continue;
+    d.bib[bag] = ibase;
+    d.bcb[bag] = E_lo;
+    if (W == 0) continue;
+
+    // wave boundaries whose targets fall in this bag's cost interval: first
+    // w >= 1 with w*S > E_lo*W, i.e. ceil(w*S/W) > E_lo; the double product
+    // is a first guess corrected by exact 128-bit comparisons
     const u128 lo_w = mul128(E_lo, W), hi_w = mul128(E_hi, W);
-    int64_t w = (int64_t)((double)lo_w / (double)S);
+    int64_t w = (int64_t)((double)E_lo * w_per_cost);
     if (w < 0) w = 0;
     while (w > 0 && mul128(w, S) > lo_w) --w;
     while (mul128(w, S) <= lo_w) ++w;
