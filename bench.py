@@ -48,11 +48,14 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def read_traffic(config_key: int):
-    """Counter-measured HBM bytes per lookup launch from profiles/, if current."""
+def read_profile(config_key: int) -> dict:
+    """Counter-measured figures of the lookup kernel from profiles/, if they
+    were taken from the current kernel sources: HBM bytes per launch and the
+    L2 hit rate (None where absent or stale)."""
     path = os.path.join(ROOT, "profiles", f"lookup_traffic_config{config_key}.txt")
+    res = {"traffic": None, "l2_hit_rate": None}
     if not os.path.exists(path):
-        return None
+        return res
     vals = {}
     with open(path) as f:
         for line in f:
@@ -60,11 +63,13 @@ def read_traffic(config_key: int):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
     if vals.get("kernel_source_hash") != kernel_source_hash():
-        return None
-    try:
-        return float(vals["hbm_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+        return res
+    for key, name in (("traffic", "hbm_bytes_per_launch"), ("l2_hit_rate", "l2_hit_rate")):
+        try:
+            res[key] = float(vals[name])
+        except (KeyError, ValueError):
+            pass
+    return res
 
 
 def _counter_per_dispatch(csv_path: str, counter: str, kernel_regex: str) -> float:
@@ -82,9 +87,11 @@ def _counter_per_dispatch(csv_path: str, counter: str, kernel_regex: str) -> flo
 
 
 def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_fetch_csv: str,
-                          copy_write_csv: str, copy_gib: float, commands: str, out_dir: str):
+                          copy_write_csv: str, copy_gib: float, commands: str, out_dir: str,
+                          l2_csv: str = None):
     """HBM bytes per lookup launch from FETCH_SIZE / WRITE_SIZE passes, each scaled by
-    what the same counter reads for a plain device copy of known size."""
+    what the same counter reads for a plain device copy of known size; optionally
+    the L2 hit rate from a TCC_HIT_sum / TCC_MISS_sum pass."""
     fetch = _counter_per_dispatch(fetch_csv, "FETCH_SIZE", "lookup_")
     write = _counter_per_dispatch(write_csv, "WRITE_SIZE", "lookup_")
     copy_bytes = copy_gib * (1 << 30)
@@ -113,6 +120,12 @@ def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_
         f.write(f"hbm_read_bytes_per_launch: {fetch * 1024.0 * f_scale:.0f}\n")
         f.write(f"hbm_write_bytes_per_launch: {write * 1024.0 * w_scale:.0f}\n")
         f.write(f"hbm_bytes_per_launch: {hbm:.0f}\n")
+        if l2_csv:
+            hit = _counter_per_dispatch(l2_csv, "TCC_HIT_sum", "lookup_")
+            miss = _counter_per_dispatch(l2_csv, "TCC_MISS_sum", "lookup_")
+            f.write(f"tcc_hit_per_dispatch: {hit:.0f}\n")
+            f.write(f"tcc_miss_per_dispatch: {miss:.0f}\n")
+            f.write(f"l2_hit_rate: {hit / (hit + miss):.4f}\n")
     print(path)
 
 
@@ -173,12 +186,16 @@ def main():
     ap.add_argument("--flags", type=int, default=0)
     ap.add_argument("--num-waves", type=int, default=0)
     ap.add_argument("--cpu-samples", type=int, default=6144)
+    ap.add_argument("--cold-steps", type=int, default=10,
+                    help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
+    ap.add_argument("--flush-mib", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="only run a plain device copy of this size (counter calibration)")
     ap.add_argument("--write-traffic-profile", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
                                                                   "COPY_WRITE_CSV"),
                     help="write profiles/lookup_traffic_config<N>.txt from rocprofv3 counter CSVs")
+    ap.add_argument("--l2-csv", default=None, help="rocprofv3 TCC_HIT_sum/TCC_MISS_sum CSV for the traffic profile")
     ap.add_argument("--summarize-kernel-stats", nargs=2, metavar=("STATS_CSV", "OUT"))
     ap.add_argument("--commands", default="", help="command lines recorded in a written profile")
     ap.add_argument("--profile-dir", default=os.path.join(ROOT, "profiles"))
@@ -186,7 +203,7 @@ def main():
 
     if args.write_traffic_profile:
         write_traffic_profile(args.config, *args.write_traffic_profile, copy_gib=args.copy_probe_gib or 1.0,
-                              commands=args.commands, out_dir=args.profile_dir)
+                              commands=args.commands, out_dir=args.profile_dir, l2_csv=args.l2_csv)
         return
     if args.summarize_kernel_stats:
         summarize_kernel_stats(*args.summarize_kernel_stats, commands=args.commands)
@@ -278,6 +295,20 @@ def main():
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
+    cold = None
+    if args.cold_steps > 0:
+        # cold series: the L2s and the 256 MB Infinity Cache are overwritten
+        # before each step, outside the timed events
+        flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
+        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.cold_steps)]
+        for i in range(args.cold_steps):
+            flush.fill_(i & 0xFF)
+            step(args.warmup + args.steps + i, cev[i])
+        torch.cuda.synchronize()
+        del flush
+        cold = {"steps": args.cold_steps, "flush_bytes": args.flush_mib << 20,
+                "p50_lookup_ms": float(np.median([e[1].elapsed_time(e[2]) for e in cev])),
+                "p50_plan_ms": float(np.median([e[0].elapsed_time(e[1]) for e in cev]))}
     plan_ms = np.array([evs[i][0].elapsed_time(evs[i][1]) for i in range(args.steps)])
     look_ms = np.array([evs[i][1].elapsed_time(evs[i][2]) for i in range(args.steps)])
     span_ms = evs[0][0].elapsed_time(evs[-1][2])
@@ -290,7 +321,7 @@ def main():
     look_mean_s = float(look_ms.mean()) / 1e3
     achieved = float(steps_alg.mean()) / look_mean_s / 1e9
     hdr = dpi.dpi_plan_export(plans[-1])["header"]
-    traffic = read_traffic(cfg.key)
+    prof = read_profile(cfg.key)
 
     line = {
         "metric": "pooled embedding rows/s",
@@ -337,8 +368,10 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": traffic,
+            "traffic": prof["traffic"],
         },
+        "l2_hit_rate": prof["l2_hit_rate"],
+        "cold": cold,
         "setup_s": setup_s,
         "kernel_source_hash": kernel_source_hash(),
     }
