@@ -37,6 +37,7 @@ WORKLOAD_TEXT = {
        "floor(LogNormal(ln 20, 0.8)) clip [0,256], Zipf(1.1) ids, even fields sum / odd fields mean",
     5: "heterogeneous: 39 fields, D in {8,16,32,64} fp32, 13 one-hot + 26 multi-hot, rows logU[10,1e7], "
        "Zipf(1.2) ids, sum",
+    6: "allocation comparison: 26 one-hot fields x 500000 rows, D=60 fp32, B=65536, Zipf(1.05) ids, sum",
 }
 
 
@@ -182,6 +183,7 @@ def main():
     ap.add_argument("--batch", type=int, default=None, help="override the batch size (heterogeneous sweep)")
     ap.add_argument("--rotations", type=int, default=4)
     ap.add_argument("--out-dtype", choices=["f16", "f32"], default=None)
+    ap.add_argument("--dim", type=int, default=None, help="override the embedding dim (allocation comparison)")
     ap.add_argument("--mapping", choices=["literal", "scattered"], default="literal")
     ap.add_argument("--flags", type=int, default=0)
     ap.add_argument("--num-waves", type=int, default=0)
@@ -234,7 +236,7 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 3}))
         return
 
-    cfg = configs.get(args.config, batch=args.batch, out_dtype=args.out_dtype)
+    cfg = configs.get(args.config, batch=args.batch, out_dtype=args.out_dtype, dim=args.dim)
     t_setup = time.perf_counter()
     tables = [G.make_table(cfg, t, dev) for t in range(cfg.num_tables)]
     batches = G.make_batches(cfg, range(args.rotations), dev, mapping=args.mapping)
@@ -338,13 +340,14 @@ def main():
         "data": "synthetic (seeded generator; stands in for Criteo-scale CTR fields)",
         "config": {
             "workload": f"config {cfg.key} " + WORKLOAD_TEXT[cfg.key]
-                        + (f" [B={cfg.batch}]" if args.batch else ""),
+                        + (f" [B={cfg.batch}]" if args.batch else "") + (f" [D={args.dim}]" if args.dim else ""),
             "global_batch": cfg.batch,
             "fields": cfg.num_tables,
             "table_dtype": cfg.dtype,
             "out_dtype": cfg.out_dtype,
             "id_mapping": args.mapping,
             "plan_flags": args.flags,
+            "allocation": "input-first" if args.flags & dpi.DPI_FLAG_INPUT_FIRST else "output-first",
             "rotating_batches": len(batches),
             "waves": int(hdr[3]),
             "items": int(hdr[9]),

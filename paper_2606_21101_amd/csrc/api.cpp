@@ -131,7 +131,7 @@ static dpi_status resolve_opts(const dpi_plan_opts* opts, int32_t T, int64_t B, 
   if (o.chunk_rows < 0 || o.item_cost_k < 0 || o.num_waves < 0)
     return fail(DPI_ERR_INVALID_ARG, "negative plan option");
   if (o.out_dtype != DPI_F32 && o.out_dtype != DPI_F16) return fail(DPI_ERR_INVALID_ARG, "bad out_dtype");
-  if (o.flags & ~(uint32_t)(DPI_FLAG_EXACT_SPLIT | DPI_FLAG_LINEAR_BLOCKS))
+  if (o.flags & ~(uint32_t)(DPI_FLAG_EXACT_SPLIT | DPI_FLAG_LINEAR_BLOCKS | DPI_FLAG_INPUT_FIRST))
     return fail(DPI_ERR_INVALID_ARG, "unknown flag bits 0x%x", o.flags);
   if (o.chunk_rows == 0) o.chunk_rows = kDefaultChunkRows;
   if (o.item_cost_k == 0) o.item_cost_k = kDefaultItemCost;
@@ -333,6 +333,7 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   a.dmax = plan->dmax;
   a.out_f16 = plan->out_dtype == DPI_F16;
   a.xcd_affine = (plan->flags & DPI_FLAG_LINEAR_BLOCKS) ? 0 : 1;
+  a.input_first = (plan->flags & DPI_FLAG_INPUT_FIRST) ? 1 : 0;
   a.uniform_class = plan->uniform_class;
   a.grid_waves = plan->waves_req;
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));

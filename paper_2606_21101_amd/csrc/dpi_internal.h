@@ -118,6 +118,7 @@ struct LookupArgs {
   int32_t out_f16;
   int32_t xcd_affine;
   int32_t uniform_class;   // TableInfo class bits shared by every field, or -1
+  int32_t input_first;     // one lane per bag instead of the plan's waves
   int64_t grid_waves;
 };
 

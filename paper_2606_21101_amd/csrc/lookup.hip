@@ -683,9 +683,111 @@ __global__ __launch_bounds__(kBlockThreads) void lookup_mixed_kernel(const Looku
   wave_body<Mixed<TOUT>>((KA)__builtin_amdgcn_kernarg_segment_ptr());
 }
 
+// ---------------------------------------------------------------------------
+// Input-first allocation (the alternative of §IV-C, kept for the paper's
+// allocation comparison): one lane per bag.  A wave takes 64 consecutive bags
+// of one field; each lane walks its own bag's rows and, 16 bytes at a time,
+// all of the row's columns, then writes its own output row.  Loads of a wave
+// touch 64 different rows and its stores 64 different output rows; the work
+// plan is used only for the field info and the offset check.
+// ---------------------------------------------------------------------------
+template <typename TIN, typename TOUT>
+__device__ __forceinline__ int input_first_bag(KA a, const TableInfo& ti, int64_t t, int64_t b) {
+  constexpr int EPL = In<TIN>::EPL;
+  constexpr int EPW = 4 / sizeof(TIN);
+  int64_t s, e;
+  bag_span(a, ti, t, b, s, e);
+  const int32_t* __restrict__ ids = a->ids + ti.id_base;
+  const char* table = reinterpret_cast<const char*>(a->tables[t]);
+  const uint32_t nrows = id_limit(ti);
+  const bool mean = is_mean(a, t) && e > s;
+  TOUT* dst = out_row<TOUT>(a, ti, b);
+  const bool vec_in = (ti.row_bytes & 15) == 0;
+  int bad = 0;
+  const int64_t pieces = vec_in ? ti.row_bytes / 16 : ti.row_bytes / 4;
+  for (int64_t q = 0; q < pieces; ++q) {
+    if (vec_in) {
+      float acc[EPL];
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+      for (int64_t r = s; r < e; ++r) {
+        const uint32_t id = (uint32_t)ids[r];
+        if (id >= nrows) {
+          bad = 1;
+          continue;
+        }
+        accumulate<TIN, EPL>(acc, *reinterpret_cast<const raw16_t*>(table + (uint64_t)id * ti.row_bytes + q * 16));
+      }
+      if (mean) {
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) acc[i] = acc[i] / (float)(e - s);
+      }
+      const int c0 = (int)q * EPL;
+      const int cn = min(EPL, ti.dim - c0);
+      if (cn == EPL && (ti.flags & kTiOutVec)) {
+        store_lane<TOUT, EPL>(dst + c0, acc, true);
+      } else {
+        for (int i = 0; i < cn; ++i) dst[c0 + i] = (TOUT)acc[i];
+      }
+    } else {
+      float acc[EPW];
+#pragma unroll
+      for (int i = 0; i < EPW; ++i) acc[i] = 0.f;
+      for (int64_t r = s; r < e; ++r) {
+        const uint32_t id = (uint32_t)ids[r];
+        if (id >= nrows) {
+          bad = 1;
+          continue;
+        }
+        const TIN* src = reinterpret_cast<const TIN*>(table + (uint64_t)id * ti.row_bytes + q * 4);
+#pragma unroll
+        for (int i = 0; i < EPW; ++i) acc[i] += (float)src[i];
+      }
+      if (mean) {
+#pragma unroll
+        for (int i = 0; i < EPW; ++i) acc[i] = acc[i] / (float)(e - s);
+      }
+#pragma unroll
+      for (int i = 0; i < EPW; ++i) dst[q * EPW + i] = (TOUT)acc[i];
+    }
+  }
+  return bad;
+}
+
+template <typename TOUT>
+__global__ __launch_bounds__(kBlockThreads) void lookup_input_first_kernel(const LookupArgs args) {
+  (void)args;
+  const KA a = (KA)__builtin_amdgcn_kernarg_segment_ptr();
+  const int lane = threadIdx.x & (kWaveSize - 1);
+  const int64_t per_field = (a->B + kWaveSize - 1) / kWaveSize;
+  const int64_t gw = (int64_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
+  if (gw >= per_field * a->T) return;
+  if (*a->status & kStatusBadOffsets) return;   // the plan rejected the offsets
+  const int64_t t = gw / per_field;
+  const int64_t b = (gw - t * per_field) * kWaveSize + lane;
+  const TableInfo ti = table_info(a, t);
+  int bad = 0;
+  if (b < a->B) {
+    bad = (ti.flags & kTiF16) ? input_first_bag<_Float16, TOUT>(a, ti, t, b)
+                              : input_first_bag<float, TOUT>(a, ti, t, b);
+  }
+  if (__any(bad) && lane == 0)
+    __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 }  // namespace
 
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s) {
+  if (a.input_first) {
+    const int64_t waves = (a.B + kWaveSize - 1) / kWaveSize * a.T;
+    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (blocks <= 0) return hipSuccess;
+    if (a.out_f16)
+      hipLaunchKernelGGL(lookup_input_first_kernel<_Float16>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL(lookup_input_first_kernel<float>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+  }
   const int64_t blocks = (a.grid_waves + kWavesPerBlock - 1) / kWavesPerBlock;
   if (blocks <= 0) return hipSuccess;
   const dim3 grid((unsigned)blocks), block(kBlockThreads);

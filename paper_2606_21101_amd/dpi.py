@@ -30,6 +30,7 @@ DPI_POOL_SUM = 0
 DPI_POOL_MEAN = 1
 DPI_FLAG_EXACT_SPLIT = 1 << 1
 DPI_FLAG_LINEAR_BLOCKS = 1 << 2
+DPI_FLAG_INPUT_FIRST = 1 << 3
 DPI_MAX_TABLES = 256
 
 

@@ -1,4 +1,4 @@
-"""The five seeded synthetic workloads of the fused multi-table lookup.
+"""The seeded synthetic workloads of the fused multi-table lookup.
 
 Each workload is a set of sparse fields (one embedding table per field,
 §IV-B), a batch size, a bag-length law per field (one-hot or multi-hot,
@@ -24,6 +24,11 @@ Readings of under-specified points (each also listed in the design doc):
     U[1, 40], each bag empty with probability 0.05, otherwise
     max(1, Poisson) clipped at 256.
   * "half tables sum, half mean": even fields sum, odd fields mean.
+
+Workload 6 is the allocation comparison of §V (output-first against
+input-first thread allocation at a batch of 65,536 and an embedding dim of
+60): 26 one-hot fields of 500,000 rows each, the paper's per-field feature
+count of its field sweep.
 """
 from __future__ import annotations
 
@@ -84,6 +89,9 @@ class Config:
     def with_out(self, out_dtype: str) -> "Config":
         return Config(**{**self.__dict__, "out_dtype": out_dtype})
 
+    def with_dim(self, dim: int) -> "Config":
+        return Config(**{**self.__dict__, "dims": (int(dim),)})
+
 
 TINY = Config(
     key=1, name="tiny-onehot", num_tables=8, batch=256, rows_lo=1000, rows_hi=1000,
@@ -114,13 +122,21 @@ HETERO = Config(
     bag=BagLaw("poisson_var", lo=0, hi=256, p_empty=0.05, mean_lo=1.0, mean_hi=40.0),
     batches=(1, 16, 128, 512, 4096))
 
-CONFIGS = {c.key: c for c in (TINY, CTR_ONEHOT, MULTIHOT, LARGE, HETERO)}
+ALLOCATION = Config(
+    key=6, name="allocation", num_tables=26, batch=65536, rows_lo=500_000, rows_hi=500_000,
+    dims=(60,), dtype=F32, out_dtype=F32, id_law="zipf", zipf_s=1.05,
+    pooling=SUM, onehot_fields=26)
+
+CONFIGS = {c.key: c for c in (TINY, CTR_ONEHOT, MULTIHOT, LARGE, HETERO, ALLOCATION)}
 
 
-def get(key: int, batch: Optional[int] = None, out_dtype: Optional[str] = None) -> Config:
+def get(key: int, batch: Optional[int] = None, out_dtype: Optional[str] = None,
+        dim: Optional[int] = None) -> Config:
     cfg = CONFIGS[int(key)]
     if batch is not None:
         cfg = cfg.with_batch(int(batch))
     if out_dtype is not None:
         cfg = cfg.with_out(out_dtype)
+    if dim is not None:
+        cfg = cfg.with_dim(int(dim))
     return cfg

@@ -55,7 +55,8 @@ def check(tables, ids, offs, pool, B, out, exact=False):
 def test_row_shapes(dims, dtypes):
     rng = np.random.default_rng(sum(dims))
     tables, ids, offs, pool = random_problem(rng, dims, dtypes, 37, 70)
-    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 53), (dpi.DPI_FLAG_LINEAR_BLOCKS, 0)):
+    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 53), (dpi.DPI_FLAG_LINEAR_BLOCKS, 0),
+                     (dpi.DPI_FLAG_INPUT_FIRST, 0)):
         for od in (torch.float32, torch.float16):
             out, st, _, _ = run_case(tables, ids, offs, pool, 37, od, flags=flags, num_waves=W, chunk_rows=8)
             assert st == dpi.DPI_OK
@@ -70,6 +71,9 @@ def test_all_bags_empty_and_zero_batch():
     out, st, _, _ = run_case(tables, ids, offs, pool, 20)
     assert st == dpi.DPI_OK
     assert torch.all(out == 0)
+    out_if, st_if, _, _ = run_case(tables, ids, offs, pool, 20, flags=dpi.DPI_FLAG_INPUT_FIRST)
+    assert st_if == dpi.DPI_OK
+    assert torch.all(out_if == 0)
     out0, st0, _, _ = run_case(tables, ids, np.zeros((2, 1), np.int32), pool, 0)
     assert st0 == dpi.DPI_OK and out0.shape == (0, 24)
 
@@ -105,6 +109,8 @@ def test_out_of_range_ids_reported_and_skipped():
     bad_ids[len(ids) - 2] = 50            # == num_rows
     out, st, _, _ = run_case(tables, bad_ids, offs, pool, 40)
     assert st == dpi.DPI_ERR_BAD_ID
+    out_if, st_if, _, _ = run_case(tables, bad_ids, offs, pool, 40, flags=dpi.DPI_FLAG_INPUT_FIRST)
+    assert st_if == dpi.DPI_ERR_BAD_ID
     # the oracle's view: out-of-range ids contribute nothing (its status is BAD_ID)
     fixed = bad_ids.copy()
     tables_z = [np.concatenate([t, np.zeros((1, t.shape[1]), t.dtype)]) for t in tables]
@@ -114,6 +120,8 @@ def test_out_of_range_ids_reported_and_skipped():
     # compare only sum-pooled columns (mean divides by the full length in both)
     out_s, _, _, _ = run_case(tables, bad_ids, offs, [0, 0], 40)
     check_outputs(out_s.double().cpu().numpy(), ref, mag, False, False)
+    out_s2, _, _, _ = run_case(tables, bad_ids, offs, [0, 0], 40, flags=dpi.DPI_FLAG_INPUT_FIRST)
+    check_outputs(out_s2.double().cpu().numpy(), ref, mag, False, False)
 
 
 def test_deterministic_and_stream():

@@ -47,11 +47,12 @@ def test_generator_same_on_gpu_and_cpu():
 
 
 @pytest.mark.parametrize("key", [1, 2])
-def test_onehot_bit_exact(key):
+@pytest.mark.parametrize("flags", [0, dpi.DPI_FLAG_INPUT_FIRST])
+def test_onehot_bit_exact(key, flags):
     cfg = configs.get(key)
     tables = gpu_tables(cfg)
     batch = G.make_batch(cfg, device="cuda")
-    out = run_gpu(cfg, tables, batch)
+    out = run_gpu(cfg, tables, batch, flags=flags)
     compare(cfg, out, exact=True)          # a one-hot lookup is a copy
 
 
@@ -62,6 +63,18 @@ def test_multihot_full():
     out = run_gpu(cfg, tables, batch)
     compare(cfg, out)
     out32 = run_gpu(cfg, tables, batch, out_dtype=torch.float32)
+    compare(cfg, out32)
+
+
+def test_multihot_input_first():
+    """The one-lane-per-bag allocation: same tolerance, and rows are summed in
+    bag order as in the default kernel's interior bags."""
+    cfg = configs.get(3)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda")
+    out = run_gpu(cfg, tables, batch, flags=dpi.DPI_FLAG_INPUT_FIRST)
+    compare(cfg, out)
+    out32 = run_gpu(cfg, tables, batch, out_dtype=torch.float32, flags=dpi.DPI_FLAG_INPUT_FIRST)
     compare(cfg, out32)
 
 
@@ -84,6 +97,23 @@ def test_hetero_sweep(batch_size):
     out2 = run_gpu(cfg, tables, batch, num_waves=max(3, batch.total_ids // 9), flags=dpi.DPI_FLAG_EXACT_SPLIT,
                    chunk_rows=4)
     compare(cfg, out2)
+    out3 = run_gpu(cfg, tables, batch, flags=dpi.DPI_FLAG_INPUT_FIRST)
+    compare(cfg, out3)
+
+
+@pytest.mark.timeout(600)
+def test_allocation_comparison_both_allocations():
+    """The allocation-comparison workload (26 one-hot fields, D=60, B=65536) in
+    both thread allocations: one-hot, so both are exact copies."""
+    cfg = configs.get(6)
+    tables = gpu_tables(cfg)
+    batch = G.make_batch(cfg, device="cuda")
+    ranges = [(0, 128), (40000, 40064), (65472, 65536)]
+    for flags in (0, dpi.DPI_FLAG_INPUT_FIRST):
+        out = run_gpu(cfg, tables, batch, flags=flags)
+        compare(cfg, out, ranges=ranges, exact=True)
+    del tables
+    torch.cuda.empty_cache()
 
 
 @pytest.fixture(scope="module")
