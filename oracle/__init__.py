@@ -34,6 +34,9 @@ def _load(path: Optional[str] = None):
                                     ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                     ctypes.c_uint32, p, p, p, p, p, p]
         lib.oracle_plan.restype = ctypes.c_int
+        lib.oracle_fm_second_order.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
+                                               ctypes.c_int32, p, p, p]
+        lib.oracle_fm_second_order.restype = ctypes.c_int
         _libs[path] = lib
     return _libs[path]
 
@@ -99,3 +102,21 @@ def plan(dims: Sequence[int], dtypes: Sequence[int], out_dtype: int, offsets: Op
     W = int(hdr[3])
     return {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib,
             "bag_cost_base": bcb, "wave_item_begin": wib[: W + 1]}
+
+
+def fm_second_order(emb: np.ndarray, num_fields: int, dim: int, with_mag: bool = True,
+                    lib_path: Optional[str] = None):
+    """Second-order FM term per sample of a [batch, row_stride] fp16/fp32 block whose
+    first num_fields * dim columns hold the fields; fp64 [batch] (and its magnitude)."""
+    lib = _load(lib_path)
+    e = np.ascontiguousarray(emb)
+    if e.dtype not in (np.float16, np.float32) or e.ndim != 2:
+        raise TypeError(e.dtype)
+    B = e.shape[0]
+    out = np.empty(B, dtype=np.float64)
+    mag = np.empty(B, dtype=np.float64) if with_mag else None
+    st = lib.oracle_fm_second_order(B, num_fields, dim, e.shape[1], 1 if e.dtype == np.float16 else 0,
+                                    _ptr(e), _ptr(out), _ptr(mag))
+    if st != OK:
+        raise OracleError(st)
+    return (out, mag) if with_mag else out

@@ -282,3 +282,32 @@ int oracle_plan(int32_t num_tables, int64_t batch, const int32_t* dims, const in
   }
   return ORACLE_OK;
 }
+
+/* ---------------------------------------------------------------------------------- */
+/* Second-order FM term (§IV-D: the explicit interaction of DeepFM holds the element- */
+/* wise square and reduce-sum operators fused there).  Written from the term's       */
+/* square-of-sum form; the tests check it against the pairwise dot-product form.     */
+/* ---------------------------------------------------------------------------------- */
+int oracle_fm_second_order(int64_t batch, int32_t num_fields, int32_t dim, int64_t row_stride,
+                           int32_t dtype, const void* emb, double* out, double* mag) {
+  if (batch < 0 || num_fields < 1 || dim < 1 || row_stride < (int64_t)num_fields * dim ||
+      (dtype != 0 && dtype != 1) || (batch > 0 && (!emb || !out)))
+    return ORACLE_BAD_ARG;
+  for (int64_t b = 0; b < batch; ++b) {
+    double y = 0.0, m = 0.0;
+    for (int32_t c = 0; c < dim; ++c) {
+      double s = 0.0, sa = 0.0, q = 0.0;
+      for (int32_t t = 0; t < num_fields; ++t) {
+        const double e = table_value(emb, dtype, b * row_stride + (int64_t)t * dim + c);
+        s += e;
+        sa += fabs(e);
+        q += e * e;
+      }
+      y += s * s - q;
+      m += sa * sa + q;
+    }
+    out[b] = 0.5 * y;
+    if (mag) mag[b] = 0.5 * m;
+  }
+  return ORACLE_OK;
+}

@@ -9,7 +9,8 @@
  * index map of the paper's multi-table lookup algorithm (§IV-B, Algorithm 1)
  * for one-hot fields, by per-field embedding_bag + concatenation, and by
  * invariants.  oracle_plan is pinned by brute-force enumeration of the work
- * items and by invariants.  The plan's format is this library's own design
+ * items and by invariants.  oracle_fm_second_order is pinned by the pairwise
+ * dot-product form of the term, closed forms and a hand-typed example.  The plan's format is this library's own design
  * (the paper prints none), so no paper value pins it.
  */
 #ifndef DPI_ORACLE_H
@@ -67,6 +68,19 @@ int oracle_plan(int32_t num_tables, int64_t batch, const int32_t* dims, const in
 
 /* bit of `flags`: boundaries are never moved to a bag end */
 #define ORACLE_FLAG_EXACT_SPLIT (1u << 1)
+
+/*
+ * Second-order factorization-machine term of DeepFM's explicit interaction
+ * module (§IV-D names it among the non-GEMM operators fused into one), over
+ * the pooled block of T fields of one dim D: for every sample b, with
+ * e[t][c] = decode(emb[b * row_stride + t * D + c]),
+ *   out[b] = 1/2 * sum over c of ((sum over t of e[t][c])^2 - sum over t of e[t][c]^2),
+ * i.e. the sum over field pairs t < u of the dot products <e[t], e[u]>.
+ * mag (optional) receives 1/2 * sum over c of ((sum_t |e|)^2 + sum_t e^2), the
+ * scale of the error bound.  dtype: 0 binary32, 1 binary16.  fp64 throughout.
+ */
+int oracle_fm_second_order(int64_t batch, int32_t num_fields, int32_t dim, int64_t row_stride,
+                           int32_t dtype, const void* emb, double* out, double* mag);
 
 #ifdef __cplusplus
 }

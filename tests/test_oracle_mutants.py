@@ -11,6 +11,7 @@ import pytest
 
 import oracle
 from oracle.build import HERE, build
+import test_fm_oracle as FP
 import test_oracle_pins as LP
 import test_plan_oracle as PP
 
@@ -37,6 +38,11 @@ MUTANTS = {
     "no_wave_clamp": ("waves_requested < N ? waves_requested : N", "waves_requested"),
     "id_base_onehot": ("int64_t nnz = offsets ? offsets[t * (B + 1) + B] : B;",
                        "int64_t nnz = offsets ? offsets[t * (B + 1) + B] : B - (t > 0);"),
+    "fm_no_half": ("out[b] = 0.5 * y;", "out[b] = y;"),
+    "fm_no_square_sum": ("y += s * s - q;", "y += s * s;"),
+    "fm_field_stride": ("b * row_stride + (int64_t)t * dim + c", "b * row_stride + (int64_t)t + c"),
+    "fm_sample_stride": ("b * row_stride + (int64_t)t * dim + c", "b * num_fields * dim + (int64_t)t * dim + c"),
+    "fm_abs_sum": ("s += e;", "s += fabs(e);"),
 }
 
 
@@ -53,6 +59,10 @@ def _pins():
         yield (lambda n: (lambda: PP.test_golden_plan(n)))(name)
     for seed in range(8):
         yield (lambda s: (lambda: PP.test_random_small_plans(s)))(seed)
+    yield FP.test_golden_fm
+    yield lambda: FP.test_equals_pairwise_dot_products(3, 5, np.float32)
+    yield lambda: FP.test_equals_pairwise_dot_products(7, 16, np.float16)
+    yield FP.test_closed_forms
 
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
