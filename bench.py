@@ -191,6 +191,8 @@ def main():
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
     ap.add_argument("--flush-mib", type=int, default=1024)
+    ap.add_argument("--fm", action="store_true",
+                    help="also time the second-order FM term over the lookup output (fields of one dim)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="only run a plain device copy of this size (counter calibration)")
@@ -297,6 +299,26 @@ def main():
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
+    fm = None
+    if args.fm:
+        dims = {cfg.dim(t) for t in range(cfg.num_tables)}
+        if len(dims) != 1:
+            raise SystemExit("--fm needs fields of one dim")
+        D = dims.pop()
+        y = torch.empty(cfg.batch, dtype=torch.float32, device=dev)
+        odt = dpi.DPI_F16 if out_dt == torch.float16 else dpi.DPI_F32
+        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps + args.warmup)]
+        for i in range(args.steps + args.warmup):
+            fev[i][0].record(stream)
+            dpi.dpi_fm_second_order(out, odt, cfg.batch, cfg.num_tables, D, total_d, y, stream=stream)
+            fev[i][1].record(stream)
+        torch.cuda.synchronize()
+        fm_ms = np.array([e[0].elapsed_time(e[1]) for e in fev[args.warmup:]])
+        fm_bytes = cfg.batch * total_d * osize + 4 * cfg.batch
+        fm_gbs = fm_bytes / (float(fm_ms.mean()) / 1e3) / 1e9
+        fm = {"kernel": "fm_kernel", "p50_ms": float(np.median(fm_ms)), "bytes_per_launch": fm_bytes,
+              "roofline": {"bound": "hbm", "achieved": fm_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                           "frac": fm_gbs / HBM_PEAK_GBS}}
     cold = None
     if args.cold_steps > 0:
         # cold series: the L2s and the 256 MB Infinity Cache are overwritten
@@ -375,6 +397,7 @@ def main():
         },
         "l2_hit_rate": prof["l2_hit_rate"],
         "cold": cold,
+        "fm_second_order": fm,
         "setup_s": setup_s,
         "kernel_source_hash": kernel_source_hash(),
     }

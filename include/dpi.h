@@ -150,6 +150,27 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
 dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids,
                       const int32_t* offsets, const int32_t* pooling, void* out, void* stream);
 
+/*
+ * Second-order factorization-machine term of DeepFM's explicit interaction
+ * over a block of T fields of one dim D -- typically dpi_lookup's output.
+ * §IV-D fuses the interaction's neighbouring non-GEMM operators (element-wise
+ * square, subtraction, reduce-sum) into one kernel; this is that kernel:
+ *   out[b] = 1/2 * sum_c ((sum_t e[b][t][c])^2 - sum_t e[b][t][c]^2),
+ *   e[b][t][c] = emb[b * row_stride + t * dim + c]  (row_stride in elements),
+ * i.e. the sum over field pairs t < u of <e[b][t], e[b][u]>.
+ *   emb:  device, dpi_dtype emb_dtype, element-aligned, read only;
+ *   out:  device fp32 [batch], fully written;  stream: hipStream_t or NULL.
+ * fp32 accumulation in a fixed order (deterministic).  Rows of dim elements
+ * that are a multiple of 16 bytes (at most 1024) with a 16-byte aligned block
+ * and row stride take the vector path; any other shape the column path.
+ * Errors: INVALID_ARG (NULL pointer with batch > 0, batch < 0, num_fields < 1,
+ * dim < 1, row_stride < num_fields * dim, bad dtype), UNSUPPORTED (dim >
+ * DPI_MAX_DIM or num_fields > 65536), MISALIGNED (emb not element-aligned,
+ * out not 4-byte aligned), HIP.
+ */
+dpi_status dpi_fm_second_order(const void* emb, int32_t emb_dtype, int64_t batch, int32_t num_fields,
+                               int32_t dim, int64_t row_stride, float* out, void* stream);
+
 /* Synchronize the plan's stream and report device-detected errors
  * (BAD_OFFSETS before BAD_ID).  Lookups on other streams must be
  * synchronized by the caller first. */

@@ -341,6 +341,36 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   return DPI_OK;
 }
 
+dpi_status dpi_fm_second_order(const void* emb, int32_t emb_dtype, int64_t batch, int32_t num_fields,
+                               int32_t dim, int64_t row_stride, float* out, void* stream) {
+  if (batch < 0) return fail(DPI_ERR_INVALID_ARG, "negative batch");
+  if (num_fields < 1 || dim < 1) return fail(DPI_ERR_INVALID_ARG, "num_fields and dim must be >= 1");
+  if (emb_dtype != DPI_F32 && emb_dtype != DPI_F16) return fail(DPI_ERR_INVALID_ARG, "bad emb_dtype");
+  if (dim > DPI_MAX_DIM || num_fields > 65536) return fail(DPI_ERR_UNSUPPORTED, "dim or num_fields too large");
+  if (row_stride < (int64_t)num_fields * dim) return fail(DPI_ERR_INVALID_ARG, "row_stride < num_fields * dim");
+  if (batch == 0) return DPI_OK;
+  if (!emb || !out) return fail(DPI_ERR_INVALID_ARG, "emb or out is NULL");
+  const int esize = emb_dtype == DPI_F16 ? 2 : 4;
+  if (reinterpret_cast<uintptr_t>(emb) % esize) return fail(DPI_ERR_MISALIGNED, "emb not element-aligned");
+  if (reinterpret_cast<uintptr_t>(out) & 3) return fail(DPI_ERR_MISALIGNED, "out not 4-byte aligned");
+  FmArgs a{};
+  a.emb = emb;
+  a.out = out;
+  a.B = batch;
+  a.row_stride = row_stride;
+  a.T = num_fields;
+  a.dim = dim;
+  a.f16 = emb_dtype == DPI_F16;
+  const int64_t field_bytes = (int64_t)dim * esize;
+  a.lpr_log = -1;
+  if (field_bytes % 16 == 0 && field_bytes <= 1024 && (row_stride * esize) % 16 == 0 &&
+      (reinterpret_cast<uintptr_t>(emb) & 15) == 0)
+    a.lpr_log = ilog2((int)(field_bytes / 16));
+  const hipError_t e = launch_fm(a, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "fm launch");
+  return DPI_OK;
+}
+
 dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
   if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
   hipError_t e = hipStreamSynchronize(plan->stream);

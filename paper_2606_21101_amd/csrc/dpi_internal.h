@@ -122,6 +122,18 @@ struct LookupArgs {
   int64_t grid_waves;
 };
 
+// Second-order FM term over a [B, row_stride] block of T fields of dim D.
+struct FmArgs {
+  const void* emb;
+  float* out;
+  int64_t B;
+  int64_t row_stride;   // elements
+  int32_t T;
+  int32_t dim;
+  int32_t f16;
+  int32_t lpr_log;      // log2 of lanes per field row on the 16-byte path, -1: column path
+};
+
 // Bags per plan thread: the fewest slabs (1, 2, 4, 8) that keep the tile
 // count at most kScanMaxTiles, so small batches still spread over many blocks.
 inline int32_t plan_slabs(int64_t TB) {
@@ -134,5 +146,6 @@ inline int32_t plan_slabs(int64_t TB) {
 // kernel launchers (plan.hip / lookup.hip); return the launch's hipError_t
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
+hipError_t launch_fm(const FmArgs& a, hipStream_t s);
 
 }  // namespace dpi

@@ -80,6 +80,8 @@ def load() -> ctypes.CDLL:
     p64 = ctypes.POINTER(i64)
     lib.dpi_plan_export.restype = ctypes.c_int
     lib.dpi_plan_export.argtypes = [vp, p64, p64, p64, p64, p64, p64]
+    lib.dpi_fm_second_order.restype = ctypes.c_int
+    lib.dpi_fm_second_order.argtypes = [vp, i32, i64, i32, i32, i64, vp, vp]
     lib.dpi_plan_destroy.restype = None
     lib.dpi_plan_destroy.argtypes = [vp]
     _lib = lib
@@ -202,6 +204,13 @@ def dpi_plan_export(plan: Plan) -> dict:
                                wib.ctypes.data_as(p64)))
     return {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib, "bag_cost_base": bcb,
             "wave_item_begin": wib}
+
+
+def dpi_fm_second_order(emb, emb_dtype: int, batch: int, num_fields: int, dim: int, row_stride: int, out,
+                        stream=None) -> None:
+    """Second-order FM term per sample of a [batch, row_stride] block (fp32 out[batch])."""
+    _check(load().dpi_fm_second_order(_ptr(emb), emb_dtype, batch, num_fields, dim, row_stride, _ptr(out),
+                                      _stream(stream)))
 
 
 def dpi_plan_destroy(plan: Plan) -> None:

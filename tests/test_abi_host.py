@@ -98,3 +98,16 @@ def test_default_waves_formula():
     w = dpi.dpi_default_waves(100, 65536, 176_805_878)
     assert w == -(-(176_805_878 + 100 * 65536) // 2048)
     assert dpi.dpi_default_waves(8, 256, 2048) == 16 * 256
+
+
+def test_fm_host_validation():
+    lib = dpi.load()
+    vp = 0x10000
+    assert lib.dpi_fm_second_order(None, dpi.DPI_F32, 0, 3, 4, 12, None, None) == dpi.DPI_OK
+    assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, -1, 3, 4, 12, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, 2, 0, 4, 12, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, 2, 3, 4, 11, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_fm_second_order(vp, 7, 2, 3, 4, 12, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, 2, 3, 70000, 1 << 20, vp, None) == dpi.DPI_ERR_UNSUPPORTED
+    assert lib.dpi_fm_second_order(vp + 2, dpi.DPI_F32, 2, 3, 4, 12, vp, None) == dpi.DPI_ERR_MISALIGNED
+    assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, 2, 3, 4, 12, vp + 2, None) == dpi.DPI_ERR_MISALIGNED
