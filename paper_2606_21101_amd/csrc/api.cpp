@@ -334,6 +334,7 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   a.out_f16 = plan->out_dtype == DPI_F16;
   a.xcd_affine = (plan->flags & DPI_FLAG_LINEAR_BLOCKS) ? 0 : 1;
   a.input_first = (plan->flags & DPI_FLAG_INPUT_FIRST) ? 1 : 0;
+  a.onehot = plan->onehot ? 1 : 0;
   a.uniform_class = plan->uniform_class;
   a.grid_waves = plan->waves_req;
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));

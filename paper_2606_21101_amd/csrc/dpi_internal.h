@@ -119,6 +119,7 @@ struct LookupArgs {
   int32_t xcd_affine;
   int32_t uniform_class;   // TableInfo class bits shared by every field, or -1
   int32_t input_first;     // one lane per bag instead of the plan's waves
+  int32_t onehot;          // no offsets: every bag holds one id
   int64_t grid_waves;
 };
 

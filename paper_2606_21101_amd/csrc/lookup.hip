@@ -684,6 +684,76 @@ __global__ __launch_bounds__(kBlockThreads) void lookup_mixed_kernel(const Looku
 }
 
 // ---------------------------------------------------------------------------
+// One-hot batches (no offsets: every bag is one id, Algorithm 1's case) of a
+// uniform row class: the pooled row is the row itself, so the plan's
+// partition is not needed.  A wave takes G * kOneHotRows consecutive samples
+// of one field; each slot copies kOneHotRows rows with all their loads in
+// flight, converting to the output dtype (a one-id mean divides by 1, which
+// is exact).
+// ---------------------------------------------------------------------------
+constexpr int kOneHotRows = 8;    // rows in flight per slot
+
+template <typename TIN, typename TOUT, int LPR>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(5)))
+void lookup_onehot_kernel(const LookupArgs args) {
+  (void)args;
+  constexpr int EPL = In<TIN>::EPL;
+  constexpr int G = kWaveSize / LPR;
+  constexpr int64_t kRowsPerWave = (int64_t)G * kOneHotRows;
+  constexpr int IPL = (kOneHotRows + LPR - 1) / LPR;
+  const KA a = (KA)__builtin_amdgcn_kernarg_segment_ptr();
+  const int lane = threadIdx.x & (kWaveSize - 1);
+  const int g = lane / LPR, k = lane % LPR;
+  const int64_t blk = a->xcd_affine ? xcd_affine_block(blockIdx.x, gridDim.x) : (int64_t)blockIdx.x;
+  const int64_t per_field = (a->B + kRowsPerWave - 1) / kRowsPerWave;
+  const int64_t gw = blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
+  if (gw >= per_field * a->T) return;
+  if (*a->status & kStatusBadOffsets) return;
+  const int64_t t = uni(gw / per_field);
+  const TableInfo ti = table_info(a, t);
+  const RowReader<true> rows(a->tables[t], ti, k);
+  const int32_t* __restrict__ ids = a->ids + ti.id_base;
+  const uint32_t nrows = id_limit(ti);
+  const bool col = k * EPL < ti.dim;
+  const bool vec = (ti.flags & kTiOutVec) != 0;
+  const int64_t b0 = (gw - t * per_field) * kRowsPerWave + (int64_t)g * kOneHotRows;
+  // ids: lane k of a slot loads ids k, k + LPR, ... and the slot exchanges them
+  int32_t idm[IPL];
+#pragma unroll
+  for (int j = 0; j < IPL; ++j) {
+    const int q = k + j * LPR;
+    idm[j] = (q < kOneHotRows && b0 + q < a->B) ? ids[b0 + q] : -1;
+  }
+  int32_t idn[kOneHotRows];
+#pragma unroll
+  for (int u = 0; u < kOneHotRows; ++u)
+    idn[u] = LPR == 1 ? idm[u] : __shfl(idm[u / LPR], g * LPR + u % LPR, kWaveSize);
+  raw16_t raw[kOneHotRows];
+  int bad = 0;
+#pragma unroll
+  for (int u = 0; u < kOneHotRows; ++u) {
+    raw[u] = raw16_t{0, 0, 0, 0};
+    const bool in_range = b0 + u < a->B;
+    const bool ok = in_range && (uint32_t)idn[u] < nrows;
+    bad |= (in_range && !ok);
+    if (ok && col) raw[u] = rows.load(idn[u]);
+  }
+  TOUT* const out_lane = out_row<TOUT>(a, ti, 0) + k * EPL;
+#pragma unroll
+  for (int u = 0; u < kOneHotRows; ++u) {
+    if (b0 + u < a->B && col) {
+      float v[EPL];
+      unpack(raw[u], v, TIN());
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) v[i] = 0.f + v[i];   // a sum from +0, as for longer bags: -0 -> +0
+      store_lane<TOUT, EPL>(out_lane + (b0 + u) * a->total_d, v, vec);
+    }
+  }
+  if (__any(bad) && lane == 0)
+    __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
 // Input-first allocation (the alternative of §IV-C, kept for the paper's
 // allocation comparison): one lane per bag.  A wave takes 64 consecutive bags
 // of one field; each lane walks its own bag's rows and, 16 bytes at a time,
@@ -786,6 +856,33 @@ hipError_t launch_lookup(const LookupArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(lookup_input_first_kernel<_Float16>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
     else
       hipLaunchKernelGGL(lookup_input_first_kernel<float>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.onehot && a.uniform_class >= 0) {
+    const int lpr = 1 << ((a.uniform_class >> kTiLprShift) & 7);
+    const int64_t rows_per_wave = (int64_t)(kWaveSize / lpr) * kOneHotRows;
+    const int64_t waves = (a.B + rows_per_wave - 1) / rows_per_wave * a.T;
+    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (blocks <= 0) return hipSuccess;
+    const dim3 grid((unsigned)blocks), block(kBlockThreads);
+    const bool f16 = (a.uniform_class & kTiF16) != 0;
+    switch ((a.uniform_class >> kTiLprShift) & 7) {
+#define DPI_CASE(L, LPR)                                                                               \
+  case L:                                                                                              \
+    if (f16 && a.out_f16)                                                                              \
+      hipLaunchKernelGGL((lookup_onehot_kernel<_Float16, _Float16, LPR>), grid, block, 0, s, a);       \
+    else if (f16)                                                                                      \
+      hipLaunchKernelGGL((lookup_onehot_kernel<_Float16, float, LPR>), grid, block, 0, s, a);          \
+    else if (a.out_f16)                                                                                \
+      hipLaunchKernelGGL((lookup_onehot_kernel<float, _Float16, LPR>), grid, block, 0, s, a);          \
+    else                                                                                               \
+      hipLaunchKernelGGL((lookup_onehot_kernel<float, float, LPR>), grid, block, 0, s, a);             \
+    break;
+      DPI_FOR_LPR(DPI_CASE)
+#undef DPI_CASE
+      default:
+        return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   }
   const int64_t blocks = (a.grid_waves + kWavesPerBlock - 1) / kWavesPerBlock;
