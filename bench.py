@@ -174,6 +174,65 @@ def cpu_baseline(cfg, samples: int):
                       f"in {dt:.3f} s ({dt * cores:.1f} thread-seconds), fp64 sequential per bag"}
 
 
+def stage_sweep(args, dev) -> dict:
+    """Host-to-device staging of one-hot features, per batch size of the
+    heterogeneous workload, over its one-hot fields.  'per_field': one pinned
+    float column per field, each copied and converted to int64 on its own
+    (the unconsolidated pipeline of the paper's breakdown), then narrowed to
+    int32 and concatenated field-major for the lookup; 'consolidated': one
+    pinned sample-major float matrix, dpi_stage_onehot (one copy, one
+    kernel).  Host wall time to ids ready on the device (synchronized), p50."""
+    import numpy as np
+    import torch
+
+    from paper_2606_21101_amd import dpi
+    from synth import configs, generate as G
+
+    base = configs.get(5)
+    T = base.onehot_fields
+    reps, warm = 200, 20
+    rows = []
+    for B in base.batches:
+        cfg = base.with_batch(B)
+        batch = G.make_batch(cfg, device="cpu")
+        ids_np = batch.ids[: T * B].numpy().reshape(T, B)          # field-major one-hot ids
+        x = torch.empty((B, T), dtype=torch.float32, pin_memory=True)
+        x.copy_(torch.from_numpy(ids_np.T.astype(np.float32)))
+        cols = [torch.empty(B, dtype=torch.float32, pin_memory=True) for _ in range(T)]
+        for t in range(T):
+            cols[t].copy_(torch.from_numpy(ids_np[t].astype(np.float32)))
+        staging = torch.empty(B * T * 4, dtype=torch.uint8, device=dev)
+        ids = torch.empty(T * B, dtype=torch.int32, device=dev)
+
+        def per_field():
+            longs = [c.to(dev, non_blocking=True).long() for c in cols]
+            out = torch.cat([v.int() for v in longs])
+            torch.cuda.synchronize()
+            return out
+
+        def consolidated():
+            dpi.dpi_stage_onehot(x, dpi.DPI_X_F32, B, T, T, staging, ids)
+            torch.cuda.synchronize()
+            return ids
+
+        if not torch.equal(per_field(), consolidated()):
+            raise SystemExit("staged ids differ")
+        res = {"batch": B, "fields": T}
+        for name, fn in (("per_field", per_field), ("consolidated", consolidated)):
+            for _ in range(warm):
+                fn()
+            ts = []
+            for _ in range(reps):
+                t0 = time.perf_counter()
+                fn()
+                ts.append(time.perf_counter() - t0)
+            res[name + "_us"] = float(np.median(ts) * 1e6)
+        res["speedup"] = res["per_field_us"] / res["consolidated_us"]
+        rows.append(res)
+    return {"metric": "one-hot input staging latency", "unit": "us", "reps": reps, "higher_is_better": False,
+            "data": "synthetic (heterogeneous workload's one-hot fields)", "results": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -191,6 +250,9 @@ def main():
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
     ap.add_argument("--flush-mib", type=int, default=1024)
+    ap.add_argument("--stage-sweep", action="store_true",
+                    help="only measure one-hot input staging latency (per-field copies and conversions "
+                         "against dpi_stage_onehot) over the heterogeneous workload's batch sizes")
     ap.add_argument("--fm", action="store_true",
                     help="also time the second-order FM term over the lookup output (fields of one dim)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -227,6 +289,10 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+
+    if args.stage_sweep:
+        print(json.dumps(stage_sweep(args, dev)), flush=True)
+        return
 
     if args.copy_probe_gib > 0:
         n = int(args.copy_probe_gib * (1 << 30)) // 4

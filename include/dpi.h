@@ -76,6 +76,7 @@ typedef enum {
 
 typedef enum { DPI_F32 = 0, DPI_F16 = 1 } dpi_dtype;
 typedef enum { DPI_POOL_SUM = 0, DPI_POOL_MEAN = 1 } dpi_pooling;
+typedef enum { DPI_X_F32 = 0, DPI_X_I64 = 1, DPI_X_I32 = 2 } dpi_x_dtype;   /* host feature matrix */
 
 /* plan flags */
 enum {
@@ -170,6 +171,30 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
  */
 dpi_status dpi_fm_second_order(const void* emb, int32_t emb_dtype, int64_t batch, int32_t num_fields,
                                int32_t dim, int64_t row_stride, float* out, void* stream);
+
+/*
+ * Input consolidation for one-hot fields (the paper's breakdown, §V: moving
+ * each field to the GPU and converting each to an integer type separately is
+ * replaced by one transfer and one conversion).  The batch's categorical
+ * features arrive as one sample-major host matrix x[batch][row_stride] whose
+ * columns [0, num_fields) hold the fields' ids (float, int64 or int32, as a
+ * data loader produces them).  One asynchronous host-to-device copy moves the
+ * matrix into `staging`, then one kernel converts and transposes it into the
+ * field-major int32 ids that dpi_plan / dpi_lookup take with offsets == NULL:
+ *   ids[t * batch + b] = x[b][t].
+ * A value that is not an integer in [0, 2^31) becomes -1, which a lookup
+ * reports as DPI_ERR_BAD_ID.
+ *   x:       host, batch * row_stride elements; pinned memory (hipHostMalloc)
+ *            makes the copy asynchronous; it must stay valid until the copy
+ *            has run (synchronize the stream before reusing it);
+ *   staging: device, 16-byte aligned, >= batch * row_stride * element size;
+ *   ids:     device int32 [num_fields * batch], 4-byte aligned.
+ * Errors: INVALID_ARG (NULL pointer with batch > 0, batch < 0, num_fields < 1,
+ * row_stride < num_fields, bad x_dtype, staging too small), MISALIGNED, HIP.
+ */
+dpi_status dpi_stage_onehot(const void* x, int32_t x_dtype, int64_t batch, int32_t num_fields,
+                            int64_t row_stride, void* staging, size_t staging_bytes, int32_t* ids,
+                            void* stream);
 
 /* Synchronize the plan's stream and report device-detected errors
  * (BAD_OFFSETS before BAD_ID).  Lookups on other streams must be

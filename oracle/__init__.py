@@ -120,3 +120,21 @@ def fm_second_order(emb: np.ndarray, num_fields: int, dim: int, with_mag: bool =
     if st != OK:
         raise OracleError(st)
     return (out, mag) if with_mag else out
+
+
+def stage_onehot(x: np.ndarray, num_fields: int) -> np.ndarray:
+    """Field-major int32 ids from a sample-major feature matrix (the transpose of
+    Algorithm 1's id matrix, §IV-B), as the input consolidation of the paper's
+    breakdown (§V) produces them: ids[t * B + b] = x[b][t] when that value is an
+    integer in [0, 2^31), else -1."""
+    v = np.asarray(x)[:, :num_fields]
+    if v.dtype.kind == "f":
+        w = v.astype(np.float64)
+        with np.errstate(invalid="ignore"):
+            ok = np.isfinite(w) & (w >= 0) & (w < 2.0 ** 31) & (w == np.trunc(w))
+        ints = np.where(ok, w, -1).astype(np.int64)
+    else:
+        w = v.astype(np.int64)
+        ok = (w >= 0) & (w < 2 ** 31)
+        ints = np.where(ok, w, -1)
+    return np.ascontiguousarray(ints.T).reshape(-1).astype(np.int32)

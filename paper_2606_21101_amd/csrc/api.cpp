@@ -372,6 +372,41 @@ dpi_status dpi_fm_second_order(const void* emb, int32_t emb_dtype, int64_t batch
   return DPI_OK;
 }
 
+dpi_status dpi_stage_onehot(const void* x, int32_t x_dtype, int64_t batch, int32_t num_fields,
+                            int64_t row_stride, void* staging, size_t staging_bytes, int32_t* ids,
+                            void* stream) {
+  if (batch < 0) return fail(DPI_ERR_INVALID_ARG, "negative batch");
+  if (num_fields < 1 || row_stride < num_fields)
+    return fail(DPI_ERR_INVALID_ARG, "num_fields must be >= 1 and <= row_stride");
+  int esize = 0;
+  switch (x_dtype) {
+    case DPI_X_F32: esize = 4; break;
+    case DPI_X_I64: esize = 8; break;
+    case DPI_X_I32: esize = 4; break;
+    default: return fail(DPI_ERR_INVALID_ARG, "bad x_dtype");
+  }
+  if (batch == 0) return DPI_OK;
+  if (!x || !staging || !ids) return fail(DPI_ERR_INVALID_ARG, "x, staging or ids is NULL");
+  const size_t bytes = (size_t)batch * (size_t)row_stride * (size_t)esize;
+  if (staging_bytes < bytes) return fail(DPI_ERR_INVALID_ARG, "staging %zu bytes, need %zu", staging_bytes, bytes);
+  if (reinterpret_cast<uintptr_t>(staging) & 15) return fail(DPI_ERR_MISALIGNED, "staging not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(x) % esize) return fail(DPI_ERR_MISALIGNED, "x not element-aligned");
+  if (reinterpret_cast<uintptr_t>(ids) & 3) return fail(DPI_ERR_MISALIGNED, "ids not 4-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(staging, x, bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  StageArgs a{};
+  a.x = staging;
+  a.ids = ids;
+  a.B = batch;
+  a.row_stride = row_stride;
+  a.T = num_fields;
+  a.x_dtype = x_dtype;
+  e = launch_stage(a, s);
+  if (e != hipSuccess) return hip_fail(e, "stage launch");
+  return DPI_OK;
+}
+
 dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
   if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
   hipError_t e = hipStreamSynchronize(plan->stream);

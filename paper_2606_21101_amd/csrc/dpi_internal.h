@@ -135,6 +135,16 @@ struct FmArgs {
   int32_t lpr_log;      // log2 of lanes per field row on the 16-byte path, -1: column path
 };
 
+// One-hot input consolidation: sample-major device matrix -> field-major ids.
+struct StageArgs {
+  const void* x;        // device copy of the host matrix
+  int32_t* ids;         // [T * B]
+  int64_t B;
+  int64_t row_stride;   // elements
+  int32_t T;
+  int32_t x_dtype;      // dpi_x_dtype
+};
+
 // Bags per plan thread: the fewest slabs (1, 2, 4, 8) that keep the tile
 // count at most kScanMaxTiles, so small batches still spread over many blocks.
 inline int32_t plan_slabs(int64_t TB) {
@@ -148,5 +158,6 @@ inline int32_t plan_slabs(int64_t TB) {
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
 hipError_t launch_fm(const FmArgs& a, hipStream_t s);
+hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 
 }  // namespace dpi

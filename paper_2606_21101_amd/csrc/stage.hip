@@ -1,0 +1,61 @@
+// Input consolidation for one-hot fields (gfx950).
+//
+// A CTR data loader hands over a batch's categorical features as one
+// sample-major matrix x[B][row_stride] (column t = field t's id, often stored
+// as float).  The paper's breakdown (§V) shows that moving every field to the
+// GPU separately and converting each one to an integer type separately costs
+// launches and copies; here the whole matrix travels in one copy and one
+// kernel converts and transposes it into the field-major int32 ids of the
+// lookup (the transpose of Algorithm 1's sample-major id matrix).
+// 64 x 64 tiles through LDS: reads along a sample's fields and writes along a
+// field's samples are both contiguous.
+#include "dpi_internal.h"
+
+namespace dpi {
+namespace {
+
+constexpr int kTile = 64;
+
+__device__ __forceinline__ int32_t to_id(float v) {
+  // an integer-valued float in [0, 2^31)
+  return (v >= 0.f && v < 2147483648.f && v == truncf(v)) ? (int32_t)v : -1;
+}
+__device__ __forceinline__ int32_t to_id(int64_t v) { return (v >= 0 && v < ((int64_t)1 << 31)) ? (int32_t)v : -1; }
+__device__ __forceinline__ int32_t to_id(int32_t v) { return v >= 0 ? v : -1; }
+
+template <typename TX>
+__global__ __launch_bounds__(kTile * 4) void stage_onehot_kernel(const StageArgs args) {
+  __shared__ int32_t tile[kTile][kTile + 1];
+  const TX* __restrict__ x = reinterpret_cast<const TX*>(args.x);
+  const int64_t b0 = (int64_t)blockIdx.x * kTile;
+  const int64_t t0 = (int64_t)blockIdx.y * kTile;
+  const int tx = threadIdx.x % kTile, ty = threadIdx.x / kTile;   // 64 x 4 threads
+  // read: rows b0 + r, columns t0 + tx (contiguous along the fields)
+  for (int r = ty; r < kTile; r += 4) {
+    const int64_t b = b0 + r, t = t0 + tx;
+    if (b < args.B && t < args.T) tile[r][tx] = to_id(x[b * args.row_stride + t]);
+  }
+  __syncthreads();
+  // write: fields t0 + r, samples b0 + tx (contiguous along the samples)
+  for (int r = ty; r < kTile; r += 4) {
+    const int64_t t = t0 + r, b = b0 + tx;
+    if (b < args.B && t < args.T) args.ids[t * args.B + b] = tile[tx][r];
+  }
+}
+
+}  // namespace
+
+hipError_t launch_stage(const StageArgs& a, hipStream_t s) {
+  if (a.B <= 0) return hipSuccess;
+  const dim3 grid((unsigned)((a.B + kTile - 1) / kTile), (unsigned)((a.T + kTile - 1) / kTile));
+  const dim3 block(kTile * 4);
+  switch (a.x_dtype) {
+    case DPI_X_F32: hipLaunchKernelGGL(stage_onehot_kernel<float>, grid, block, 0, s, a); break;
+    case DPI_X_I64: hipLaunchKernelGGL(stage_onehot_kernel<int64_t>, grid, block, 0, s, a); break;
+    case DPI_X_I32: hipLaunchKernelGGL(stage_onehot_kernel<int32_t>, grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace dpi

@@ -26,6 +26,9 @@ DPI_ERR_HIP = 7
 
 DPI_F32 = 0
 DPI_F16 = 1
+DPI_X_F32 = 0
+DPI_X_I64 = 1
+DPI_X_I32 = 2
 DPI_POOL_SUM = 0
 DPI_POOL_MEAN = 1
 DPI_FLAG_EXACT_SPLIT = 1 << 1
@@ -82,6 +85,8 @@ def load() -> ctypes.CDLL:
     lib.dpi_plan_export.argtypes = [vp, p64, p64, p64, p64, p64, p64]
     lib.dpi_fm_second_order.restype = ctypes.c_int
     lib.dpi_fm_second_order.argtypes = [vp, i32, i64, i32, i32, i64, vp, vp]
+    lib.dpi_stage_onehot.restype = ctypes.c_int
+    lib.dpi_stage_onehot.argtypes = [vp, i32, i64, i32, i64, vp, sz, vp, vp]
     lib.dpi_plan_destroy.restype = None
     lib.dpi_plan_destroy.argtypes = [vp]
     _lib = lib
@@ -211,6 +216,16 @@ def dpi_fm_second_order(emb, emb_dtype: int, batch: int, num_fields: int, dim: i
     """Second-order FM term per sample of a [batch, row_stride] block (fp32 out[batch])."""
     _check(load().dpi_fm_second_order(_ptr(emb), emb_dtype, batch, num_fields, dim, row_stride, _ptr(out),
                                       _stream(stream)))
+
+
+def dpi_stage_onehot(x, x_dtype: int, batch: int, num_fields: int, row_stride: int, staging, ids,
+                     staging_bytes: Optional[int] = None, stream=None) -> None:
+    """One host-to-device copy of a sample-major feature matrix and one conversion kernel
+    into field-major int32 ids (x: host memory, ideally pinned)."""
+    if staging_bytes is None:
+        staging_bytes = int(staging.numel() * staging.element_size())
+    _check(load().dpi_stage_onehot(_ptr(x), x_dtype, batch, num_fields, row_stride, _ptr(staging),
+                                   staging_bytes, _ptr(ids), _stream(stream)))
 
 
 def dpi_plan_destroy(plan: Plan) -> None:

@@ -111,3 +111,15 @@ def test_fm_host_validation():
     assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, 2, 3, 70000, 1 << 20, vp, None) == dpi.DPI_ERR_UNSUPPORTED
     assert lib.dpi_fm_second_order(vp + 2, dpi.DPI_F32, 2, 3, 4, 12, vp, None) == dpi.DPI_ERR_MISALIGNED
     assert lib.dpi_fm_second_order(vp, dpi.DPI_F32, 2, 3, 4, 12, vp + 2, None) == dpi.DPI_ERR_MISALIGNED
+
+
+def test_stage_host_validation():
+    lib = dpi.load()
+    vp = 0x10000
+    assert lib.dpi_stage_onehot(None, dpi.DPI_X_F32, 0, 3, 4, None, 0, None, None) == dpi.DPI_OK
+    assert lib.dpi_stage_onehot(vp, dpi.DPI_X_F32, -1, 3, 4, vp, 1 << 20, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_onehot(vp, dpi.DPI_X_F32, 2, 5, 4, vp, 1 << 20, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_onehot(vp, 9, 2, 3, 4, vp, 1 << 20, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_onehot(vp, dpi.DPI_X_I64, 2, 3, 4, vp, 63, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_onehot(vp, dpi.DPI_X_F32, 2, 3, 4, vp + 4, 1 << 20, vp, None) == dpi.DPI_ERR_MISALIGNED
+    assert lib.dpi_stage_onehot(vp, dpi.DPI_X_F32, 2, 3, 4, vp, 1 << 20, vp + 2, None) == dpi.DPI_ERR_MISALIGNED

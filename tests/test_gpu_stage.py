@@ -1,0 +1,72 @@
+"""One-hot input consolidation on the GPU (dpi_stage_onehot) against the
+oracle, bit for bit, and end to end through the lookup."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_21101_amd import dpi
+from paper_2606_21101_amd.lookup import FusedLookup
+
+pytestmark = pytest.mark.gpu
+
+XT = {dpi.DPI_X_F32: (np.float32, torch.float32), dpi.DPI_X_I64: (np.int64, torch.int64),
+      dpi.DPI_X_I32: (np.int32, torch.int32)}
+
+
+def stage(x_np, x_dtype, T):
+    B, stride = x_np.shape
+    host = torch.empty((B, stride), dtype=XT[x_dtype][1], pin_memory=True)
+    host.copy_(torch.from_numpy(x_np))
+    staging = torch.empty(max(1, B * stride * host.element_size()), dtype=torch.uint8, device="cuda")
+    ids = torch.full((max(1, T * B),), 12345, dtype=torch.int32, device="cuda")
+    dpi.dpi_stage_onehot(host, x_dtype, B, T, stride, staging, ids)
+    torch.cuda.synchronize()
+    return ids[: T * B].cpu().numpy()
+
+
+def features(rng, B, stride, x_dtype, rows=1000):
+    x = rng.integers(0, rows, size=(B, stride)).astype(np.float64)
+    bad = rng.random((B, stride)) < 0.05
+    if x_dtype == dpi.DPI_X_F32:
+        junk = rng.choice([-1.0, 0.5, 2.0 ** 31, np.nan, np.inf, -0.0, 1e10], size=int(bad.sum()))
+    else:
+        junk = rng.choice([-1, -2 ** 40, 2 ** 31, 2 ** 31 - 1, 2 ** 33], size=int(bad.sum())).astype(np.float64)
+    x[bad] = junk
+    if x_dtype == dpi.DPI_X_I32:
+        x = np.clip(x, -2 ** 31, 2 ** 31 - 1)
+    return x.astype(XT[x_dtype][0])
+
+
+@pytest.mark.parametrize("x_dtype", [dpi.DPI_X_F32, dpi.DPI_X_I64, dpi.DPI_X_I32])
+@pytest.mark.parametrize("B,T,extra", [(1, 1, 0), (1, 39, 0), (63, 13, 2), (64, 64, 0), (65, 65, 1),
+                                       (1000, 26, 13), (4096, 39, 0), (300, 130, 5)])
+def test_stage_matches_oracle(x_dtype, B, T, extra):
+    rng = np.random.default_rng(B * 1000 + T * 10 + x_dtype)
+    x = features(rng, B, T + extra, x_dtype)
+    got = stage(x, x_dtype, T)
+    assert np.array_equal(got, oracle.stage_onehot(x, T))
+
+
+def test_stage_then_lookup_equals_direct_ids():
+    rng = np.random.default_rng(9)
+    B, T, D, rows = 777, 13, 16, 500
+    tables = [torch.from_numpy((rng.standard_normal((rows, D)) * 0.01).astype(np.float32)).cuda() for _ in range(T)]
+    x = rng.integers(0, rows, size=(B, T + 2)).astype(np.float32)
+    ids_staged = torch.from_numpy(stage(x, dpi.DPI_X_F32, T)).cuda()
+    ids_direct = torch.from_numpy(np.ascontiguousarray(x[:, :T].T.astype(np.int32)).reshape(-1)).cuda()
+    fl = FusedLookup(tables)
+    assert torch.equal(fl(ids_staged, None, B), fl(ids_direct, None, B))
+
+
+def test_stage_rejects_bad_arguments():
+    staging = torch.empty(64, dtype=torch.uint8, device="cuda")
+    ids = torch.empty(8, dtype=torch.int32, device="cuda")
+    x = torch.zeros((2, 4), dtype=torch.float32, pin_memory=True)
+    for args, code in (((x, 7, 2, 4, 4), dpi.DPI_ERR_INVALID_ARG),
+                       ((x, dpi.DPI_X_F32, 2, 5, 4), dpi.DPI_ERR_INVALID_ARG),
+                       ((x, dpi.DPI_X_I64, 2, 4, 8), dpi.DPI_ERR_INVALID_ARG)):   # staging too small
+        with pytest.raises(dpi.DpiError) as ei:
+            dpi.dpi_stage_onehot(*args, staging, ids)
+        assert ei.value.status == code
+    dpi.dpi_stage_onehot(x, dpi.DPI_X_F32, 0, 4, 4, staging, ids)    # empty batch: nothing to do
