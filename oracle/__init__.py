@@ -138,3 +138,42 @@ def stage_onehot(x: np.ndarray, num_fields: int) -> np.ndarray:
         ok = (w >= 0) & (w < 2 ** 31)
         ints = np.where(ok, w, -1)
     return np.ascontiguousarray(ints.T).reshape(-1).astype(np.int32)
+
+
+def breadth_first_order(n_explicit: int, n_implicit: int):
+    """Launch queue of Algorithm 2 (§IV-E): the two interaction modules' operators
+    interleaved one by one, starting with the module that has more operators (the
+    explicit one on a tie), the longer module's remaining operators at the end.
+    Entries are ("E", i) for explicit operator i and ("I", j) for implicit operator j."""
+    if n_implicit > n_explicit:
+        first, second, n_first, n_second = "I", "E", n_implicit, n_explicit
+    else:
+        first, second, n_first, n_second = "E", "I", n_explicit, n_implicit
+    q = []
+    for i in range(n_second):
+        q.append((first, i))
+        q.append((second, i))
+    for j in range(n_second, n_first):
+        q.append((first, j))
+    return q
+
+
+def dcn_forward(x0: np.ndarray, cross_w, cross_b, mlp_w, mlp_b):
+    """The interaction modules over the pooled block x0 [B, d], in fp64:
+    explicit (a DCNv2 cross network, §IV-D): x_{l+1} = x0 * (x_l W_l^T + b_l) + x_l;
+    implicit (an MLP): h_{l+1} = max(0, h_l V_l^T + c_l).
+    Returns (x_L, h_M, mag_x, mag_h): the magnitudes are the same networks run on
+    absolute values without the ReLU, the scale of the error bounds."""
+    x0 = np.asarray(x0, np.float64)
+    ax0 = np.abs(x0)
+    x, ax = x0.copy(), ax0.copy()
+    for W, b in zip(cross_w, cross_b):
+        W, b = np.asarray(W, np.float64), np.asarray(b, np.float64)
+        x = x0 * (x @ W.T + b) + x
+        ax = ax0 * (ax @ np.abs(W).T + np.abs(b)) + ax
+    h, ah = x0.copy(), ax0.copy()
+    for V, c in zip(mlp_w, mlp_b):
+        V, c = np.asarray(V, np.float64), np.asarray(c, np.float64)
+        h = np.maximum(0.0, h @ V.T + c)
+        ah = ah @ np.abs(V).T + np.abs(c)
+    return x, h, ax, ah
