@@ -233,6 +233,58 @@ def stage_sweep(args, dev) -> dict:
             "data": "synthetic (heterogeneous workload's one-hot fields)", "results": rows}
 
 
+def sched_sweep(args, dev) -> dict:
+    """The interaction modules after the lookup (a cross network of 3 layers and
+    an MLP of 1024-512-256 over the CTR one-hot workload's pooled block,
+    B = 4096 and B = 16384, d = 26 * 16) under the three launch orders.
+    Reported per order: p50 of the whole forward (HIP events on the stream the
+    modules join), and p50 of the gap between the starts of the two modules'
+    first operators (device wall clock), the measurement of §V for
+    Algorithm 2."""
+    import numpy as np
+    import torch
+
+    from paper_2606_21101_amd import dpi
+
+    khz = dpi.dpi_wall_clock_khz()
+    rng = np.random.default_rng(2606)
+    d, n_cross, mlp = 26 * 16, 3, [1024, 512, 256]
+    cw = [torch.from_numpy((rng.standard_normal((d, d)) / np.sqrt(d)).astype(np.float32)).to(dev) for _ in range(n_cross)]
+    cb = [torch.zeros(d, device=dev) for _ in range(n_cross)]
+    mw, mb, prev = [], [], d
+    for h in mlp:
+        mw.append(torch.from_numpy((rng.standard_normal((h, prev)) / np.sqrt(prev)).astype(np.float32)).to(dev))
+        mb.append(torch.zeros(h, device=dev))
+        prev = h
+    names = {dpi.DPI_SCHED_BREADTH_FIRST: "breadth_first", dpi.DPI_SCHED_DEPTH_FIRST: "depth_first",
+             dpi.DPI_SCHED_ONE_STREAM: "one_stream"}
+    se, si = torch.cuda.Stream(), torch.cuda.Stream()
+    after = torch.cuda.current_stream()
+    results = []
+    for B in (4096, 16384):
+        head = dpi.DcnHead(B, d, cw, cb, mw, mb)
+        x0 = torch.from_numpy(rng.standard_normal((B, d)).astype(np.float32)).to(dev)
+        oc = torch.empty((B, d), device=dev)
+        om = torch.empty((B, mlp[-1]), device=dev)
+        marks = torch.zeros((args.steps + args.warmup, 2), dtype=torch.int64, device=dev)
+        row = {"batch": B}
+        for mode, name in names.items():
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps + args.warmup)]
+            for i in range(args.steps + args.warmup):
+                evs[i][0].record(after)
+                head.forward(x0, oc, om, mode, se, si, after, marks[i])
+                evs[i][1].record(after)
+                torch.cuda.synchronize()
+            ms = [e[0].elapsed_time(e[1]) for e in evs[args.warmup:]]
+            m = marks[args.warmup:].cpu().numpy().astype(np.float64)
+            gap_us = np.abs(m[:, 1] - m[:, 0]) / khz * 1e3
+            row[name] = {"p50_forward_ms": float(np.median(ms)), "p50_start_gap_us": float(np.median(gap_us))}
+        results.append(row)
+        del head
+    return {"metric": "interaction modules: forward time and start gap of the two modules", "unit": "ms / us",
+            "wall_clock_khz": khz, "cross_layers": n_cross, "mlp": mlp, "dim": d, "results": results}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -253,6 +305,8 @@ def main():
     ap.add_argument("--stage-sweep", action="store_true",
                     help="only measure one-hot input staging latency (per-field copies and conversions "
                          "against dpi_stage_onehot) over the heterogeneous workload's batch sizes")
+    ap.add_argument("--sched-sweep", action="store_true",
+                    help="only measure the interaction modules under the three launch orders (Algorithm 2)")
     ap.add_argument("--fm", action="store_true",
                     help="also time the second-order FM term over the lookup output (fields of one dim)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -292,6 +346,9 @@ def main():
 
     if args.stage_sweep:
         print(json.dumps(stage_sweep(args, dev)), flush=True)
+        return
+    if args.sched_sweep:
+        print(json.dumps(sched_sweep(args, dev)), flush=True)
         return
 
     if args.copy_probe_gib > 0:

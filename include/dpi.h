@@ -196,6 +196,76 @@ dpi_status dpi_stage_onehot(const void* x, int32_t x_dtype, int64_t batch, int32
                             int64_t row_stride, void* staging, size_t staging_bytes, int32_t* ids,
                             void* stream);
 
+/*
+ * Breadth-first two-stream scheduling of the interaction modules (§IV-E,
+ * Algorithm 2).  A model's explicit interaction module (e.g. a cross network)
+ * and implicit one (an MLP) are independent, so each gets a stream; the host
+ * enqueues their operators interleaved one by one, starting with the module
+ * that has more operators (the explicit one on a tie) and ending with the
+ * longer module's remaining operators, so both modules start at once.
+ * An operator is a host callback that enqueues its work on the stream given.
+ */
+enum { DPI_SCHED_BREADTH_FIRST = 0,   /* Algorithm 2's queue, two streams */
+       DPI_SCHED_DEPTH_FIRST = 1,     /* all explicit operators, then all implicit ones, two streams */
+       DPI_SCHED_ONE_STREAM = 2 };    /* depth-first on stream_explicit only (no overlap) */
+
+typedef struct {
+  dpi_status (*launch)(void* ctx, void* stream);   /* enqueue on `stream` (a hipStream_t) */
+  void* ctx;
+} dpi_op;
+
+/* Algorithm 2's queue for n_explicit and n_implicit operators: order[k] = i
+ * for explicit operator i, -(j + 1) for implicit operator j; order holds
+ * n_explicit + n_implicit entries.  Host only. */
+dpi_status dpi_breadth_first_order(int32_t n_explicit, int32_t n_implicit, int32_t* order);
+
+/* Enqueue both modules' operators in `mode`'s order on their streams.  Both
+ * streams first wait for the work already enqueued on `after` (e.g. the
+ * lookup); `after` then waits for both.  Streams are caller-owned, default
+ * priority.  An operator's error stops the enqueueing and is returned. */
+dpi_status dpi_launch_two_streams(const dpi_op* explicit_ops, int32_t n_explicit, const dpi_op* implicit_ops,
+                                  int32_t n_implicit, int32_t mode, void* stream_explicit, void* stream_implicit,
+                                  void* after);
+
+/* Tick rate in kHz of the device wall clock that dpi_dcn_forward's marks read. */
+int64_t dpi_wall_clock_khz(void);
+
+/*
+ * Interaction head of the paper's DCN-style models over the pooled block
+ * x0 [batch][dim] (fp32, row-major), to drive the scheduler with real work:
+ *   explicit: a DCNv2 cross network, x_{l+1} = x0 * (x_l W_l^T + b_l) + x_l,
+ *             W_l [dim][dim], b_l [dim], l < n_cross;  out_cross = x_{n_cross};
+ *   implicit: an MLP, h_{l+1} = max(0, h_l V_l^T + c_l), h_0 = x0,
+ *             V_l [mlp_dims[l]][previous dim], c_l [mlp_dims[l]];  out_mlp = h_{n_mlp}.
+ * Each GEMM is a rocBLAS fp32 GEMM; the element-wise run after it is one fused
+ * kernel (the non-GEMM fusion of §IV-D).  All pointers are device memory owned
+ * by the caller; biases and activations 16-byte aligned when their row length
+ * is a multiple of 4.  The head borrows the weights and a workspace of
+ * dpi_dcn_workspace_bytes (256-byte aligned) and owns a rocBLAS handle (which
+ * manages its own device workspace).  One forward in flight per head.
+ */
+typedef struct {
+  int64_t batch;
+  int32_t dim;
+  int32_t n_cross;
+  int32_t n_mlp;
+  const int32_t* mlp_dims;          /* host [n_mlp] */
+  const float* const* cross_w;      /* host [n_cross] of device pointers */
+  const float* const* cross_b;
+  const float* const* mlp_w;        /* host [n_mlp] of device pointers */
+  const float* const* mlp_b;
+} dpi_dcn_desc;
+
+typedef struct dpi_dcn_s* dpi_dcn_t;
+
+size_t dpi_dcn_workspace_bytes(const dpi_dcn_desc* desc);   /* 0 on invalid arguments */
+dpi_status dpi_dcn_create(const dpi_dcn_desc* desc, void* workspace, size_t workspace_bytes, dpi_dcn_t* out);
+/* marks: NULL, or device uint64 [2] receiving the device wall clock when each
+ * module's first operator starts (explicit, implicit). */
+dpi_status dpi_dcn_forward(dpi_dcn_t head, const float* x0, float* out_cross, float* out_mlp, int32_t mode,
+                           void* stream_explicit, void* stream_implicit, void* after, uint64_t* marks);
+void dpi_dcn_destroy(dpi_dcn_t head);
+
 /* Synchronize the plan's stream and report device-detected errors
  * (BAD_OFFSETS before BAD_ID).  Lookups on other streams must be
  * synchronized by the caller first. */

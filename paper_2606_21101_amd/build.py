@@ -7,7 +7,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdpi.so")
-SOURCES = ["api.cpp", "plan.hip", "lookup.hip", "fm.hip", "stage.hip"]
+SOURCES = ["api.cpp", "plan.hip", "lookup.hip", "fm.hip", "stage.hip", "interact.hip", "sched.cpp"]
 ARCH = os.environ.get("DPI_OFFLOAD_ARCH", "gfx950")
 
 HIPCC_FLAGS = [
@@ -30,7 +30,8 @@ def build(verbose: bool = False) -> str:
             print(" ".join(cmd), flush=True)
         subprocess.check_call(cmd)
         objs.append(obj)
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", LIB + ".tmp", *objs]
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", LIB + ".tmp", *objs,
+           "-L/opt/rocm/lib", "-lrocblas"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.check_call(cmd)

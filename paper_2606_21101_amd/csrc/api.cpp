@@ -81,6 +81,19 @@ int ilog2(int x) {
 
 }  // namespace
 
+// error helpers for the other host files (not part of the C ABI)
+__attribute__((visibility("hidden"))) dpi_status dpi_fail_status(dpi_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+__attribute__((visibility("hidden"))) dpi_status dpi_hip_status(hipError_t e, const char* what) {
+  return hip_fail(e, what);
+}
+
 struct dpi_plan_s {
   int32_t T;
   int64_t B;

@@ -2,6 +2,8 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 #include <stdint.h>
 
 #include "dpi.h"
@@ -159,5 +161,11 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
 hipError_t launch_fm(const FmArgs& a, hipStream_t s);
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);
+// interaction modules' fused element-wise operators (16-byte alignment of all
+// pointers is required when n is a multiple of 4)
+hipError_t launch_cross_fuse(const float* x0, const float* y, const float* bias, const float* x, float* out,
+                             int64_t rows, int32_t n, hipStream_t s);
+hipError_t launch_bias_relu(float* z, const float* bias, int64_t rows, int32_t n, hipStream_t s);
+hipError_t launch_mark(uint64_t* slot, hipStream_t s);
 
 }  // namespace dpi

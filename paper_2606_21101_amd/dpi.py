@@ -34,6 +34,9 @@ DPI_POOL_MEAN = 1
 DPI_FLAG_EXACT_SPLIT = 1 << 1
 DPI_FLAG_LINEAR_BLOCKS = 1 << 2
 DPI_FLAG_INPUT_FIRST = 1 << 3
+DPI_SCHED_BREADTH_FIRST = 0
+DPI_SCHED_DEPTH_FIRST = 1
+DPI_SCHED_ONE_STREAM = 2
 DPI_MAX_TABLES = 256
 
 
@@ -44,6 +47,20 @@ class dpi_table_meta(ctypes.Structure):
 class dpi_plan_opts(ctypes.Structure):
     _fields_ = [("chunk_rows", ctypes.c_int32), ("item_cost_k", ctypes.c_int32), ("num_waves", ctypes.c_int64),
                 ("out_dtype", ctypes.c_int32), ("flags", ctypes.c_uint32)]
+
+
+DPI_OP_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p)
+
+
+class dpi_op(ctypes.Structure):
+    _fields_ = [("launch", DPI_OP_FN), ("ctx", ctypes.c_void_p)]
+
+
+class dpi_dcn_desc(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("dim", ctypes.c_int32), ("n_cross", ctypes.c_int32),
+                ("n_mlp", ctypes.c_int32), ("mlp_dims", ctypes.POINTER(ctypes.c_int32)),
+                ("cross_w", ctypes.POINTER(ctypes.c_void_p)), ("cross_b", ctypes.POINTER(ctypes.c_void_p)),
+                ("mlp_w", ctypes.POINTER(ctypes.c_void_p)), ("mlp_b", ctypes.POINTER(ctypes.c_void_p))]
 
 
 class DpiError(RuntimeError):
@@ -87,6 +104,20 @@ def load() -> ctypes.CDLL:
     lib.dpi_fm_second_order.argtypes = [vp, i32, i64, i32, i32, i64, vp, vp]
     lib.dpi_stage_onehot.restype = ctypes.c_int
     lib.dpi_stage_onehot.argtypes = [vp, i32, i64, i32, i64, vp, sz, vp, vp]
+    lib.dpi_breadth_first_order.restype = ctypes.c_int
+    lib.dpi_breadth_first_order.argtypes = [i32, i32, ctypes.POINTER(i32)]
+    lib.dpi_launch_two_streams.restype = ctypes.c_int
+    lib.dpi_launch_two_streams.argtypes = [ctypes.POINTER(dpi_op), i32, ctypes.POINTER(dpi_op), i32, i32, vp, vp, vp]
+    lib.dpi_wall_clock_khz.restype = i64
+    lib.dpi_wall_clock_khz.argtypes = []
+    lib.dpi_dcn_workspace_bytes.restype = sz
+    lib.dpi_dcn_workspace_bytes.argtypes = [ctypes.POINTER(dpi_dcn_desc)]
+    lib.dpi_dcn_create.restype = ctypes.c_int
+    lib.dpi_dcn_create.argtypes = [ctypes.POINTER(dpi_dcn_desc), vp, sz, ctypes.POINTER(vp)]
+    lib.dpi_dcn_forward.restype = ctypes.c_int
+    lib.dpi_dcn_forward.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, vp]
+    lib.dpi_dcn_destroy.restype = None
+    lib.dpi_dcn_destroy.argtypes = [vp]
     lib.dpi_plan_destroy.restype = None
     lib.dpi_plan_destroy.argtypes = [vp]
     _lib = lib
@@ -226,6 +257,63 @@ def dpi_stage_onehot(x, x_dtype: int, batch: int, num_fields: int, row_stride: i
         staging_bytes = int(staging.numel() * staging.element_size())
     _check(load().dpi_stage_onehot(_ptr(x), x_dtype, batch, num_fields, row_stride, _ptr(staging),
                                    staging_bytes, _ptr(ids), _stream(stream)))
+
+
+def dpi_breadth_first_order(n_explicit: int, n_implicit: int) -> list:
+    """Algorithm 2's queue: i for explicit operator i, -(j + 1) for implicit operator j."""
+    n = n_explicit + n_implicit
+    arr = (ctypes.c_int32 * max(1, n))()
+    _check(load().dpi_breadth_first_order(n_explicit, n_implicit, arr))
+    return [int(arr[k]) for k in range(n)]
+
+
+def dpi_launch_two_streams(explicit_ops, implicit_ops, mode: int, stream_explicit, stream_implicit, after) -> None:
+    """explicit_ops / implicit_ops: sequences of dpi_op."""
+    ne, ni = len(explicit_ops), len(implicit_ops)
+    ea = (dpi_op * max(1, ne))(*explicit_ops)
+    ia = (dpi_op * max(1, ni))(*implicit_ops)
+    _check(load().dpi_launch_two_streams(ea, ne, ia, ni, mode, _stream(stream_explicit), _stream(stream_implicit),
+                                         _stream(after)))
+
+
+def dpi_wall_clock_khz() -> int:
+    return int(load().dpi_wall_clock_khz())
+
+
+class DcnHead:
+    """dpi_dcn_t over torch fp32 weights (kept alive here): cross network + MLP."""
+
+    def __init__(self, batch: int, dim: int, cross_w, cross_b, mlp_w, mlp_b, device=None):
+        import torch
+        lib = load()
+        self.keep = [list(cross_w), list(cross_b), list(mlp_w), list(mlp_b)]
+        self.mlp_dims = [int(w.shape[0]) for w in mlp_w]
+        dims = (ctypes.c_int32 * len(self.mlp_dims))(*self.mlp_dims)
+        ptrs = [(ctypes.c_void_p * max(1, len(v)))(*[_ptr(t) for t in v]) for v in self.keep]
+        self._c = (dims, ptrs)
+        self.desc = dpi_dcn_desc(batch, dim, len(cross_w), len(mlp_w), dims, ptrs[0], ptrs[1], ptrs[2], ptrs[3])
+        need = int(lib.dpi_dcn_workspace_bytes(ctypes.byref(self.desc)))
+        if need == 0:
+            raise DpiError(DPI_ERR_INVALID_ARG, "dpi_dcn_workspace_bytes failed")
+        dev = device if device is not None else cross_w[0].device
+        self.ws = torch.empty(need + 256, dtype=torch.uint8, device=dev)
+        base = _ptr(self.ws)
+        off = (-base) % 256
+        h = ctypes.c_void_p()
+        _check(lib.dpi_dcn_create(ctypes.byref(self.desc), base + off, need, ctypes.byref(h)))
+        self.handle = h.value
+        self.batch, self.dim = batch, dim
+
+    def forward(self, x0, out_cross, out_mlp, mode: int = DPI_SCHED_BREADTH_FIRST, stream_explicit=None,
+                stream_implicit=None, after=None, marks=None) -> None:
+        _check(load().dpi_dcn_forward(ctypes.c_void_p(self.handle), _ptr(x0), _ptr(out_cross), _ptr(out_mlp), mode,
+                                      _stream(stream_explicit), _stream(stream_implicit), _stream(after),
+                                      _ptr(marks)))
+
+    def __del__(self):
+        if getattr(self, "handle", None) and _lib is not None:
+            _lib.dpi_dcn_destroy(ctypes.c_void_p(self.handle))
+            self.handle = None
 
 
 def dpi_plan_destroy(plan: Plan) -> None:

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def declared_functions():
     text = open(os.path.join(ROOT, "include", "dpi.h")).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dpi_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(dpi_[a-z_]+)\s*\((?!\s*\*)", text)))
 
 
 def test_exports_every_declared_symbol():
@@ -123,3 +123,27 @@ def test_stage_host_validation():
     assert lib.dpi_stage_onehot(vp, dpi.DPI_X_I64, 2, 3, 4, vp, 63, vp, None) == dpi.DPI_ERR_INVALID_ARG
     assert lib.dpi_stage_onehot(vp, dpi.DPI_X_F32, 2, 3, 4, vp + 4, 1 << 20, vp, None) == dpi.DPI_ERR_MISALIGNED
     assert lib.dpi_stage_onehot(vp, dpi.DPI_X_F32, 2, 3, 4, vp, 1 << 20, vp + 2, None) == dpi.DPI_ERR_MISALIGNED
+
+
+def test_breadth_first_order_matches_oracle():
+    import oracle
+    for ne in range(6):
+        for ni in range(6):
+            got = dpi.dpi_breadth_first_order(ne, ni)
+            want = [i if k == "E" else -(i + 1) for k, i in oracle.breadth_first_order(ne, ni)]
+            assert got == want
+
+
+def test_scheduler_host_validation():
+    lib = dpi.load()
+    none = (dpi.dpi_op * 1)()
+    assert lib.dpi_breadth_first_order(-1, 2, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_breadth_first_order(1, 2, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_launch_two_streams(none, 1, none, 1, 0, None, None, None) == dpi.DPI_ERR_INVALID_ARG  # no launch fn
+    assert lib.dpi_launch_two_streams(None, 1, None, 0, 0, None, None, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_launch_two_streams(none, 0, none, 0, 9, None, None, None) == dpi.DPI_ERR_INVALID_ARG
+    d = dpi.dpi_dcn_desc()
+    assert lib.dpi_dcn_workspace_bytes(ctypes.byref(d)) == 0          # batch 0, no layers
+    out = ctypes.c_void_p()
+    assert lib.dpi_dcn_create(ctypes.byref(d), None, 0, ctypes.byref(out)) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_dcn_forward(None, None, None, None, 0, None, None, None, None) == dpi.DPI_ERR_INVALID_ARG
