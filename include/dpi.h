@@ -18,9 +18,10 @@
  *
  * Memory and streams
  *   - The caller owns every device buffer (tables, ids, offsets, out,
- *     workspace).  The library allocates only the small host object behind
- *     dpi_plan_t.  A plan borrows its workspace: the workspace must outlive
- *     the plan and every lookup issued with it.
+ *     workspace).  The library allocates only the small host objects behind
+ *     dpi_plan_t and dpi_dcn_t (the latter also holds a rocBLAS handle, which
+ *     manages device memory of its own).  A plan borrows its workspace: the
+ *     workspace must outlive the plan and every lookup issued with it.
  *   - dpi_plan and dpi_lookup validate host-visible arguments synchronously,
  *     enqueue kernels on `stream` (a hipStream_t; NULL = default stream) and
  *     return without synchronizing.  Device-detected errors (malformed
