@@ -305,6 +305,10 @@ def main():
     ap.add_argument("--stage-sweep", action="store_true",
                     help="only measure one-hot input staging latency (per-field copies and conversions "
                          "against dpi_stage_onehot) over the heterogeneous workload's batch sizes")
+    ap.add_argument("--inflight", type=int, default=2,
+                    help="also time a series with this many batches in flight (each with its own stream, "
+                         "workspace and output, so one batch's plan overlaps another's lookup, as in a "
+                         "serving loop); 1: no such series.  value stays the one-batch-at-a-time series")
     ap.add_argument("--sched-sweep", action="store_true",
                     help="only measure the interaction modules under the three launch orders (Algorithm 2)")
     ap.add_argument("--fm", action="store_true",
@@ -422,6 +426,43 @@ def main():
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
+    inflight = None
+    if args.inflight > 1:
+        # steps dealt round-robin to `inflight` streams, each with its own
+        # workspace and output; one batch's plan overlaps another's lookup
+        n = args.inflight
+        streams = [torch.cuda.Stream() for _ in range(n)]
+        wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n)]
+        outs = [torch.empty_like(out) for _ in range(n)]
+        keep = []
+
+        def step_on(i, k):
+            bt = batches[i % len(batches)]
+            p = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, fl.opts(args.num_waves), wss[k],
+                             ws_bytes, stream=streams[k])
+            dpi.dpi_lookup(p, tables, bt.ids, bt.offsets, pool, outs[k], stream=streams[k])
+            keep.append(p)
+
+        for i in range(args.warmup):
+            step_on(i, i % n)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for st in streams:
+            st.wait_stream(stream)
+        for i in range(args.steps):
+            step_on(args.warmup + i, i % n)
+        for st in streams:
+            stream.wait_stream(st)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        span = e0.elapsed_time(e1)
+        for p in keep[-n:]:
+            if dpi.dpi_plan_sync_status(p) != dpi.DPI_OK:
+                raise SystemExit("device reported an error in the in-flight series")
+        inflight = {"batches_in_flight": n, "ms_per_step": span / args.steps,
+                    "value": sum(nnz_list[(args.warmup + i) % len(batches)] for i in range(args.steps)) / (span / 1e3)}
+        del keep
     fm = None
     if args.fm:
         dims = {cfg.dim(t) for t in range(cfg.num_tables)}
@@ -521,6 +562,7 @@ def main():
         "l2_hit_rate": prof["l2_hit_rate"],
         "cold": cold,
         "fm_second_order": fm,
+        "inflight": inflight,
         "setup_s": setup_s,
         "kernel_source_hash": kernel_source_hash(),
     }
