@@ -154,14 +154,17 @@ def summarize_kernel_stats(stats_csv: str, out_path: str, commands: str):
     print(out_path)
 
 
-def cpu_baseline(cfg, samples: int):
-    """Time the CPU oracle on samples [0, samples) of rotation 0, all fields."""
+def cpu_baseline(cfg, samples: int, threads: int = 0):
+    """Time the CPU oracle on samples [0, samples) of rotation 0, all fields
+    (on `threads` threads; 0: every host core available)."""
     sys.path.insert(0, os.path.join(ROOT, "tests"))
     import oracle
     from cases import sub_problem
     cores = len(os.sched_getaffinity(0))
     if os.environ.get("OMP_NUM_THREADS", "").isdigit():
         cores = min(cores, int(os.environ["OMP_NUM_THREADS"]))
+    if threads > 0:
+        cores = min(cores, threads)
     samples = min(samples, cfg.batch)
     p = sub_problem(cfg, ranges=[(0, samples)])
     nnz = int(len(p["ids"]))
@@ -299,6 +302,7 @@ def main():
     ap.add_argument("--flags", type=int, default=0)
     ap.add_argument("--num-waves", type=int, default=0)
     ap.add_argument("--cpu-samples", type=int, default=6144)
+    ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads for cpu_baseline (0: all cores)")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
     ap.add_argument("--flush-mib", type=int, default=1024)
@@ -567,7 +571,7 @@ def main():
         "kernel_source_hash": kernel_source_hash(),
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_samples)
+        line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_samples, args.cpu_threads)
     print(json.dumps(line), flush=True)
 
 

@@ -107,8 +107,12 @@ typedef struct {
 typedef struct dpi_plan_s* dpi_plan_t;
 
 /*
- * Default wave count for a batch: max(16 * compute units of the current
- * device, ceil((total_ids + T*B) / 2048)).  The plan uses
+ * Default wave count for a batch: max(min(16 * compute units of the current
+ * device, max(ceil(T*B / 8), min(ceil(total_ids / 32) + T*B, 8 * T))),
+ * ceil((total_ids + T*B) / 2048), 1).  Large batches get about 2048 rows and
+ * bags per wave; small ones enough waves for the device but about 8 bags per
+ * wave (fewer bags cut between waves), and tiny ones about one work item per
+ * wave (a wave walks its fields one after the other).  The plan uses
  * W = min(requested, number of work items).
  */
 int64_t dpi_default_waves(int32_t num_tables, int64_t batch, int64_t total_ids);

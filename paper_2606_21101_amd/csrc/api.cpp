@@ -30,6 +30,8 @@ dpi_status hip_fail(hipError_t e, const char* what) {
 
 inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+constexpr int64_t kSmallBagsPerWave = 8;   // default-wave rule for small batches
+
 struct Layout {
   size_t hdr, status, tinfo, col_base, id_base, block_sum, bib, bcb, wib, wave_bag, head_first, split_pieces,
       split_last, tickets, partial, total;
@@ -133,8 +135,18 @@ const char* dpi_status_str(dpi_status s) {
 
 int64_t dpi_default_waves(int32_t num_tables, int64_t batch, int64_t total_ids) {
   const int64_t units = total_ids + (int64_t)num_tables * batch;
+  // large batches: about kDefaultRowsPerWave rows and bags per wave.  Small
+  // ones: enough waves for the GPU, but at least ~8 bags per wave (fewer,
+  // shorter waves cut bags between waves, and a cut bag costs a cross-wave
+  // combine) and few fields per wave when batches are tiny (a wave walks its
+  // fields one after the other).
   const int64_t by_work = (units + kDefaultRowsPerWave - 1) / kDefaultRowsPerWave;
-  return std::max<int64_t>((int64_t)kDefaultWavesPerCU * device_cus(), by_work);
+  const int64_t bags = (int64_t)num_tables * batch;
+  const int64_t items_bound = (total_ids + kDefaultChunkRows - 1) / kDefaultChunkRows + bags;
+  const int64_t by_bags = std::max<int64_t>((bags + kSmallBagsPerWave - 1) / kSmallBagsPerWave,
+                                            std::min<int64_t>(items_bound, kSmallBagsPerWave * num_tables));
+  const int64_t fill = std::min<int64_t>((int64_t)kDefaultWavesPerCU * device_cus(), by_bags);
+  return std::max<int64_t>(std::max<int64_t>(fill, by_work), 1);
 }
 
 static dpi_status resolve_opts(const dpi_plan_opts* opts, int32_t T, int64_t B, int64_t total_ids,
@@ -349,7 +361,10 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   a.input_first = (plan->flags & DPI_FLAG_INPUT_FIRST) ? 1 : 0;
   a.onehot = plan->onehot ? 1 : 0;
   a.uniform_class = plan->uniform_class;
-  a.grid_waves = plan->waves_req;
+  // the plan has W = min(requested, N) waves, and N = sum over bags of
+  // max(1, ceil(L / C)) <= ceil(total_ids / C) + T * B: launch no more
+  a.grid_waves = std::min<int64_t>(plan->waves_req,
+                                   (plan->total_ids + plan->C - 1) / plan->C + (int64_t)plan->T * plan->B);
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lookup launch");
   return DPI_OK;

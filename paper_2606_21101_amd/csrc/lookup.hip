@@ -17,7 +17,7 @@
 //     ahead and shared across the slot's lanes by permutes, kUnroll rows in
 //     flight), closing a bag whenever the stream
 //     crosses the bag's end (fp32 accumulation, rows in bag order).
-//   * Few or long bags: all slots of the wave pool one bag together (rows
+//   * Few, long bags: all slots of the wave pool one bag together (rows
 //     dealt round-robin to slots, then a fixed xor-butterfly across slots).
 //   * A bag split between waves is pooled cooperatively by each wave holding
 //     a piece; its fp32 partial goes to the workspace and the last wave to
@@ -282,8 +282,10 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
 
   for (int64_t tb0 = b_lo; tb0 < b_hi; tb0 += kTileBags) {
     const int nb = (int)min((int64_t)kTileBags, b_hi - tb0);
-    if (nb * 2 <= G) {
-      // few bags: the whole wave pools one bag at a time
+    if (nb * 2 <= G &&
+        (int64_t)(bag_offset(a, ti, t, tb0 + nb) - bag_offset(a, ti, t, tb0)) >= (int64_t)nb * G) {
+      // few bags, each at least G rows long on average: the whole wave pools
+      // one bag at a time (short bags are faster one per slot, in parallel)
       bad |= pool_bags_coop<TIN, TOUT, LPR, BUF>(a, t, tb0, tb0 + nb, lane);
       continue;
     }
@@ -677,8 +679,11 @@ void lookup_uniform_kernel(const LookupArgs args) {
   wave_body<Uniform<TIN, TOUT, LPR>>((KA)__builtin_amdgcn_kernarg_segment_ptr());
 }
 
+// four waves per SIMD (at most 128 VGPRs): faster than the two an
+// unconstrained allocation gives, despite some spilling
 template <typename TOUT>
-__global__ __launch_bounds__(kBlockThreads) void lookup_mixed_kernel(const LookupArgs args) {
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void lookup_mixed_kernel(const LookupArgs args) {
   (void)args;
   wave_body<Mixed<TOUT>>((KA)__builtin_amdgcn_kernarg_segment_ptr());
 }

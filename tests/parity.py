@@ -64,9 +64,12 @@ def plan_args(cfg):
 
 
 def default_waves(cfg, total_ids):
-    """The library's documented default: max(16 * CUs, ceil((ids + T*B) / 2048))."""
+    """The library's documented default: max(min(16 * CUs, max(ceil(T*B/8),
+    min(ceil(ids/32) + T*B, 8*T))), ceil((ids + T*B) / 2048), 1)."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    return max(16 * cus, -(-(total_ids + cfg.num_tables * cfg.batch) // 2048))
+    T, B = cfg.num_tables, cfg.batch
+    fill = min(16 * cus, max(-(-(T * B) // 8), min(-(-total_ids // 32) + T * B, 8 * T)))
+    return max(fill, -(-(total_ids + T * B) // 2048), 1)
 
 
 __all__ = ["check_outputs", "oracle_ref", "gpu_tables", "out_torch_dtype", "plan_args", "default_waves",

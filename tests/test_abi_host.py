@@ -92,12 +92,19 @@ def test_lookup_rejects_null_plan_and_destroy_null():
     lib.dpi_plan_destroy(None)
 
 
+def default_waves_rule(T, B, ids, cus=256):
+    by_work = -(-(ids + T * B) // 2048)
+    fill = min(16 * cus, max(-(-(T * B) // 8), min(-(-ids // 32) + T * B, 8 * T)))
+    return max(fill, by_work, 1)
+
+
 def test_default_waves_formula():
-    # max(16 * CUs, ceil((total_ids + T*B) / 2048)); on a host without a GPU
-    # the CU count falls back to 256
-    w = dpi.dpi_default_waves(100, 65536, 176_805_878)
-    assert w == -(-(176_805_878 + 100 * 65536) // 2048)
-    assert dpi.dpi_default_waves(8, 256, 2048) == 16 * 256
+    # on a host without a GPU the CU count falls back to 256
+    assert dpi.dpi_default_waves(100, 65536, 176_805_878) == -(-(176_805_878 + 100 * 65536) // 2048)
+    assert dpi.dpi_default_waves(26, 16384, 4_260_852) == 16 * 256
+    for T, B, ids, want in ((39, 1, 552, 57), (39, 16, 8588, 312), (39, 128, 67979, 624), (39, 512, 272316, 2496),
+                            (39, 4096, 2173692, 4096), (8, 256, 2048, 256), (1, 0, 0, 1)):
+        assert dpi.dpi_default_waves(T, B, ids) == want == default_waves_rule(T, B, ids)
 
 
 def test_fm_host_validation():
