@@ -4,7 +4,8 @@
 // is known before it runs (§III, opportunity 2) and fuses every field's
 // lookup into one pass whose output size is fixed in advance (§IV-B), with
 // the work spread over threads afterwards (§IV-C).  This file computes that
-// plan on the device from the per-field offsets, in two launches:
+// plan on the device from the per-field offsets, in two launches (one, both
+// steps in a single block, when the batch fits one tile):
 //   plan_reduce    per tile of bags: sum of item counts and costs, offset
 //                  validation; tile 0 also writes the per-field table info,
 //                  column bases and id bases, and resets the per-wave arrays.
@@ -127,16 +128,13 @@ __device__ __forceinline__ int64_t block_sum_i64(int64_t v) {
 // ---------------------------------------------------------------------------
 // Launch 1: tile sums, validation, field info, wave-array reset.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArgs args) {
-  (void)args;
-  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
-  const int64_t blk = blockIdx.x;
   const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
 
-  for (int64_t w = blk * kScanThreads + tid; w < p.waves_req; w += (int64_t)gridDim.x * kScanThreads) {
+  for (int64_t w = blk * kScanThreads + tid; w < p.waves_req; w += nblocks * kScanThreads) {
     d.head_first[w] = -1;
     d.split_pieces[w] = 0;
     d.split_last[w] = -1;
@@ -208,13 +206,10 @@ __global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArg
 // ---------------------------------------------------------------------------
 // Launch 2: prefixes and partition.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs args) {
-  (void)args;
-  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+__device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
-  const int64_t blk = blockIdx.x;
   const int64_t nblk = p.nblk;
 
   // this tile's exclusive prefix and the totals, from the tile sums
@@ -355,10 +350,34 @@ __global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs 
   }
 }
 
+__global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArgs args) {
+  (void)args;
+  plan_reduce_block((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x, gridDim.x);
+}
+
+__global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs args) {
+  (void)args;
+  plan_scan_block((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x);
+}
+
+// A batch of one tile: both steps in one block, one launch (the barrier makes
+// the first step's global writes visible to the whole block).
+__global__ __launch_bounds__(kScanThreads) void plan_single_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  plan_reduce_block(pa, 0, 1);
+  __syncthreads();
+  plan_scan_block(pa, 0);
+}
+
 }  // namespace
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   const unsigned blocks = (unsigned)(a.p.nblk > 0 ? a.p.nblk : 1);
+  if (blocks == 1) {
+    hipLaunchKernelGGL(plan_single_kernel, dim3(1), dim3(kScanThreads), 0, s, a);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(plan_reduce_kernel, dim3(blocks), dim3(kScanThreads), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
