@@ -202,6 +202,25 @@ dpi_status dpi_stage_onehot(const void* x, int32_t x_dtype, int64_t batch, int32
                             void* stream);
 
 /*
+ * Input consolidation for multi-hot fields: one host array `packed` of
+ * x_dtype elements holds every field's offsets ([num_fields][batch + 1], local
+ * per field as dpi_plan takes them) followed by the fields' concatenated ids
+ * (total_ids), as a data loader can lay them out; one asynchronous copy moves
+ * it into `staging` and one kernel converts both parts to the int32 `offsets`
+ * and `ids` of dpi_plan / dpi_lookup.  Values that are not integers in
+ * [0, 2^31) become -1 (dpi_plan then reports malformed offsets, a lookup a
+ * bad id).
+ *   packed:  host, (num_fields * (batch + 1) + total_ids) elements, ideally
+ *            pinned, valid until the copy has run;
+ *   staging: device, 16-byte aligned, at least that many elements;
+ *   offsets: device int32 [num_fields][batch + 1];  ids: device int32 [total_ids].
+ * Errors: INVALID_ARG, MISALIGNED, HIP.
+ */
+dpi_status dpi_stage_csr(const void* packed, int32_t x_dtype, int32_t num_fields, int64_t batch,
+                         int64_t total_ids, void* staging, size_t staging_bytes, int32_t* offsets, int32_t* ids,
+                         void* stream);
+
+/*
  * Breadth-first two-stream scheduling of the interaction modules (§IV-E,
  * Algorithm 2).  A model's explicit interaction module (e.g. a cross network)
  * and implicit one (an MLP) are independent, so each gets a stream; the host

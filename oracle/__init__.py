@@ -177,3 +177,22 @@ def dcn_forward(x0: np.ndarray, cross_w, cross_b, mlp_w, mlp_b):
         h = np.maximum(0.0, h @ V.T + c)
         ah = ah @ np.abs(V).T + np.abs(c)
     return x, h, ax, ah
+
+
+def stage_csr(packed: np.ndarray, num_fields: int, batch: int, total_ids: int):
+    """Multi-hot input consolidation (§V breakdown): one packed host array holding
+    every field's offsets ([T][B+1], local per field) followed by the fields'
+    concatenated ids, as a loader produces them; returns the int32 offsets and ids
+    the plan and lookup take.  A value that is not an integer in [0, 2^31) becomes -1."""
+    v = np.asarray(packed)
+    n_off = num_fields * (batch + 1)
+    if v.dtype.kind == "f":
+        w = v.astype(np.float64)
+        with np.errstate(invalid="ignore"):
+            ok = np.isfinite(w) & (w >= 0) & (w < 2.0 ** 31) & (w == np.trunc(w))
+        ints = np.where(ok, w, -1).astype(np.int64)
+    else:
+        w = v.astype(np.int64)
+        ints = np.where((w >= 0) & (w < 2 ** 31), w, -1)
+    return (ints[:n_off].astype(np.int32).reshape(num_fields, batch + 1),
+            ints[n_off:n_off + total_ids].astype(np.int32))

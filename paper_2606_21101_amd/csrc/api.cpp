@@ -435,6 +435,35 @@ dpi_status dpi_stage_onehot(const void* x, int32_t x_dtype, int64_t batch, int32
   return DPI_OK;
 }
 
+dpi_status dpi_stage_csr(const void* packed, int32_t x_dtype, int32_t num_fields, int64_t batch,
+                         int64_t total_ids, void* staging, size_t staging_bytes, int32_t* offsets, int32_t* ids,
+                         void* stream) {
+  if (batch < 0 || total_ids < 0 || num_fields < 1)
+    return fail(DPI_ERR_INVALID_ARG, "batch and total_ids must be >= 0, num_fields >= 1");
+  int esize = 0;
+  switch (x_dtype) {
+    case DPI_X_F32: esize = 4; break;
+    case DPI_X_I64: esize = 8; break;
+    case DPI_X_I32: esize = 4; break;
+    default: return fail(DPI_ERR_INVALID_ARG, "bad x_dtype");
+  }
+  const int64_t n_off = (int64_t)num_fields * (batch + 1);
+  const size_t bytes = (size_t)(n_off + total_ids) * (size_t)esize;
+  if (!packed || !staging || !offsets || (total_ids > 0 && !ids))
+    return fail(DPI_ERR_INVALID_ARG, "packed, staging, offsets or ids is NULL");
+  if (staging_bytes < bytes) return fail(DPI_ERR_INVALID_ARG, "staging %zu bytes, need %zu", staging_bytes, bytes);
+  if (reinterpret_cast<uintptr_t>(staging) & 15) return fail(DPI_ERR_MISALIGNED, "staging not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(packed) % esize) return fail(DPI_ERR_MISALIGNED, "packed not element-aligned");
+  if ((reinterpret_cast<uintptr_t>(offsets) | reinterpret_cast<uintptr_t>(ids)) & 3)
+    return fail(DPI_ERR_MISALIGNED, "offsets or ids not 4-byte aligned");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = hipMemcpyAsync(staging, packed, bytes, hipMemcpyHostToDevice, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  e = launch_stage_csr(staging, x_dtype, n_off, total_ids, offsets, ids, s);
+  if (e != hipSuccess) return hip_fail(e, "stage launch");
+  return DPI_OK;
+}
+
 dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
   if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
   hipError_t e = hipStreamSynchronize(plan->stream);

@@ -161,6 +161,8 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
 hipError_t launch_fm(const FmArgs& a, hipStream_t s);
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);
+hipError_t launch_stage_csr(const void* src, int32_t x_dtype, int64_t n_off, int64_t n_ids, int32_t* offsets,
+                            int32_t* ids, hipStream_t s);
 // interaction modules' fused element-wise operators (16-byte alignment of all
 // pointers is required when n is a multiple of 4)
 hipError_t launch_cross_fuse(const float* x0, const float* y, const float* bias, const float* x, float* out,

@@ -1,4 +1,4 @@
-// Input consolidation for one-hot fields (gfx950).
+// Input consolidation (gfx950): one-hot and multi-hot batches.
 //
 // A CTR data loader hands over a batch's categorical features as one
 // sample-major matrix x[B][row_stride] (column t = field t's id, often stored
@@ -43,7 +43,45 @@ __global__ __launch_bounds__(kTile * 4) void stage_onehot_kernel(const StageArgs
   }
 }
 
+// Multi-hot batches: the device copy holds every field's offsets ([T][B+1])
+// followed by the fields' ids; both are converted in one grid-stride pass.
+template <typename TX>
+__global__ __launch_bounds__(kBlockThreads) void stage_csr_kernel(const void* __restrict__ src, int64_t n_off,
+                                                                  int64_t n_ids, int32_t* __restrict__ offsets,
+                                                                  int32_t* __restrict__ ids) {
+  const TX* __restrict__ x = reinterpret_cast<const TX*>(src);
+  const int64_t n = n_off + n_ids;
+  for (int64_t i = (int64_t)blockIdx.x * kBlockThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kBlockThreads) {
+    const int32_t v = to_id(x[i]);
+    if (i < n_off)
+      offsets[i] = v;
+    else
+      ids[i - n_off] = v;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_stage_csr(const void* src, int32_t x_dtype, int64_t n_off, int64_t n_ids, int32_t* offsets,
+                            int32_t* ids, hipStream_t s) {
+  const int64_t n = n_off + n_ids;
+  if (n <= 0) return hipSuccess;
+  const unsigned blocks = (unsigned)std::min<int64_t>((n + kBlockThreads - 1) / kBlockThreads, 8192);
+  switch (x_dtype) {
+    case DPI_X_F32:
+      hipLaunchKernelGGL(stage_csr_kernel<float>, dim3(blocks), dim3(kBlockThreads), 0, s, src, n_off, n_ids, offsets, ids);
+      break;
+    case DPI_X_I64:
+      hipLaunchKernelGGL(stage_csr_kernel<int64_t>, dim3(blocks), dim3(kBlockThreads), 0, s, src, n_off, n_ids, offsets, ids);
+      break;
+    case DPI_X_I32:
+      hipLaunchKernelGGL(stage_csr_kernel<int32_t>, dim3(blocks), dim3(kBlockThreads), 0, s, src, n_off, n_ids, offsets, ids);
+      break;
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_stage(const StageArgs& a, hipStream_t s) {
   if (a.B <= 0) return hipSuccess;

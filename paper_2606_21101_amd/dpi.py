@@ -104,6 +104,8 @@ def load() -> ctypes.CDLL:
     lib.dpi_fm_second_order.argtypes = [vp, i32, i64, i32, i32, i64, vp, vp]
     lib.dpi_stage_onehot.restype = ctypes.c_int
     lib.dpi_stage_onehot.argtypes = [vp, i32, i64, i32, i64, vp, sz, vp, vp]
+    lib.dpi_stage_csr.restype = ctypes.c_int
+    lib.dpi_stage_csr.argtypes = [vp, i32, i32, i64, i64, vp, sz, vp, vp, vp]
     lib.dpi_breadth_first_order.restype = ctypes.c_int
     lib.dpi_breadth_first_order.argtypes = [i32, i32, ctypes.POINTER(i32)]
     lib.dpi_launch_two_streams.restype = ctypes.c_int
@@ -314,6 +316,16 @@ class DcnHead:
         if getattr(self, "handle", None) and _lib is not None:
             _lib.dpi_dcn_destroy(ctypes.c_void_p(self.handle))
             self.handle = None
+
+
+def dpi_stage_csr(packed, x_dtype: int, num_fields: int, batch: int, total_ids: int, staging, offsets, ids,
+                  staging_bytes: Optional[int] = None, stream=None) -> None:
+    """One host-to-device copy of [all fields' offsets | all ids] and one conversion
+    kernel into the int32 offsets and ids of dpi_plan / dpi_lookup."""
+    if staging_bytes is None:
+        staging_bytes = int(staging.numel() * staging.element_size())
+    _check(load().dpi_stage_csr(_ptr(packed), x_dtype, num_fields, batch, total_ids, _ptr(staging), staging_bytes,
+                                _ptr(offsets), _ptr(ids), _stream(stream)))
 
 
 def dpi_plan_destroy(plan: Plan) -> None:

@@ -154,3 +154,15 @@ def test_scheduler_host_validation():
     out = ctypes.c_void_p()
     assert lib.dpi_dcn_create(ctypes.byref(d), None, 0, ctypes.byref(out)) == dpi.DPI_ERR_INVALID_ARG
     assert lib.dpi_dcn_forward(None, None, None, None, 0, None, None, None, None) == dpi.DPI_ERR_INVALID_ARG
+
+
+def test_stage_csr_host_validation():
+    lib = dpi.load()
+    vp = 0x10000
+    assert lib.dpi_stage_csr(vp, dpi.DPI_X_I64, 0, 2, 4, vp, 1 << 20, vp, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_csr(vp, dpi.DPI_X_I64, 2, -1, 4, vp, 1 << 20, vp, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_csr(vp, 5, 2, 2, 4, vp, 1 << 20, vp, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_csr(None, dpi.DPI_X_I64, 2, 2, 4, vp, 1 << 20, vp, vp, None) == dpi.DPI_ERR_INVALID_ARG
+    assert lib.dpi_stage_csr(vp, dpi.DPI_X_I64, 2, 2, 4, vp, 79, vp, vp, None) == dpi.DPI_ERR_INVALID_ARG  # 10 * 8 bytes
+    assert lib.dpi_stage_csr(vp, dpi.DPI_X_I64, 2, 2, 4, vp + 8, 1 << 20, vp, vp, None) == dpi.DPI_ERR_MISALIGNED
+    assert lib.dpi_stage_csr(vp + 4, dpi.DPI_X_I64, 2, 2, 4, vp, 1 << 20, vp, vp, None) == dpi.DPI_ERR_MISALIGNED

@@ -70,3 +70,48 @@ def test_stage_rejects_bad_arguments():
             dpi.dpi_stage_onehot(*args, staging, ids)
         assert ei.value.status == code
     dpi.dpi_stage_onehot(x, dpi.DPI_X_F32, 0, 4, 4, staging, ids)    # empty batch: nothing to do
+
+
+def stage_csr(packed_np, x_dtype, T, B, n_ids):
+    host = torch.empty(len(packed_np), dtype=XT[x_dtype][1], pin_memory=True)
+    host.copy_(torch.from_numpy(packed_np))
+    staging = torch.empty(max(16, len(packed_np) * host.element_size()), dtype=torch.uint8, device="cuda")
+    offs = torch.full((T, B + 1), 777, dtype=torch.int32, device="cuda")
+    ids = torch.full((max(1, n_ids),), 777, dtype=torch.int32, device="cuda")
+    dpi.dpi_stage_csr(host, x_dtype, T, B, n_ids, staging, offs, ids)
+    torch.cuda.synchronize()
+    return offs.cpu().numpy(), ids[:n_ids].cpu().numpy()
+
+
+@pytest.mark.parametrize("x_dtype", [dpi.DPI_X_F32, dpi.DPI_X_I64, dpi.DPI_X_I32])
+@pytest.mark.parametrize("T,B", [(1, 1), (39, 16), (26, 512), (3, 5000)])
+def test_stage_csr_matches_oracle(x_dtype, T, B):
+    rng = np.random.default_rng(T * 7 + B)
+    lens = rng.integers(0, 30, size=(T, B))
+    offs = np.zeros((T, B + 1), np.int64)
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    n_ids = int(offs[:, -1].sum())
+    ids = rng.integers(0, 1 << 20, size=n_ids)
+    packed = np.concatenate([offs.reshape(-1), ids]).astype(np.float64)
+    bad = rng.random(len(packed)) < 0.02
+    packed[bad] = -5 if x_dtype != dpi.DPI_X_F32 else 2.5
+    packed = packed.astype(XT[x_dtype][0])
+    got_o, got_i = stage_csr(packed, x_dtype, T, B, n_ids)
+    want_o, want_i = oracle.stage_csr(packed, T, B, n_ids)
+    assert np.array_equal(got_o, want_o) and np.array_equal(got_i, want_i)
+
+
+def test_stage_csr_then_lookup_equals_direct():
+    rng = np.random.default_rng(21)
+    T, B, D, rows = 5, 300, 32, 400
+    tables = [torch.from_numpy((rng.standard_normal((rows, D)) * 0.01).astype(np.float16)).cuda() for _ in range(T)]
+    lens = rng.integers(0, 12, size=(T, B))
+    offs = np.zeros((T, B + 1), np.int64)
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    n_ids = int(offs[:, -1].sum())
+    ids = rng.integers(0, rows, size=n_ids)
+    got_o, got_i = stage_csr(np.concatenate([offs.reshape(-1), ids]), dpi.DPI_X_I64, T, B, n_ids)
+    fl = FusedLookup(tables, [0, 1, 0, 1, 0])
+    a = fl(torch.from_numpy(got_i).cuda(), torch.from_numpy(got_o).cuda(), B)
+    b = fl(torch.from_numpy(ids.astype(np.int32)).cuda(), torch.from_numpy(offs.astype(np.int32)).cuda(), B)
+    assert torch.equal(a, b)

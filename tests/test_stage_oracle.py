@@ -37,3 +37,17 @@ def test_integer_matrix_is_transposed():
 def test_out_of_range_integers():
     x = np.array([[-1, 2 ** 31, 2 ** 31 - 1]], np.int64)
     assert list(oracle.stage_onehot(x, 3)) == [-1, -1, 2 ** 31 - 1]
+
+
+def test_csr_hand_typed():
+    # 2 fields, batch 2: field 0 bags {3, 4} {}, field 1 bags {7} {1, 1}
+    # packed = offsets of field 0, offsets of field 1, then the ids
+    packed = np.array([0, 2, 2, 0, 1, 3, 3, 4, 7, 1, 1], np.int64)
+    offs, ids = oracle.stage_csr(packed, 2, 2, 5)
+    assert offs.tolist() == [[0, 2, 2], [0, 1, 3]]
+    assert ids.tolist() == [3, 4, 7, 1, 1]
+    bad = packed.astype(np.float32)
+    bad[9] = 1.5
+    bad[1] = -2
+    offs, ids = oracle.stage_csr(bad, 2, 2, 5)
+    assert offs.tolist() == [[0, -1, 2], [0, 1, 3]] and ids.tolist() == [3, 4, 7, -1, 1]
