@@ -355,7 +355,7 @@ def main():
     ap.add_argument("--stage-sweep", action="store_true",
                     help="only measure one-hot input staging latency (per-field copies and conversions "
                          "against dpi_stage_onehot) over the heterogeneous workload's batch sizes")
-    ap.add_argument("--inflight", type=int, default=2,
+    ap.add_argument("--inflight", type=int, default=1,
                     help="also time a series with this many batches in flight (each with its own stream, "
                          "workspace and output, so one batch's plan overlaps another's lookup, as in a "
                          "serving loop); 1: no such series.  value stays the one-batch-at-a-time series")
