@@ -21,6 +21,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -105,7 +106,7 @@ def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_
     with open(path, "w") as f:
         f.write(f"# HBM traffic of the fused lookup kernel, workload config {config_key}\n")
         f.write(f"# {WORKLOAD_TEXT[config_key]}\n")
-        f.write("# commands (run from /tmp, repository at $R):\n")
+        f.write("# commands (run from /tmp, repository at $R, profiler output under $OUT):\n")
         for line in commands.strip().splitlines():
             f.write(f"#   {_portable(line)}\n")
         f.write("# FETCH_SIZE / WRITE_SIZE are KiB per dispatch; each is scaled by the ratio of the\n")
@@ -131,9 +132,11 @@ def write_traffic_profile(config_key: int, fetch_csv: str, write_csv: str, copy_
 
 
 def _portable(command: str) -> str:
-    """A recorded command with this checkout's absolute path written as $R."""
+    """A recorded command with the profiler's output directory written as $OUT
+    and this checkout's absolute path as $R."""
     root = os.path.dirname(os.path.abspath(__file__))
-    return command.strip().replace(root, "$R")
+    out = re.sub(re.escape(root) + r"/[A-Za-z0-9_]+/prof[0-9]+", "$OUT", command.strip())
+    return out.replace(root, "$R")
 
 
 def summarize_kernel_stats(stats_csv: str, out_path: str, commands: str):
@@ -143,7 +146,7 @@ def summarize_kernel_stats(stats_csv: str, out_path: str, commands: str):
     keep = [r for r in rows if any(k in r["Name"] for k in ("lookup_", "plan_"))]
     with open(out_path, "w") as f:
         f.write("# rocprofv3 kernel statistics of the library's kernels (durations in ns)\n")
-        f.write("# commands (run from /tmp, repository at $R):\n")
+        f.write("# commands (run from /tmp, repository at $R, profiler output under $OUT):\n")
         for line in commands.strip().splitlines():
             f.write(f"#   {_portable(line)}\n")
         f.write(f"# kernel_source_hash: {kernel_source_hash()}\n")

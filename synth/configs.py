@@ -10,7 +10,7 @@ inference workloads (§V-A); no record of either dataset is used.  Every
 number drawn at random (row counts, bag lengths, ids, table values) comes
 from :mod:`synth.generate`, seeded by ``Config.seed``.
 
-Readings of under-specified points (each also listed in the design doc):
+Readings of under-specified points:
   * "~N(0, 0.01)" values: standard deviation 0.01.
   * "Zipf(s) over each table's rows": bounded Zipf, P(rank r) ~ r^-s for
     r in [1, n_t]; the literal mapping sends rank r to row r-1 (a
