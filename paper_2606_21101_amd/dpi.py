@@ -37,7 +37,9 @@ DPI_FLAG_INPUT_FIRST = 1 << 3
 DPI_SCHED_BREADTH_FIRST = 0
 DPI_SCHED_DEPTH_FIRST = 1
 DPI_SCHED_ONE_STREAM = 2
+DPI_ABI_VERSION = 1
 DPI_MAX_TABLES = 256
+DPI_MAX_DIM = 65536
 
 
 class dpi_table_meta(ctypes.Structure):

@@ -166,3 +166,15 @@ def test_stage_csr_host_validation():
     assert lib.dpi_stage_csr(vp, dpi.DPI_X_I64, 2, 2, 4, vp, 79, vp, vp, None) == dpi.DPI_ERR_INVALID_ARG  # 10 * 8 bytes
     assert lib.dpi_stage_csr(vp, dpi.DPI_X_I64, 2, 2, 4, vp + 8, 1 << 20, vp, vp, None) == dpi.DPI_ERR_MISALIGNED
     assert lib.dpi_stage_csr(vp + 4, dpi.DPI_X_I64, 2, 2, 4, vp, 1 << 20, vp, vp, None) == dpi.DPI_ERR_MISALIGNED
+
+
+def test_binding_constants_mirror_the_header():
+    text = open(os.path.join(ROOT, "include", "dpi.h")).read()
+    for name, value in re.findall(r"#define (DPI_[A-Z_]+)\s+(\d+)", text):
+        assert getattr(dpi, name) == int(value), name
+    enums = dict(re.findall(r"\b(DPI_[A-Z0-9_]+) = (\d+)\b", text))
+    shifts = dict(re.findall(r"\b(DPI_FLAG_[A-Z_]+) = 1u << (\d+)", text))
+    for name, value in enums.items():
+        assert getattr(dpi, name) == int(value), name
+    for name, bit in shifts.items():
+        assert getattr(dpi, name) == 1 << int(bit), name

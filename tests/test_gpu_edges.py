@@ -148,6 +148,40 @@ def test_deterministic_and_stream():
     assert torch.equal(a, d)
 
 
+def test_max_tables_and_max_dim():
+    """DPI_MAX_TABLES fields of mixed row classes (the mixed-class kernel), and
+    one field of DPI_MAX_DIM elements per row (the general path, 256 KiB rows)."""
+    rng = np.random.default_rng(256)
+    T = dpi.DPI_MAX_TABLES
+    dims = [(4, 8, 16, 32, 6)[t % 5] for t in range(T)]
+    dtypes = [t % 2 for t in range(T)]
+    tables, ids, offs, pool = random_problem(rng, dims, dtypes, 33, 9)
+    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 301), (dpi.DPI_FLAG_INPUT_FIRST, 0)):
+        out, st, _, _ = run_case(tables, ids, offs, pool, 33, flags=flags, num_waves=W, chunk_rows=4)
+        assert st == dpi.DPI_OK
+        check(tables, ids, offs, pool, 33, out)
+    tables, ids, offs, pool = random_problem(rng, [dpi.DPI_MAX_DIM], [0], 3, 4, rows=5)
+    for flags, W in ((0, 0), (dpi.DPI_FLAG_EXACT_SPLIT, 3), (dpi.DPI_FLAG_INPUT_FIRST, 0)):
+        out, st, _, _ = run_case(tables, ids, offs, pool, 3, flags=flags, num_waves=W, chunk_rows=1)
+        assert st == dpi.DPI_OK
+        check(tables, ids, offs, pool, 3, out)
+
+
+def test_million_sample_onehot_batch():
+    """2^20 one-hot samples over three fields (the one-hot kernel), sampled rows
+    against the oracle, every output row written."""
+    rng = np.random.default_rng(20)
+    B, dims, rows = 1 << 20, [16, 32, 8], 1000
+    tables = [(rng.standard_normal((rows, d)) * 0.01).astype(np.float32) for d in dims]
+    ids = rng.integers(0, rows, size=3 * B).astype(np.int32)
+    out, st, _, _ = run_case(tables, ids, None, [0, 1, 0], B)
+    assert st == dpi.DPI_OK
+    pick = np.concatenate([np.arange(100), np.arange(B // 2, B // 2 + 100), np.arange(B - 100, B)])
+    sub_ids = np.concatenate([ids[t * B:(t + 1) * B][pick] for t in range(3)])
+    ref, mag = oracle.lookup(dims, tables, sub_ids, None, [0, 1, 0], len(pick))
+    check_outputs(out[torch.from_numpy(pick).cuda()].double().cpu().numpy(), ref, mag, False, False, exact=True)
+
+
 def test_rows_beyond_2gib_of_a_table():
     """Rows whose byte offset exceeds 2^31 (buffer-descriptor range up to 4 GiB)
     and a table above 4 GiB (64-bit addressing) are read correctly."""

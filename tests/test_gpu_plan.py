@@ -25,7 +25,8 @@ def run_plan(dims, dtypes, out_dtype, rows, lengths, onehot, C=0, K=0, W=0, flag
     if W == 0:
         # the library's documented default, computed here from the device's CU count
         cus = torch.cuda.get_device_properties(0).multi_processor_count
-        W = max(16 * cus, -(-(total + T * B) // 2048))
+        fill = min(16 * cus, max(-(-(T * B) // 8), min(-(-total // 32) + T * B, 8 * T)))
+        W = max(fill, -(-(total + T * B) // 2048), 1)
     plan = fl.plan(offs, B, total, num_waves=W)
     got = dpi.dpi_plan_export(plan)
     assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_OK
@@ -52,7 +53,8 @@ def test_plan_parity_configs(key, batch):
 
 
 @pytest.mark.parametrize("case", ["all_empty", "one_long_bag", "single_table", "w1", "w_over_n", "c1",
-                                  "mixed_dims", "zero_batch"])
+                                  "mixed_dims", "zero_batch", "max_tables", "max_dim", "huge_wave_request",
+                                  "default_waves"])
 def test_plan_parity_edges(case):
     rng = np.random.default_rng(3)
     dims, dtypes, rows, lengths, kw = [16, 8], [0, 1], [100, 100], None, {}
@@ -80,7 +82,33 @@ def test_plan_parity_edges(case):
     elif case == "zero_batch":
         lengths = np.zeros((2, 0), np.int64)
         kw = dict(W=8)
+    elif case == "max_tables":                      # DPI_MAX_TABLES fields of mixed row classes
+        T = dpi.DPI_MAX_TABLES
+        dims = [(4, 8, 16, 32, 3)[t % 5] for t in range(T)]
+        dtypes = [t % 2 for t in range(T)]
+        dims = [d if (d * (2 if dt else 4)) % 4 == 0 else d + 1 for d, dt in zip(dims, dtypes)]
+        rows = [50] * T
+        lengths = rng.integers(0, 12, size=(T, 20))
+        kw = dict(W=333)
+    elif case == "max_dim":                         # DPI_MAX_DIM elements per row
+        dims, dtypes, rows = [65536], [0], [4]
+        lengths = np.array([[2, 0, 5]], np.int64)
+        kw = dict(W=3, flags=dpi.DPI_FLAG_EXACT_SPLIT)
+    elif case == "huge_wave_request":
+        lengths = rng.integers(0, 40, size=(2, 100))
+        kw = dict(W=1_000_000)
+    elif case == "default_waves":
+        lengths = rng.integers(0, 40, size=(2, 1000))
     run_plan(dims, dtypes, 0, rows, lengths.astype(np.int64), False, **kw)
+
+
+def test_plan_parity_large_onehot_batch():
+    """A million one-hot samples over two fields (no offsets): the plan's closed
+    form for one-id bags, 2^21 bags."""
+    B = 1 << 20
+    lengths = np.ones((2, B), np.int64)
+    got = run_plan([16, 8], [0, 0], 0, [1000, 1000], lengths, True, W=5000)
+    assert got["header"][9] == 2 * B
 
 
 def test_plan_onehot_null_offsets_equals_explicit():
