@@ -43,10 +43,15 @@ WORKLOAD_TEXT = {
 
 
 def kernel_source_hash() -> str:
+    """Hash of the lookup and plan kernel sources, comments and whitespace
+    removed (a comment edit does not make a profile stale)."""
     h = hashlib.sha256()
     for name in ("lookup.hip", "plan.hip", "dpi_internal.h"):
-        with open(os.path.join(ROOT, "paper_2606_21101_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2606_21101_amd", "csrc", name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        h.update("".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -15,14 +15,20 @@
 //     a contiguous run of whole bags holding about the same number of rows,
 //     and each slot walks its rows as one stream (ids prefetched one step
 //     ahead and shared across the slot's lanes by permutes, kUnroll rows in
-//     flight), closing a bag whenever the stream
-//     crosses the bag's end (fp32 accumulation, rows in bag order).
+//     flight), closing a bag whenever the stream crosses the bag's end (fp32
+//     accumulation, rows in bag order).
 //   * Few, long bags: all slots of the wave pool one bag together (rows
 //     dealt round-robin to slots, then a fixed xor-butterfly across slots).
 //   * A bag split between waves is pooled cooperatively by each wave holding
 //     a piece; its fp32 partial goes to the workspace and the last wave to
 //     arrive (agent-scope ticket) adds the partials in wave order and writes
 //     the row -- deterministic, no floating-point atomics.
+// Kernels: one fully inlined kernel per row class when every field shares
+// one (lookup_uniform_kernel), a per-field dispatching one otherwise
+// (lookup_mixed_kernel), a plain row copy for one-hot batches of one row
+// class (lookup_onehot_kernel), and the input-first allocation kept for
+// comparison (lookup_input_first_kernel).  Workgroups are remapped so each
+// of the 8 XCDs takes a contiguous range of waves (a few fields per L2).
 // Rows are read with buffer loads (32-bit offsets, range-checked by the
 // descriptor) when the table is below 4 GiB, with 64-bit global loads
 // otherwise.
