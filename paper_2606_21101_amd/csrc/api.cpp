@@ -40,8 +40,7 @@ struct Layout {
 Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
   Layout L{};
   const int64_t TB = T * B;
-  const int64_t tile = (int64_t)kScanThreads * plan_slabs(TB);
-  const int64_t nblk = (TB + tile - 1) / tile;
+  const int64_t nblk = plan_tiles(TB);
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -53,7 +52,7 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
   L.tinfo = take(T * sizeof(TableInfo));
   L.col_base = take((T + 1) * sizeof(int64_t));
   L.id_base = take((T + 1) * sizeof(int64_t));
-  L.block_sum = take(3 * std::max<int64_t>(nblk, 1) * sizeof(int64_t));
+  L.block_sum = take((3 * nblk + 3) * sizeof(int64_t));
   L.bib = take((TB + 1) * sizeof(int64_t));
   L.bcb = take((TB + 1) * sizeof(int64_t));
   L.wib = take((waves_req + 1) * sizeof(int64_t));
@@ -291,12 +290,13 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   p.T = num_tables;
   p.C = o.chunk_rows;
   p.K = o.item_cost_k;
+  p.c_shift = (o.chunk_rows & (o.chunk_rows - 1)) == 0 ? ilog2(o.chunk_rows) : -1;
   p.out_dtype = o.out_dtype;
   p.flags = o.flags;
   p.B = batch;
   p.TB = (int64_t)num_tables * batch;
   p.slabs = plan_slabs(p.TB);
-  p.nblk = (int32_t)((p.TB + (int64_t)kScanThreads * p.slabs - 1) / ((int64_t)kScanThreads * p.slabs));
+  p.nblk = (int32_t)plan_tiles(p.TB);
   p.total_ids = total_ids;
   p.waves_req = o.num_waves;
   p.total_d = total_d;

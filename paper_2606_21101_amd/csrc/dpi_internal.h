@@ -13,10 +13,11 @@ namespace dpi {
 constexpr int kWaveSize = 64;
 constexpr int kBlockThreads = 256;          // 4 independent waves per workgroup
 constexpr int kWavesPerBlock = kBlockThreads / kWaveSize;
-constexpr int kScanThreads = 256;           // plan scan: threads per block
-constexpr int kScanPerThread = 8;           // most bags per thread (slabs per tile)
-constexpr int kScanTile = kScanThreads * kScanPerThread;   // largest tile
-constexpr int kScanMaxTiles = 2048;          // tiles above which a tile grows to more slabs
+constexpr int kScanThreads = 256;           // plan: threads per block (one bag per thread per slab)
+constexpr int kPlanMaxSlabs = 32;           // most slabs per tile
+constexpr int kPlanChunk = 8;               // slabs whose offset loads are in flight together
+constexpr int kPlanTargetTiles = 512;       // a tile grows until the batch has at most this many
+constexpr int kPlanDirectTiles = 1024;      // most tiles whose sums every scan block reads itself
 constexpr int kDefaultChunkRows = 32;
 constexpr int kDefaultItemCost = 64;
 constexpr int kDefaultRowsPerWave = 2048;
@@ -58,7 +59,8 @@ struct PlanDev {
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
-  int64_t* block_sum;    // [3 * nblk]  (items, cost, offsets rejected) per scan tile
+  int64_t* block_sum;    // [3 * nblk + 3]: per tile items, then costs, then malformed-offset flags; the
+                         // last three: totals (when the tiles are scanned by their own launch)
   int64_t* bib;          // bag_item_base [TB+1]
   int64_t* bcb;          // bag_cost_base [TB+1]
   int64_t* wib;          // wave_item_begin [Wreq+1]
@@ -76,8 +78,9 @@ struct PlanParams {
   int32_t K;
   int32_t out_dtype;
   uint32_t flags;
-  int32_t nblk;       // tiles of slabs * kScanThreads bags
-  int32_t slabs;      // 1, 2, 4 or 8: bags per thread
+  int32_t nblk;       // tiles of slabs * kScanThreads bags (at least 1)
+  int32_t slabs;      // bags per thread: 1, 2, 4, ..., kPlanMaxSlabs
+  int32_t c_shift;    // log2(C) when C is a power of two, else -1
   int64_t B;
   int64_t TB;
   int64_t total_ids;
@@ -147,13 +150,27 @@ struct StageArgs {
   int32_t x_dtype;      // dpi_x_dtype
 };
 
-// Bags per plan thread: the fewest slabs (1, 2, 4, 8) that keep the tile
-// count at most kScanMaxTiles, so small batches still spread over many blocks.
+// Slabs per plan tile (bags per plan thread), a power of two.  A batch of at
+// most kPlanChunk slabs is one tile, planned by a single block in one launch;
+// a larger one takes the fewest slabs (at most kPlanMaxSlabs) that keep the
+// tile count at most kPlanTargetTiles.
 inline int32_t plan_slabs(int64_t TB) {
   int32_t s = 1;
-  while (s < kScanPerThread && (TB + (int64_t)kScanThreads * s - 1) / ((int64_t)kScanThreads * s) > kScanMaxTiles)
+  if (TB <= (int64_t)kScanThreads * kPlanChunk) {
+    while ((int64_t)kScanThreads * s < TB) s <<= 1;
+    return s;
+  }
+  while (s < kPlanMaxSlabs && (TB + (int64_t)kScanThreads * s - 1) / ((int64_t)kScanThreads * s) > kPlanTargetTiles)
     s <<= 1;
   return s;
+}
+
+// Plan tiles of a batch of TB bags (at least one, so an empty batch still
+// runs the block that writes the header).
+inline int64_t plan_tiles(int64_t TB) {
+  const int64_t tile = (int64_t)kScanThreads * plan_slabs(TB);
+  const int64_t n = (TB + tile - 1) / tile;
+  return n > 1 ? n : 1;
 }
 
 // kernel launchers (plan.hip / lookup.hip); return the launch's hipError_t

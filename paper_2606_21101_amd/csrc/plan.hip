@@ -4,14 +4,25 @@
 // is known before it runs (§III, opportunity 2) and fuses every field's
 // lookup into one pass whose output size is fixed in advance (§IV-B), with
 // the work spread over threads afterwards (§IV-C).  This file computes that
-// plan on the device from the per-field offsets, in two launches (one, both
-// steps in a single block, when the batch fits one tile):
-//   plan_reduce    per tile of bags: sum of item counts and costs, offset
+// plan on the device from the per-field offsets:
+//   plan_reduce    per tile of bags: sums of item counts and costs, offset
 //                  validation; tile 0 also writes the per-field table info,
-//                  column bases and id bases, and resets the per-wave arrays.
-//   plan_scan      per tile: its exclusive prefix (sum of the preceding tile
-//                  sums), the per-bag exclusive prefixes of items and cost,
-//                  and every wave boundary that falls in a bag's cost interval.
+//                  column bases and id bases; every block resets a share of
+//                  the per-wave arrays.
+//   plan_tiles     only when the batch has more than kPlanDirectTiles tiles:
+//                  one block turns the tile sums into exclusive prefixes and
+//                  totals, so the next launch reads one entry per tile.
+//   plan_scan      per tile: its exclusive prefix, the per-bag exclusive
+//                  prefixes of items and cost, and every wave boundary that
+//                  falls in a bag's cost interval.
+// A batch of one tile runs both steps in a single block (one launch).
+//
+// A tile is V slabs of kScanThreads consecutive bags; thread i holds bag i of
+// every slab, so the offset loads and prefix stores are coalesced.  The loads
+// of a group of slabs carry no branches between them and are all in flight
+// together.  Within a slab a bag's prefix is a DPP wave scan plus the totals
+// of the slab's earlier waves, read from LDS after one barrier per group of
+// slabs.
 //
 // Definitions (the contract checked bit-for-bit against the CPU plan):
 //   bag (t, b) is number t*B + b (field-major); it holds L ids, has
@@ -36,68 +47,123 @@ typedef const __attribute__((address_space(4))) PlanDev& PDR;
 
 __device__ __forceinline__ u128 mul128(int64_t a, int64_t b) { return (u128)(uint64_t)a * (uint64_t)b; }
 
-// smallest q >= 0 with q * den >= num (den > 0; the result fits int64)
-__device__ __forceinline__ int64_t ceil_div128(u128 num, int64_t den) {
-  int64_t q = (int64_t)((double)num / (double)den);
+// A double near a 128-bit value (two roundings; callers only use it as a
+// first guess and then correct with exact comparisons).
+__device__ __forceinline__ double approx_u128(u128 x) {
+  return (double)(uint64_t)(x >> 64) * 0x1p64 + (double)(uint64_t)x;
+}
+
+// smallest q >= 0 with q * den >= num (den > 0; the result fits int64);
+// inv_den approximates 1/den
+__device__ __forceinline__ int64_t ceil_div128(u128 num, int64_t den, double inv_den) {
+  int64_t q = (int64_t)(approx_u128(num) * inv_den);
   if (q < 0) q = 0;
   while (q > 0 && mul128(q - 1, den) >= num) --q;
   while (mul128(q, den) < num) ++q;
   return q;
 }
 
-// field of bag l: floor(l / B), exact
-__device__ __forceinline__ int64_t field_of(int64_t l, int64_t B, double inv_b) {
-  int64_t t = (int64_t)((double)l * inv_b);
-  while (t > 0 && t * B > l) --t;
-  while ((t + 1) * B <= l) ++t;
+// largest q >= 0 with q * den <= num, from a first guess g
+__device__ __forceinline__ int64_t floor_div128(u128 num, int64_t den, double g) {
+  int64_t q = (int64_t)g;
+  if (q < 0) q = 0;
+  while (q > 0 && mul128(q, den) > num) --q;
+  while (mul128(q + 1, den) <= num) ++q;
+  return q;
+}
+
+// field of bag l: floor(l / B), exact (the quotient is below DPI_MAX_TABLES)
+__device__ __forceinline__ int32_t field_of(int64_t l, int64_t B, double inv_b) {
+  int32_t t = (int32_t)((double)l * inv_b);
+  while (t > 0 && (int64_t)t * B > l) --t;
+  while ((int64_t)(t + 1) * B <= l) ++t;
   return t;
 }
 
 __device__ __forceinline__ int32_t packed_dim(uint32_t pk) { return (int32_t)(pk & 0x1ffffu); }
 __device__ __forceinline__ int32_t packed_flags(uint32_t pk) { return (int32_t)(pk >> 17); }
 
-struct BagCost {
-  int64_t items;
-  int64_t cost;
-};
-
-__device__ __forceinline__ BagCost bag_cost(int64_t L, PPR p, uint32_t pk) {
-  const int64_t dim = packed_dim(pk);
-  const int64_t row_bytes = dim * ((packed_flags(pk) & kTiF16) ? 2 : 4);
-  const int64_t out_bytes = dim * (p.out_dtype == DPI_F16 ? 2 : 4);
-  const uint32_t C = (uint32_t)p.C;
-  int64_t n = (int64_t)(((uint32_t)L + C - 1u) / C);   // L < 2^31, C < 2^31
-  if (n < 1) n = 1;
-  // every item pays K; rows sum to L; the first item also pays the output row
-  return BagCost{n, L * row_bytes + out_bytes + n * (int64_t)p.K};
+// ---------------------------------------------------------------------------
+// Cross-lane sums.
+// ---------------------------------------------------------------------------
+template <int CTRL>
+__device__ __forceinline__ int64_t dpp_move(int64_t x) {
+  const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)(uint64_t)x, CTRL, 0xf, 0xf, false);
+  const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)((uint64_t)x >> 32), CTRL, 0xf, 0xf, false);
+  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
 }
 
-// Length of bag (t, b) and whether its offsets are well formed.
-__device__ __forceinline__ int64_t bag_length(PPR p, int64_t t, int64_t b, bool& bad) {
-  if (!p.offsets) return 1;
-  const int32_t* o = p.offsets + t * (p.B + 1);
-  const int64_t lo = o[b], hi = o[b + 1];
-  if ((b == 0 && lo != 0) || hi < lo) {
-    bad = true;
-    return 0;
+// Inclusive scan over the 64 lanes: shifts within rows of 16 lanes, then the
+// row-15 and lane-31 broadcasts.  Lanes whose DPP source does not exist never
+// add what they received.
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t x, int lane) {
+  const int r = lane & 15;
+  int64_t y;
+  y = dpp_move<0x111>(x);   // row_shr:1
+  x = r >= 1 ? x + y : x;
+  y = dpp_move<0x112>(x);   // row_shr:2
+  x = r >= 2 ? x + y : x;
+  y = dpp_move<0x114>(x);   // row_shr:4
+  x = r >= 4 ? x + y : x;
+  y = dpp_move<0x118>(x);   // row_shr:8
+  x = r >= 8 ? x + y : x;
+  y = dpp_move<0x142>(x);   // row_bcast:15
+  x = (lane & 16) ? x + y : x;
+  y = dpp_move<0x143>(x);   // row_bcast:31
+  x = lane >= 32 ? x + y : x;
+  return x;
+}
+
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_move_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xf, 0xf, false);
+}
+
+// The same scan for values whose wave total fits 32 bits.
+__device__ __forceinline__ uint32_t wave_incl_scan32(uint32_t x, int lane) {
+  const int r = lane & 15;
+  uint32_t y;
+  y = dpp_move_u32<0x111>(x);
+  x = r >= 1 ? x + y : x;
+  y = dpp_move_u32<0x112>(x);
+  x = r >= 2 ? x + y : x;
+  y = dpp_move_u32<0x114>(x);
+  x = r >= 4 ? x + y : x;
+  y = dpp_move_u32<0x118>(x);
+  x = r >= 8 ? x + y : x;
+  y = dpp_move_u32<0x142>(x);
+  x = (lane & 16) ? x + y : x;
+  y = dpp_move_u32<0x143>(x);
+  x = lane >= 32 ? x + y : x;
+  return x;
+}
+
+// Block-wide sums of M values (every thread of the block takes part; all
+// threads receive the sums).  s holds one row per wave.
+template <int M>
+__device__ __forceinline__ void block_sums(int64_t (&v)[M], int64_t (&s)[kWavesPerBlock][M]) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    const int64_t x = wave_incl_scan(v[m], lane);
+    if (lane == 63) s[wv][m] = x;
   }
-  return hi - lo;
+  __syncthreads();
+#pragma unroll
+  for (int m = 0; m < M; ++m) {
+    int64_t a = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) a += s[w][m];
+    v[m] = a;
+  }
 }
 
-// Block-wide exclusive scan of a pair of int64 values (kScanThreads threads).
+// Block-wide exclusive scan of a pair (field info only: one block, once).
 __device__ __forceinline__ void block_scan_pair(int64_t a, int64_t b, int64_t& ea, int64_t& eb, int64_t& ta,
                                                 int64_t& tb) {
-  __shared__ int64_t wsum[2][kScanThreads / kWaveSize];
+  __shared__ int64_t wsum[2][kWavesPerBlock];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  int64_t ia = a, ib = b;
-  for (int d = 1; d < 64; d <<= 1) {
-    const int64_t xa = __shfl_up(ia, d, 64);
-    const int64_t xb = __shfl_up(ib, d, 64);
-    if (lane >= d) {
-      ia += xa;
-      ib += xb;
-    }
-  }
+  const int64_t ia = wave_incl_scan(a, lane), ib = wave_incl_scan(b, lane);
   if (lane == 63) {
     wsum[0][wv] = ia;
     wsum[1][wv] = ib;
@@ -106,7 +172,8 @@ __device__ __forceinline__ void block_scan_pair(int64_t a, int64_t b, int64_t& e
   int64_t pa = 0, pb = 0;
   ta = 0;
   tb = 0;
-  for (int v = 0; v < kScanThreads / kWaveSize; ++v) {
+#pragma unroll
+  for (int v = 0; v < kWavesPerBlock; ++v) {
     if (v < wv) {
       pa += wsum[0][v];
       pb += wsum[1][v];
@@ -119,21 +186,128 @@ __device__ __forceinline__ void block_scan_pair(int64_t a, int64_t b, int64_t& e
   __syncthreads();
 }
 
-__device__ __forceinline__ int64_t block_sum_i64(int64_t v) {
-  int64_t e, d0, tot, d1;
-  block_scan_pair(v, 0, e, d0, tot, d1);
-  return tot;
+// ---------------------------------------------------------------------------
+// Bag lengths, item counts and costs of CH slabs, loads first.
+// ---------------------------------------------------------------------------
+// Per-field row and output-row bytes, staged in LDS by every block.
+struct FieldBytes {
+  int32_t row[DPI_MAX_TABLES];
+  int32_t out[DPI_MAX_TABLES];
+};
+
+// (the caller's next barrier publishes them)
+__device__ __forceinline__ void stage_fields(PA pa, FieldBytes& f) {
+  PPR p = pa->p;
+  for (int t = threadIdx.x; t < p.T; t += kScanThreads) {
+    const uint32_t pk = pa->packed[t];
+    const int32_t dim = packed_dim(pk);
+    f.row[t] = dim * ((packed_flags(pk) & kTiF16) ? 2 : 4);
+    f.out[t] = dim * (p.out_dtype == DPI_F16 ? 2 : 4);
+  }
+}
+
+// Bag l of slab k is first + k*kScanThreads.  Lanes past the last bag read
+// the last bag's offsets (always in bounds) and report items 0, cost 0.
+// Loading (slab_load) and costing (slab_cost) are separate so that a group's
+// loads can be issued before a barrier or before the previous group's work.
+// Both require TB > 0.
+template <int CH>
+struct SlabRaw {
+  int32_t t[CH];      // field
+  int32_t lo[CH];     // offsets of the bag's first id and one past its last
+  int32_t hi[CH];
+  bool ok[CH];        // a bag of the batch
+  bool first[CH];     // the first bag of its field
+};
+
+template <int CH>
+struct SlabBags {
+  int32_t t[CH];     // field
+  int32_t n[CH];     // items (n <= max(1, L) < 2^31)
+  int64_t c[CH];     // cost
+  bool bad;          // some valid bag has malformed offsets
+};
+
+template <int CH>
+__device__ __forceinline__ void slab_load(PA pa, int64_t first, SlabRaw<CH>& r) {
+  PPR p = pa->p;
+  const int64_t TB = p.TB, B = p.B;
+  int64_t lc[CH];   // clamped bag number
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    const int64_t l = first + (int64_t)k * kScanThreads;
+    r.ok[k] = l < TB;
+    lc[k] = r.ok[k] ? l : TB - 1;
+  }
+  const double inv_b = 1.0 / (double)B;
+  if (B >= kScanThreads) {
+    // consecutive slabs of a lane cross at most one field start
+    int32_t t = field_of(lc[0], B, inv_b);
+    int64_t start = (int64_t)t * B;
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const bool next = lc[k] >= start + B;
+      t += next ? 1 : 0;
+      start += next ? B : 0;
+      r.t[k] = t;
+      r.first[k] = lc[k] == start;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      r.t[k] = field_of(lc[k], B, inv_b);
+      r.first[k] = lc[k] == (int64_t)r.t[k] * B;
+    }
+  }
+  if (p.offsets) {
+    // bag (t, b) = t*B + b has its offsets at t*(B+1) + b = l + t
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      const int32_t* o = p.offsets + lc[k] + r.t[k];
+      r.lo[k] = o[0];
+      r.hi[k] = o[1];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      r.lo[k] = 0;
+      r.hi[k] = 1;
+    }
+  }
+}
+
+template <int CH>
+__device__ __forceinline__ void slab_cost(PA pa, const FieldBytes& f, const SlabRaw<CH>& r, SlabBags<CH>& s) {
+  PPR p = pa->p;
+  const uint32_t C = (uint32_t)p.C;
+  const int32_t sh = p.c_shift;
+  s.bad = false;
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    const bool bad = (r.first[k] & (r.lo[k] != 0)) | (r.hi[k] < r.lo[k]);
+    s.bad |= r.ok[k] & bad;
+    const uint32_t L = bad ? 0u : (uint32_t)(r.hi[k] - r.lo[k]);
+    const uint32_t up = L + C - 1u;   // L < 2^31, C < 2^31
+    uint32_t n = sh >= 0 ? up >> sh : up / C;
+    n = n < 1u ? 1u : n;
+    const int t = r.t[k];
+    const int64_t c = (int64_t)L * f.row[t] + f.out[t] + (int64_t)n * p.K;
+    s.t[k] = t;
+    s.n[k] = r.ok[k] ? (int32_t)n : 0;
+    s.c[k] = r.ok[k] ? c : 0;
+  }
 }
 
 // ---------------------------------------------------------------------------
 // Launch 1: tile sums, validation, field info, wave-array reset.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks) {
+// Duties outside the bag sums: this block's share of the per-wave reset and,
+// in block 0, the per-field info and the zeroed header.  Returns whether the
+// id counts are malformed.
+__device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk, int64_t nblocks) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
-  const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
-
   for (int64_t w = blk * kScanThreads + tid; w < p.waves_req; w += nblocks * kScanThreads) {
     d.head_first[w] = -1;
     d.split_pieces[w] = 0;
@@ -142,21 +316,6 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
   }
 
   bool bad = false;
-  int64_t items = 0, cost = 0;
-  const int64_t tile0 = blk * (int64_t)kScanThreads * p.slabs;
-#pragma unroll
-  for (int k = 0; k < kScanPerThread; ++k) {
-    if (k >= p.slabs) break;
-    const int64_t l = tile0 + (int64_t)k * kScanThreads + tid;   // coalesced over threads
-    if (l < p.TB) {
-      const int64_t t = field_of(l, p.B, inv_b);
-      const int64_t L = bag_length(p, t, l - t * p.B, bad);
-      const BagCost bc = bag_cost(L, p, pa->packed[t]);
-      items += bc.items;
-      cost += bc.cost;
-    }
-  }
-
   if (blk == 0) {
     // per-field info: dims -> column bases, id counts -> id bases
     int64_t dim = 0, nnz = 0;
@@ -192,46 +351,265 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
     }
     if (tid < 16) d.hdr[tid] = 0;
   }
+  return bad;
+}
 
-  int64_t ea, eb, ta, tb;
-  block_scan_pair(items, cost, ea, eb, ta, tb);
-  const int64_t any_bad = block_sum_i64(bad ? 1 : 0);
+template <int V>
+__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks) {
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x;
+  constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
+  bool bad = plan_setup_block(pa, blk, nblocks);
+
+  int64_t v[3] = {0, 0, 0};   // items, cost, malformed offsets
+  if (p.TB > 0) {
+    __shared__ FieldBytes s_f;
+    stage_fields(pa, s_f);
+    const int64_t tile0 = blk * (int64_t)kScanThreads * V;
+    SlabRaw<CH> raw;
+    slab_load<CH>(pa, tile0 + tid, raw);   // in flight across the barrier
+    __syncthreads();
+#pragma unroll
+    for (int c0 = 0; c0 < V; c0 += CH) {
+      SlabBags<CH> s;
+      slab_cost<CH>(pa, s_f, raw, s);
+      if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw);
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        v[0] += s.n[k];
+        v[1] += s.c[k];
+      }
+      bad |= s.bad;
+    }
+  }
+  v[2] = bad ? 1 : 0;
+  __shared__ int64_t s_red[kWavesPerBlock][3];
+  block_sums<3>(v, s_red);
   if (tid == 0) {
-    d.block_sum[3 * blk] = ta;
-    d.block_sum[3 * blk + 1] = tb;
-    d.block_sum[3 * blk + 2] = any_bad;
+    const int64_t nb = p.nblk;
+    d.block_sum[blk] = v[0];
+    d.block_sum[nb + blk] = v[1];
+    d.block_sum[2 * nb + blk] = v[2];
   }
 }
 
 // ---------------------------------------------------------------------------
-// Launch 2: prefixes and partition.
+// Launch 2 (large batches only): tile sums -> exclusive tile prefixes.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk) {
+__global__ __launch_bounds__(kScanThreads) void plan_tiles_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
   PPR p = pa->p;
   PDR d = pa->d;
-  const int tid = threadIdx.x;
-  const int64_t nblk = p.nblk;
-
-  // this tile's exclusive prefix and the totals, from the tile sums
-  int64_t pre_i = 0, pre_c = 0, tot_i = 0, tot_c = 0, err = 0;
-#pragma unroll 4
-  for (int64_t i = tid; i < nblk; i += kScanThreads) {
-    const int64_t si = d.block_sum[3 * i], sc = d.block_sum[3 * i + 1];
-    if (i < blk) {
-      pre_i += si;
-      pre_c += sc;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t nb = p.nblk;
+  int64_t* bs = d.block_sum;
+  __shared__ int64_t s_w[2][2][kWavesPerBlock];   // double-buffered per round
+  int64_t run_i = 0, run_c = 0;
+  int err = 0;
+  int buf = 0;
+  for (int64_t i0 = 0; i0 < nb; i0 += kScanThreads, buf ^= 1) {
+    const int64_t i = i0 + tid;
+    const bool in = i < nb;
+    const int64_t ic = in ? i : nb - 1;
+    const int64_t si = in ? bs[ic] : 0, sc = in ? bs[nb + ic] : 0;
+    err |= (in && bs[2 * nb + ic] != 0) ? 1 : 0;
+    const int64_t xi = wave_incl_scan(si, lane), xc = wave_incl_scan(sc, lane);
+    if (lane == 63) {
+      s_w[buf][0][wv] = xi;
+      s_w[buf][1][wv] = xc;
     }
-    tot_i += si;
-    tot_c += sc;
-    err |= d.block_sum[3 * i + 2];
+    __syncthreads();
+    int64_t bi = 0, bc = 0, ai = 0, ac = 0;
+#pragma unroll
+    for (int v = 0; v < kWavesPerBlock; ++v) {
+      const int64_t a = s_w[buf][0][v], b = s_w[buf][1][v];
+      ai += a;
+      ac += b;
+      if (v < wv) {
+        bi += a;
+        bc += b;
+      }
+    }
+    if (in) {
+      bs[i] = run_i + bi + xi - si;
+      bs[nb + i] = run_c + bc + xc - sc;
+    }
+    run_i += ai;
+    run_c += ac;
   }
-  int64_t e0, e1, s0, s1;
-  block_scan_pair(pre_i, pre_c, e0, e1, s0, s1);
-  pre_i = s0;
-  pre_c = s1;
-  block_scan_pair(tot_i, tot_c, e0, e1, s0, s1);
-  const int64_t N = s0, S = s1;
-  err = block_sum_i64(err);
+  err = __syncthreads_or(err);
+  if (tid == 0) {
+    bs[3 * nb] = run_i;
+    bs[3 * nb + 1] = run_c;
+    bs[3 * nb + 2] = err ? 1 : 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Launch 3: prefixes and partition.
+// ---------------------------------------------------------------------------
+// Wave targets of a plan: c_w = ceil(w*S/W) for w = 1..W (shared by a block).
+struct Targets {
+  int64_t W, S, slack;
+  double scale;     // W / S
+  double inv_w;     // 1 / W
+  bool exact;       // no snapping of starts to bag ends
+};
+
+// A bag whose cost interval may hold a wave target (after the filter in the
+// scan loop); a wave collects these and resolves them together.
+struct Cand {
+  int64_t bag, ibase, E_lo, E_hi;
+  int32_t t, n;
+};
+
+// Plan arrays the boundary writes go to, staged in LDS.
+struct BoundaryOut {
+  int64_t* hdr;
+  int64_t* wib;
+  int64_t* wave_bag;
+  int32_t* head_first;
+  int32_t* split_pieces;
+  int32_t* split_last;
+  int64_t C, K;
+};
+
+// Wave boundaries whose targets fall in the cost interval (E_lo, E_hi] of a
+// bag with n items whose first item is number ibase.  Target c_w lies in it
+// exactly when floor(E_lo*W/S) < w <= floor(E_hi*W/S).
+// Returns whether the bag is split between waves.
+__device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targets& g, const FieldBytes& f,
+                                               const Cand& cd) {
+  const int64_t W = g.W, S = g.S, E_lo = cd.E_lo, E_hi = cd.E_hi, n = cd.n;
+  const int64_t f_lo = floor_div128(mul128(E_lo, W), S, floor((double)E_lo * g.scale));
+  int64_t f_hi = floor_div128(mul128(E_hi, W), S, floor((double)E_hi * g.scale));
+  if (f_hi > W) f_hi = W;
+  const int64_t out_bytes = f.out[cd.t];
+  const int64_t per_item = o.C * f.row[cd.t] + o.K;
+  const double inv_item = 1.0 / (double)per_item;
+  int64_t w_first = -1, begin_prev = -1, pieces = 1, w_last = -1;
+  for (int64_t w = f_lo + 1; w <= f_hi; ++w) {
+    const int64_t c = ceil_div128(mul128(w, S), W, g.inv_w);   // ceil(w*S/W), in (E_lo, E_hi]
+    // smallest j in [1, n] whose cost prefix reaches c
+    const int64_t num = c - E_lo - out_bytes;
+    int64_t j = num <= 0 ? 1 : ceil_div128((u128)(uint64_t)num, per_item, inv_item);
+    if (j < 1) j = 1;
+    if (j > n - 1) j = n;
+    bool inside = j < n;
+    int64_t begin = cd.ibase + j;
+    if (inside && !g.exact && E_hi - c <= g.slack) {
+      inside = false;
+      begin = cd.ibase + n;
+    }
+    o.wib[w] = begin;
+    o.wave_bag[w] = inside ? cd.bag : cd.bag + 1;
+    if (inside && w < W) {
+      if (w_first < 0) w_first = w - 1;   // the wave holding the bag's first item
+      o.head_first[w] = (int32_t)w_first;
+      if (begin_prev >= 0 && begin_prev < begin) ++pieces;   // previous inside wave was nonempty
+      begin_prev = begin;
+      w_last = w;
+    }
+  }
+  if (w_first >= 0) {
+    ++pieces;   // the last inside wave always holds the bag's remaining items
+    o.split_pieces[w_first] = (int32_t)pieces;
+    o.split_last[w_first] = (int32_t)w_last;
+    return true;
+  }
+  return false;
+}
+
+// Lanes [0, count) of the wave each resolve one collected candidate.
+__device__ __forceinline__ void resolve_candidates(const BoundaryOut& o, const Targets& g, const FieldBytes& f,
+                                                   const Cand* list, int count, int lane) {
+  // the list was written by other lanes of this wave: keep the reads after the writes
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  const bool split = lane < count && bag_boundaries(o, g, f, list[lane]);
+  const uint64_t m = __ballot(split);
+  if (m != 0 && lane == 0) atomicAdd((unsigned long long*)&o.hdr[kHdrSplit], (unsigned long long)__popcll(m));
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+}
+
+// SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
+// its sums come straight from the block instead of from plan_reduce, and
+// setup_bad carries plan_setup_block's verdict.
+template <int V, bool SINGLE>
+__device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_bad) {
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t nb = p.nblk;
+  const int64_t* bs = d.block_sum;
+  constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
+  const int64_t tile0 = blk * (int64_t)kScanThreads * V;
+
+  // the first group's offsets, in flight while the tile prefix is formed
+  __shared__ FieldBytes s_f;
+  SlabRaw<CH> raw;
+  if (p.TB > 0) {
+    stage_fields(pa, s_f);
+    slab_load<CH>(pa, tile0 + tid, raw);
+  }
+
+  // this tile's exclusive prefix and the totals
+  int64_t pre_i, pre_c, N, S;
+  bool err;
+  if constexpr (SINGLE) {
+    static_assert(V <= kPlanChunk, "one group of slabs");
+    __syncthreads();   // field bytes
+    int64_t v[3] = {0, 0, setup_bad ? 1 : 0};
+    if (p.TB > 0) {
+      SlabBags<CH> s0;
+      slab_cost<CH>(pa, s_f, raw, s0);
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        v[0] += s0.n[k];
+        v[1] += s0.c[k];
+      }
+      v[2] += s0.bad ? 1 : 0;
+    }
+    __shared__ int64_t s_tot[kWavesPerBlock][3];
+    block_sums<3>(v, s_tot);
+    pre_i = 0;
+    pre_c = 0;
+    N = v[0];
+    S = v[1];
+    err = v[2] != 0;
+  } else if (nb <= kPlanDirectTiles) {
+    // from the tile sums: every entry loaded at once, then block sums
+    int64_t v[5] = {0, 0, 0, 0, 0};   // prefix items, prefix cost, items, cost, malformed
+#pragma unroll
+    for (int j = 0; j < kPlanDirectTiles / kScanThreads; ++j) {
+      const int64_t i = tid + (int64_t)j * kScanThreads;
+      const int64_t ic = i < nb ? i : nb - 1;
+      const int64_t si = bs[ic], sc = bs[nb + ic], se = bs[2 * nb + ic];
+      const bool in = i < nb, before = i < blk;
+      v[0] += before ? si : 0;
+      v[1] += before ? sc : 0;
+      v[2] += in ? si : 0;
+      v[3] += in ? sc : 0;
+      v[4] += (in && se != 0) ? 1 : 0;
+    }
+    __shared__ int64_t s_red[kWavesPerBlock][5];
+    block_sums<5>(v, s_red);
+    pre_i = v[0];
+    pre_c = v[1];
+    N = v[2];
+    S = v[3];
+    err = v[4] != 0;
+  } else {
+    // plan_tiles left exclusive prefixes in place and the totals after them
+    pre_i = bs[blk];
+    pre_c = bs[nb + blk];
+    N = bs[3 * nb];
+    S = bs[3 * nb + 1];
+    err = bs[3 * nb + 2] != 0;
+  }
   const int64_t W = p.waves_req < N ? p.waves_req : N;
 
   if (blk == 0 && tid == 0) {
@@ -259,130 +637,161 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk) {
   }
   if (p.TB == 0) return;
 
-  // the tile's bags as p.slabs coalesced slabs, one after the other:
-  // thread tid holds bag tile0 + k*kScanThreads + tid of slab k; its
-  // exclusive prefix is the running total of the earlier slabs plus a block
-  // scan within the slab
-  const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
-  const int64_t tile0 = blk * (int64_t)kScanThreads * p.slabs;
-  const bool exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
-  const int64_t slack = W > 0 ? S / (2 * W) : 0;
-  const double w_per_cost = W > 0 ? (double)W / (double)S : 0.0;
-  // all slabs' bag costs first (their offset loads overlap), kept in LDS
-  __shared__ int32_t s_items[kScanPerThread][kScanThreads];
-  __shared__ int64_t s_cost[kScanPerThread][kScanThreads];
-#pragma unroll
-  for (int k = 0; k < kScanPerThread; ++k) {
-    if (k >= p.slabs) break;
-    const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
-    int64_t n = 0, bag_c = 0;
-    if (bag < p.TB) {
-      const int64_t t = field_of(bag, p.B, inv_b);
-      bool ignored = false;   // validation was done by plan_reduce
-      const BagCost bc = bag_cost(bag_length(p, t, bag - t * p.B, ignored), p, pa->packed[t]);
-      n = bc.items;
-      bag_c = bc.cost;
-    }
-    s_items[k][tid] = (int32_t)n;   // n <= max(1, L) < 2^31
-    s_cost[k][tid] = bag_c;
+  __shared__ Targets g;
+  __shared__ BoundaryOut o;
+  if (tid == 0) {
+    g.W = W;
+    g.S = S;
+    g.slack = W > 0 ? S / (2 * W) : 0;
+    g.scale = W > 0 ? (double)W / (double)S : 0.0;
+    g.inv_w = W > 0 ? 1.0 / (double)W : 0.0;
+    g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
+    o.hdr = d.hdr;
+    o.wib = d.wib;
+    o.wave_bag = d.wave_bag;
+    o.head_first = d.head_first;
+    o.split_pieces = d.split_pieces;
+    o.split_last = d.split_last;
+    o.C = p.C;
+    o.K = p.K;
   }
+  __syncthreads();   // publishes the field bytes, g and o
+  const double scale = g.scale;
+  // per slab and wave: the wave's item and cost totals
+  __shared__ int64_t s_wt[V][2][kWavesPerBlock];
+  __shared__ Cand s_cand[kWavesPerBlock][kWaveSize];
+  int ncand = 0;   // collected candidates of this wave (wave-uniform)
   int64_t run_i = pre_i, run_c = pre_c;
 #pragma unroll 1
-  for (int k = 0; k < p.slabs; ++k) {
-    const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
-    const int64_t n = s_items[k][tid], bag_c = s_cost[k][tid];   // this thread's own entries
-    int64_t xi, xc, si, sc;
-    block_scan_pair(n, bag_c, xi, xc, si, sc);   // every thread takes part
-    const int64_t ibase = run_i + xi;
-    const int64_t E_lo = run_c + xc, E_hi = E_lo + bag_c;
-    run_i += si;
-    run_c += sc;
-    if (bag >= p.TB) continue;
-    d.bib[bag] = ibase;
-    d.bcb[bag] = E_lo;
-    if (W == 0) continue;
-
-    // wave boundaries whose targets fall in this bag's cost interval: first
-    // w >= 1 with w*S > E_lo*W, i.e. ceil(w*S/W) > E_lo; the double product
-    // is a first guess corrected by exact 128-bit comparisons
-    const u128 lo_w = mul128(E_lo, W), hi_w = mul128(E_hi, W);
-    int64_t w = (int64_t)((double)E_lo * w_per_cost);
-    if (w < 0) w = 0;
-    while (w > 0 && mul128(w, S) > lo_w) --w;
-    while (mul128(w, S) <= lo_w) ++w;
-    if (w > W || mul128(w, S) > hi_w) continue;   // no target in this bag (the common case)
-    const int64_t t = field_of(bag, p.B, inv_b);
-    const uint32_t pk = pa->packed[t];
-    const int64_t dim = packed_dim(pk);
-    const int64_t row_bytes = dim * ((packed_flags(pk) & kTiF16) ? 2 : 4);
-    const int64_t out_bytes = dim * (p.out_dtype == DPI_F16 ? 2 : 4);
-    const int64_t per_item = (int64_t)p.C * row_bytes + p.K;
-    int64_t w_first = -1, begin_prev = -1, pieces = 1, w_last = -1;
-    for (; w <= W && mul128(w, S) <= hi_w; ++w) {
-      const int64_t c = ceil_div128(mul128(w, S), W);   // ceil(w*S/W), in (E_lo, E_hi]
-      // smallest j in [1, n] whose cost prefix reaches c
-      const int64_t num = c - E_lo - out_bytes;
-      int64_t j = num <= 0 ? 1 : ceil_div128((u128)(uint64_t)num, per_item);
-      if (j < 1) j = 1;
-      if (j > n - 1) j = n;
-      bool inside = j < n;
-      int64_t begin = ibase + j;
-      if (inside && !exact && E_hi - c <= slack) {
-        inside = false;
-        begin = ibase + n;
+  for (int c0 = 0; c0 < V; c0 += CH) {
+    SlabBags<CH> s;
+    slab_cost<CH>(pa, s_f, raw, s);
+    if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw);   // next group
+    int64_t xi[CH], xc[CH];
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      // wave totals below 2^32 (every cost below 2^25) take the 32-bit scan
+      if (__all(s.c[k] < ((int64_t)1 << 25))) {
+        xi[k] = wave_incl_scan32((uint32_t)s.n[k], lane);
+        xc[k] = wave_incl_scan32((uint32_t)s.c[k], lane);
+      } else {
+        xi[k] = wave_incl_scan(s.n[k], lane);
+        xc[k] = wave_incl_scan(s.c[k], lane);
       }
-      d.wib[w] = begin;
-      d.wave_bag[w] = inside ? bag : bag + 1;
-      if (inside && w < W) {
-        if (w_first < 0) w_first = w - 1;   // the wave holding the bag's first item
-        d.head_first[w] = (int32_t)w_first;
-        if (begin_prev >= 0 && begin_prev < begin) ++pieces;   // previous inside wave was nonempty
-        begin_prev = begin;
-        w_last = w;
+      if (lane == 63) {
+        s_wt[c0 + k][0][wv] = xi[k];
+        s_wt[c0 + k][1][wv] = xc[k];
       }
     }
-    if (w_first >= 0) {
-      ++pieces;   // the last inside wave always holds the bag's remaining items
-      d.split_pieces[w_first] = (int32_t)pieces;
-      d.split_last[w_first] = (int32_t)w_last;
-      atomicAdd((unsigned long long*)&d.hdr[kHdrSplit], 1ull);
+    __syncthreads();   // every slab of the group has its own LDS slots: one barrier per group
+#pragma unroll
+    for (int k = 0; k < CH; ++k) {
+      int64_t bi = 0, bc = 0, ai = 0, ac = 0;
+#pragma unroll
+      for (int v = 0; v < kWavesPerBlock; ++v) {
+        const int64_t a = s_wt[c0 + k][0][v], b = s_wt[c0 + k][1][v];
+        ai += a;
+        ac += b;
+        bi += v < wv ? a : 0;
+        bc += v < wv ? b : 0;
+      }
+      const int64_t ibase = run_i + bi + xi[k] - s.n[k];
+      const int64_t E_lo = run_c + bc + xc[k] - s.c[k];
+      const int64_t E_hi = E_lo + s.c[k];
+      run_i += ai;
+      run_c += ac;
+      const int64_t bag = tile0 + (int64_t)(c0 + k) * kScanThreads + tid;
+      const bool valid = bag < p.TB;
+      if (valid) {
+        d.bib[bag] = ibase;
+        d.bcb[bag] = E_lo;
+      }
+      if (W == 0) continue;
+      // filter in double: both products are within (x + 1) * 2^-50 of E*W/S,
+      // so equal floors of the widened interval prove it holds no target
+      const double x_lo = (double)E_lo * scale, x_hi = (double)E_hi * scale;
+      const double margin = (x_hi + 1.0) * 0x1p-45;
+      const bool cand = valid && floor(x_hi + margin) != floor(x_lo - margin);
+      const uint64_t m = __ballot(cand);
+      if (m == 0) continue;
+      const int cnt = __popcll(m);
+      if (ncand + cnt > kWaveSize) {
+        resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
+        ncand = 0;
+      }
+      if (cand) {
+        const int pos = ncand + __popcll(m & ((1ull << lane) - 1ull));
+        Cand& e = s_cand[wv][pos];
+        e.bag = bag;
+        e.ibase = ibase;
+        e.E_lo = E_lo;
+        e.E_hi = E_hi;
+        e.t = s.t[k];
+        e.n = s.n[k];
+      }
+      ncand += cnt;
     }
   }
+  if (ncand > 0) resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
 }
 
+template <int V>
 __global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArgs args) {
   (void)args;
-  plan_reduce_block((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x, gridDim.x);
+  plan_reduce_block<V>((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x, gridDim.x);
 }
 
+template <int V>
 __global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs args) {
   (void)args;
-  plan_scan_block((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x);
+  plan_scan_block<V, false>((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x, false);
 }
 
-// A batch of one tile: both steps in one block, one launch (the barrier makes
-// the first step's global writes visible to the whole block).
+// A batch of one tile: one block, one launch; the bag sums never leave the
+// block (the scan's barriers order the setup's header reset before the
+// header writes and split counts).
+template <int V>
 __global__ __launch_bounds__(kScanThreads) void plan_single_kernel(const PlanArgs args) {
   (void)args;
   const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
-  plan_reduce_block(pa, 0, 1);
-  __syncthreads();
-  plan_scan_block(pa, 0);
+  const bool bad = plan_setup_block(pa, 0, 1);
+  plan_scan_block<V, true>(pa, 0, bad);
+}
+
+template <int V>
+hipError_t launch_plan_v(const PlanArgs& a, hipStream_t s) {
+  const unsigned blocks = (unsigned)a.p.nblk;
+  if constexpr (V <= kPlanChunk) {
+    if (blocks == 1) {
+      hipLaunchKernelGGL(plan_single_kernel<V>, dim3(1), dim3(kScanThreads), 0, s, a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL(plan_reduce_kernel<V>, dim3(blocks), dim3(kScanThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (blocks > (unsigned)kPlanDirectTiles) {
+    hipLaunchKernelGGL(plan_tiles_kernel, dim3(1), dim3(kScanThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(plan_scan_kernel<V>, dim3(blocks), dim3(kScanThreads), 0, s, a);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
-  const unsigned blocks = (unsigned)(a.p.nblk > 0 ? a.p.nblk : 1);
-  if (blocks == 1) {
-    hipLaunchKernelGGL(plan_single_kernel, dim3(1), dim3(kScanThreads), 0, s, a);
-    return hipGetLastError();
+  if (a.p.nblk < 1) return hipErrorInvalidValue;
+  switch (a.p.slabs) {
+    case 1: return launch_plan_v<1>(a, s);
+    case 2: return launch_plan_v<2>(a, s);
+    case 4: return launch_plan_v<4>(a, s);
+    case 8: return launch_plan_v<8>(a, s);
+    case 16: return launch_plan_v<16>(a, s);
+    case 32: return launch_plan_v<32>(a, s);
+    default: return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(plan_reduce_kernel, dim3(blocks), dim3(kScanThreads), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(plan_scan_kernel, dim3(blocks), dim3(kScanThreads), 0, s, a);
-  return hipGetLastError();
 }
 
 }  // namespace dpi

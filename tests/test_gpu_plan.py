@@ -111,6 +111,26 @@ def test_plan_parity_large_onehot_batch():
     assert got["header"][9] == 2 * B
 
 
+@pytest.mark.parametrize("T,B", [(1, 1024 * 8192), (1, 1024 * 8192 + 1), (3, 3_000_000)])
+def test_plan_parity_tile_counts(T, B):
+    """One-hot batches around the largest tile count whose sums every scan
+    block reads itself (1024 tiles of 8192 bags): at it, one past it, and well
+    beyond it, where a separate launch scans the tile sums."""
+    lengths = np.ones((T, B), np.int64)
+    got = run_plan([16, 8, 4][:T], [0, 1, 0][:T], 0, [1000] * T, lengths, True, W=4099)
+    assert got["header"][9] == T * B
+
+
+def test_plan_parity_many_tiles_multihot():
+    """Explicit offsets over 9 M bags (about 1100 tiles): lengths 0..5, some
+    empty bags, the tile-sum launch and split bags under a tight wave count."""
+    rng = np.random.default_rng(11)
+    lengths = rng.integers(0, 6, size=(3, 3_000_000))
+    run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False, W=70_001, C=2,
+             flags=dpi.DPI_FLAG_EXACT_SPLIT)
+    run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False)
+
+
 def test_plan_onehot_null_offsets_equals_explicit():
     cfg = configs.get(2)
     lengths = G.bag_lengths(cfg)
