@@ -758,6 +758,95 @@ __global__ __launch_bounds__(kScanThreads) void plan_single_kernel(const PlanArg
   plan_scan_block<V, true>(pa, 0, bad);
 }
 
+// ---------------------------------------------------------------------------
+// One-hot batches (no offsets): every bag holds one id and is one item, so
+// the prefixes and the wave starts have closed forms and one fully parallel
+// launch writes them.  Field t's bags each cost cost_t = row_bytes_t +
+// out_bytes_t + K, its first bag starts at F_t = sum over t' < t of
+// B*cost_t', and target c_w lies in bag (t, b) of field t with
+// F_t < c_w <= F_{t+1} and b = ceil((c_w - F_t)/cost_t) - 1.  A one-item bag
+// is never split: wave w starts after that bag.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x;
+  const bool bad = __syncthreads_or(plan_setup_block(pa, blockIdx.x, gridDim.x) ? 1 : 0) != 0;
+
+  // per-field bag cost and the cost prefix over fields
+  __shared__ int64_t s_cost[DPI_MAX_TABLES];
+  __shared__ int64_t s_F[DPI_MAX_TABLES + 1];
+  int64_t cost = 0;
+  if (tid < p.T) {
+    const uint32_t pk = pa->packed[tid];
+    const int64_t dim = packed_dim(pk);
+    cost = dim * ((packed_flags(pk) & kTiF16) ? 2 : 4) + dim * (p.out_dtype == DPI_F16 ? 2 : 4) + p.K;
+  }
+  int64_t F, unused0, S, unused1;
+  block_scan_pair(p.B * cost, 0, F, unused0, S, unused1);
+  if (tid < p.T) {
+    s_cost[tid] = cost;
+    s_F[tid] = F;
+  }
+  if (tid == 0) s_F[p.T] = S;
+  __syncthreads();
+  const int64_t TB = p.TB, N = TB;
+  const int64_t W = p.waves_req < N ? p.waves_req : N;
+
+  if (blockIdx.x == 0 && tid == 0) {
+    int64_t* h = d.hdr;
+    h[kHdrAbi] = DPI_ABI_VERSION;
+    h[kHdrT] = p.T;
+    h[kHdrB] = p.B;
+    h[kHdrW] = W;
+    h[kHdrC] = p.C;
+    h[kHdrK] = p.K;
+    h[kHdrOutDtype] = p.out_dtype;
+    h[kHdrFlags] = p.flags;
+    h[kHdrTotalD] = p.total_d;
+    h[kHdrItems] = N;
+    h[kHdrCost] = S;
+    h[kHdrTotalIds] = p.total_ids;
+    h[kHdrWaveReq] = p.waves_req;
+    *d.status = bad ? kStatusBadOffsets : 0;
+  }
+  const int64_t first = (int64_t)blockIdx.x * kScanThreads + tid, stride = (int64_t)gridDim.x * kScanThreads;
+  const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
+  for (int64_t l = first; l <= TB; l += stride) {
+    if (l == TB) {
+      d.bib[l] = N;
+      d.bcb[l] = S;
+    } else {
+      const int32_t t = field_of(l, p.B, inv_b);
+      d.bib[l] = l;
+      d.bcb[l] = s_F[t] + (l - (int64_t)t * p.B) * s_cost[t];
+    }
+  }
+  const double inv_w = W > 0 ? 1.0 / (double)W : 0.0;
+  for (int64_t w = first; w <= W; w += stride) {
+    int64_t start = 0;
+    if (w > 0) {
+      const int64_t c = ceil_div128(mul128(w, S), W, inv_w);   // in (0, S]
+      // the field with F_t < c <= F_{t+1}
+      int lo = 0, hi = p.T - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (s_F[mid] < c) lo = mid;
+        else hi = mid - 1;
+      }
+      const int64_t ct = s_cost[lo], local = c - s_F[lo];   // in (0, B*ct]
+      int64_t q = (int64_t)((double)local / (double)ct);     // then exact: q = ceil(local/ct)
+      while (q > 0 && (q - 1) * ct >= local) --q;
+      while (q * ct < local) ++q;
+      start = (int64_t)lo * p.B + q;   // bag (lo, q - 1) ends where wave w starts
+    }
+    d.wib[w] = start;
+    d.wave_bag[w] = start;
+  }
+}
+
 template <int V>
 hipError_t launch_plan_v(const PlanArgs& a, hipStream_t s) {
   const unsigned blocks = (unsigned)a.p.nblk;
@@ -783,6 +872,13 @@ hipError_t launch_plan_v(const PlanArgs& a, hipStream_t s) {
 
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   if (a.p.nblk < 1) return hipErrorInvalidValue;
+  if (!a.p.offsets) {
+    // enough threads for the larger of the bag and wave arrays, grid-strided beyond
+    const int64_t span = std::max<int64_t>(a.p.TB, a.p.waves_req) + 1;
+    const int64_t blocks = std::min<int64_t>((span + kScanThreads - 1) / kScanThreads, 16384);
+    hipLaunchKernelGGL(plan_onehot_kernel, dim3((unsigned)blocks), dim3(kScanThreads), 0, s, a);
+    return hipGetLastError();
+  }
   switch (a.p.slabs) {
     case 1: return launch_plan_v<1>(a, s);
     case 2: return launch_plan_v<2>(a, s);

@@ -113,12 +113,14 @@ def test_plan_parity_large_onehot_batch():
 
 @pytest.mark.parametrize("T,B", [(1, 1024 * 8192), (1, 1024 * 8192 + 1), (3, 3_000_000)])
 def test_plan_parity_tile_counts(T, B):
-    """One-hot batches around the largest tile count whose sums every scan
-    block reads itself (1024 tiles of 8192 bags): at it, one past it, and well
-    beyond it, where a separate launch scans the tile sums."""
+    """Batches with explicit unit offsets around the largest tile count whose
+    sums every scan block reads itself (1024 tiles of 8192 bags): at it, one
+    past it, and well beyond it, where a separate launch scans the tile sums.
+    The same batches without offsets take the closed-form one-hot plan."""
     lengths = np.ones((T, B), np.int64)
-    got = run_plan([16, 8, 4][:T], [0, 1, 0][:T], 0, [1000] * T, lengths, True, W=4099)
-    assert got["header"][9] == T * B
+    for onehot in (False, True):
+        got = run_plan([16, 8, 4][:T], [0, 1, 0][:T], 0, [1000] * T, lengths, onehot, W=4099)
+        assert got["header"][9] == T * B
 
 
 def test_plan_parity_many_tiles_multihot():
@@ -129,6 +131,19 @@ def test_plan_parity_many_tiles_multihot():
     run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False, W=70_001, C=2,
              flags=dpi.DPI_FLAG_EXACT_SPLIT)
     run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False)
+
+
+@pytest.mark.parametrize("W", [1, 7, 26 * 4096, 1_000_000, 0])
+def test_plan_onehot_closed_form_wave_counts(W):
+    """The closed-form one-hot plan against the oracle at wave counts from one
+    to beyond the number of bags (0: the default rule), mixed row classes."""
+    rng = np.random.default_rng(5)
+    dims = [int(d) for d in rng.choice([4, 8, 16, 32, 60, 128], size=26)]
+    dtypes = [int(x) for x in rng.integers(0, 2, size=26)]
+    dims = [d if (d * (2 if dt else 4)) % 4 == 0 else d + 1 for d, dt in zip(dims, dtypes)]
+    lengths = np.ones((26, 4096), np.int64)
+    run_plan(dims, dtypes, 1, [100] * 26, lengths, True, W=W)
+    run_plan(dims, dtypes, 0, [100] * 26, lengths, True, W=W, K=1000)
 
 
 def test_plan_onehot_null_offsets_equals_explicit():
