@@ -347,6 +347,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warm-seconds", type=float, default=0.3,
+                    help="untimed steps for this long before the warm-up steps (clock ramp)")
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--batch", type=int, default=None, help="override the batch size (heterogeneous sweep)")
     ap.add_argument("--rotations", type=int, default=4)
@@ -471,6 +473,15 @@ def main():
             ev[2].record(stream)
         return plan
 
+    # untimed steps until the clocks have ramped (short steps would otherwise be
+    # timed partly at idle clocks), then the W warm-up steps
+    t_warm, i = time.perf_counter(), 0
+    while time.perf_counter() - t_warm < args.warm_seconds:
+        step(i)
+        i += 1
+        if i % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -575,7 +586,7 @@ def main():
         "unit": "rows/s",
         "n_gpus": 1,
         "steps": args.steps,
-        "warmup": args.warmup,
+        "warmup": args.warmup, "warm_seconds": args.warm_seconds,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
         "scaling": "weak",
