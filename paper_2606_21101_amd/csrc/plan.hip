@@ -15,7 +15,9 @@
 //   plan_scan      per tile: its exclusive prefix, the per-bag exclusive
 //                  prefixes of items and cost, and every wave boundary that
 //                  falls in a bag's cost interval.
-// A batch of one tile runs both steps in a single block (one launch).
+// A batch of one tile runs both steps in a single block (one launch), and a
+// one-hot batch (no offsets) takes plan_onehot, which writes the closed forms
+// of the same arrays in one fully parallel launch.
 //
 // A tile is V slabs of kScanThreads consecutive bags; thread i holds bag i of
 // every slab, so the offset loads and prefix stores are coalesced.  The loads
