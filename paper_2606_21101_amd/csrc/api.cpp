@@ -48,7 +48,7 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
     return at;
   };
   L.hdr = take(16 * sizeof(int64_t));
-  L.status = take(sizeof(int32_t));
+  L.status = take(2 * sizeof(int32_t));
   L.tinfo = take(T * sizeof(TableInfo));
   L.col_base = take((T + 1) * sizeof(int64_t));
   L.id_base = take((T + 1) * sizeof(int64_t));
@@ -106,11 +106,39 @@ struct dpi_plan_s {
   int64_t total_d;
   bool onehot;
   int32_t uniform_class;   // shared row class of every field, or -1
+  int32_t direct_jlog;     // small batches looked up bag by bag: log2 of bags per wave, or -1
   hipStream_t stream;
   char* ws;
   Layout layout;
   int32_t row_class[DPI_MAX_TABLES];
 };
+
+// Small batches (at most kDirectMaxBags bags, every field on the 16-byte row
+// path) are looked up bag by bag when the caller left the wave count to the
+// library: a wave takes J = 2^jlog bags of one field, each pooled by G/J row
+// slots, where G = 64 / (row bytes / 16) is the field's slot count.  J is the
+// same for every field (at most the smallest G), chosen so that an average bag
+// needs about one group of 8 rows per slot, and no larger than the batch.
+// Returns jlog, or -1 for the plan's partition (also the choice for one-hot
+// batches of one row class, which have their own kernel, and for the
+// input-first allocation).
+int32_t direct_jlog(int32_t T, int64_t B, int64_t total_ids, const int32_t* row_class, bool onehot,
+                    int32_t uniform_class, uint32_t flags, bool waves_given) {
+  if (waves_given || (flags & DPI_FLAG_INPUT_FIRST) || (onehot && uniform_class >= 0)) return -1;
+  if (B < 1 || (int64_t)T * B > kDirectMaxBags) return -1;
+  int gmin = kWaveSize;
+  for (int t = 0; t < T; ++t) {
+    if (!(row_class[t] & kTiFast)) return -1;
+    gmin = std::min(gmin, kWaveSize >> ((row_class[t] >> kTiLprShift) & 7));
+  }
+  const int64_t bags = (int64_t)T * B;
+  const int64_t avg = (total_ids + bags - 1) / bags;          // ids per bag, rounded up
+  int64_t slots = 1;                                          // slots an average bag fills with groups of 8
+  while (slots * kDirectGroupRows < avg && slots < gmin) slots <<= 1;
+  int64_t J = std::max<int64_t>(1, gmin / slots);
+  while (J > 1 && J > B) J >>= 1;
+  return ilog2((int)J);
+}
 
 extern "C" {
 
@@ -261,6 +289,8 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   plan->total_d = total_d;
   plan->onehot = offsets == nullptr;
   plan->uniform_class = uniform_class;
+  plan->direct_jlog = direct_jlog(num_tables, batch, total_ids, row_class, offsets == nullptr, uniform_class,
+                                  o.flags, opts && opts->num_waves != 0);
   plan->stream = reinterpret_cast<hipStream_t>(stream);
   plan->ws = reinterpret_cast<char*>(workspace);
   plan->layout = L;
@@ -365,6 +395,8 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   // max(1, ceil(L / C)) <= ceil(total_ids / C) + T * B: launch no more
   a.grid_waves = std::min<int64_t>(plan->waves_req,
                                    (plan->total_ids + plan->C - 1) / plan->C + (int64_t)plan->T * plan->B);
+  a.direct_jlog = plan->direct_jlog;
+  a.direct_wpf = plan->direct_jlog >= 0 ? (plan->B + (1 << plan->direct_jlog) - 1) >> plan->direct_jlog : 0;
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lookup launch");
   return DPI_OK;

@@ -22,6 +22,12 @@ constexpr int kDefaultChunkRows = 32;
 constexpr int kDefaultItemCost = 64;
 constexpr int kDefaultRowsPerWave = 2048;
 constexpr int kDefaultWavesPerCU = 16;
+// Small batches are looked up bag by bag, without the plan's partition, when
+// no bag holds more than kDirectMaxItems chunks of C ids (the plan counts the
+// longer ones) and the batch has at most kDirectMaxBags bags.
+constexpr int kDirectMaxItems = 4;
+constexpr int kDirectGroupRows = 8;   // rows in flight per slot
+constexpr int64_t kDirectMaxBags = 16384;
 
 // status word bits (device-latched errors)
 constexpr int kStatusBadOffsets = 1;
@@ -55,7 +61,7 @@ struct alignas(16) TableInfo {
 // Device pointers of a plan inside the caller's workspace.
 struct PlanDev {
   int64_t* hdr;          // [16]
-  int32_t* status;       // [1]
+  int32_t* status;       // [2]: error bits; bags of more than kDirectMaxItems items
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
@@ -126,6 +132,8 @@ struct LookupArgs {
   int32_t input_first;     // one lane per bag instead of the plan's waves
   int32_t onehot;          // no offsets: every bag holds one id
   int64_t grid_waves;
+  int32_t direct_jlog;     // small batches: log2 of the bags a wave takes, or -1 (the plan's partition)
+  int64_t direct_wpf;      // ... and the waves per field, ceil(B / 2^direct_jlog)
 };
 
 // Second-order FM term over a [B, row_stride] block of T fields of dim D.

@@ -46,6 +46,7 @@ typedef _Float16 half4_t __attribute__((ext_vector_type(4)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kUnroll = 8;        // rows in flight per slot
+static_assert(kUnroll == kDirectGroupRows, "the host sizes direct bag groups by this");
 constexpr int kTileBags = 256;    // bags whose offsets a wave stages in LDS at once
 constexpr uint32_t kBufferWord3 = 0x00020000;   // raw buffer descriptor, gfx9 family
 
@@ -765,6 +766,127 @@ void lookup_onehot_kernel(const LookupArgs args) {
 }
 
 // ---------------------------------------------------------------------------
+// Small batches, bag by bag.  With few bags, none of them long, the plan's
+// balanced partition buys nothing and costs a chain of dependent loads (wave
+// range, bag bases, field info) before the first row is requested.  Here wave
+// w takes J = 2^jlog consecutive bags of one field, read straight from the
+// offsets: the G row slots of the wave form J groups of P = G/J slots, group
+// j pools bag b0 + j with its P slots taking rows p, p + P, p + 2P, ... (8 in
+// flight per slot, the next ids prefetched), and the P partial sums meet in a
+// fixed xor butterfly.  J is the same for every field, so a field has
+// ceil(B/J) waves and a wave finds its field by one division.  The plan still
+// runs first: it validates the offsets and counts the bags longer than
+// kDirectMaxItems chunks; with any such bag the launch falls back to the
+// plan's partition (same kernel, wave_body), so one long bag never holds up
+// a whole lookup.
+// ---------------------------------------------------------------------------
+template <typename TIN, typename TOUT, int LPR, bool BUF>
+__device__ __forceinline__ int direct_bags(KA a, int64_t t, int64_t b0, int jlog, int lane) {
+  constexpr int EPL = In<TIN>::EPL;
+  constexpr int G = kWaveSize / LPR;
+  constexpr int GLOG = __builtin_ctz(G);
+  const int g = lane / LPR, k = lane % LPR;
+  const int plog = GLOG - jlog;   // J <= G for every field (chosen on the host)
+  const int P = 1 << plog;
+  const int j = g >> plog, p = g & (P - 1);
+  const TableInfo ti = table_info(a, t);
+  const int64_t b = b0 + j;
+  const bool active = b < a->B;
+  int64_t s = 0, e = 0;
+  if (active) bag_span(a, ti, t, b, s, e);
+  const RowReader<BUF> rows(a->tables[t], ti, k);
+  const int32_t* __restrict__ ids = a->ids + ti.id_base;
+  const uint32_t nrows = id_limit(ti);
+  const bool col = k * EPL < ti.dim;
+  float acc[EPL];
+#pragma unroll
+  for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
+  int bad = 0;
+  const int64_t stride = (int64_t)P * kUnroll;
+  int32_t idn[kUnroll];
+#pragma unroll
+  for (int u = 0; u < kUnroll; ++u) {
+    const int64_t r = s + p + (int64_t)u * P;
+    idn[u] = r < e ? ids[r] : -1;
+  }
+  for (int64_t r = s + p; r < e; r += stride) {
+    raw16_t raw[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      raw[u] = raw16_t{0, 0, 0, 0};
+      const bool in_bag = r + (int64_t)u * P < e;
+      const bool ok = in_bag && (uint32_t)idn[u] < nrows;
+      bad |= (in_bag && !ok);
+      if (ok && col) raw[u] = rows.load(idn[u]);
+    }
+    const int64_t rn = r + stride;
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t q = rn + (int64_t)u * P;
+      idn[u] = q < e ? ids[q] : -1;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
+  }
+  // the P slots of a bag are consecutive: combine them (every lane active)
+  for (int m = LPR; m < LPR * P; m <<= 1) {
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) acc[i] += __shfl_xor(acc[i], m, kWaveSize);
+  }
+  if (p == 0 && active && col) {
+    if (is_mean(a, t) && e > s) {
+      const float L = (float)(e - s);
+#pragma unroll
+      for (int i = 0; i < EPL; ++i) acc[i] = acc[i] / L;
+    }
+    store_lane<TOUT, EPL>(out_row<TOUT>(a, ti, b) + k * EPL, acc, (ti.flags & kTiOutVec) != 0);
+  }
+  return bad;
+}
+
+template <typename TOUT>
+__device__ __forceinline__ int direct_wave(KA a, int64_t w, int lane) {
+  const int64_t wpf = a->direct_wpf;
+  const int jlog = a->direct_jlog;
+  const int64_t t = uni(w / wpf);
+  const int64_t b0 = (w - t * wpf) << jlog;
+  const TableInfo ti = table_info(a, t);
+  const bool buf = use_buffer(ti), f16 = (ti.flags & kTiF16) != 0;
+  switch ((ti.flags >> kTiLprShift) & 7) {
+#define DPI_CASE(L, LPR)                                                                          \
+  case L:                                                                                         \
+    if (f16)                                                                                      \
+      return buf ? direct_bags<_Float16, TOUT, LPR, true>(a, t, b0, jlog, lane)                   \
+                 : direct_bags<_Float16, TOUT, LPR, false>(a, t, b0, jlog, lane);                 \
+    return buf ? direct_bags<float, TOUT, LPR, true>(a, t, b0, jlog, lane)                        \
+               : direct_bags<float, TOUT, LPR, false>(a, t, b0, jlog, lane);
+    DPI_FOR_LPR(DPI_CASE)
+#undef DPI_CASE
+    default:
+      return 0;
+  }
+}
+
+// four waves per SIMD, as the mixed kernel it falls back to
+template <typename TOUT>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void lookup_direct_kernel(const LookupArgs args) {
+  (void)args;
+  const KA a = (KA)__builtin_amdgcn_kernarg_segment_ptr();
+  if (a->status[0] & kStatusBadOffsets) return;   // the plan rejected the offsets
+  if (a->status[1] != 0) {                        // a long bag: the plan's partition
+    wave_body<Mixed<TOUT>>(a);
+    return;
+  }
+  const int lane = threadIdx.x & (kWaveSize - 1);
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
+  if (w >= a->direct_wpf * a->T) return;
+  const int bad = direct_wave<TOUT>(a, w, lane);
+  if (__any(bad) && lane == 0)
+    __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
 // Input-first allocation (the alternative of §IV-C, kept for the paper's
 // allocation comparison): one lane per bag.  A wave takes 64 consecutive bags
 // of one field; each lane walks its own bag's rows and, 16 bytes at a time,
@@ -894,6 +1016,17 @@ hipError_t launch_lookup(const LookupArgs& a, hipStream_t s) {
       default:
         return hipErrorInvalidValue;
     }
+    return hipGetLastError();
+  }
+  if (a.direct_jlog >= 0) {
+    // enough waves for either mode: bag groups, or the plan's waves
+    const int64_t waves = std::max<int64_t>(a.direct_wpf * a.T, a.grid_waves);
+    const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
+    if (blocks <= 0) return hipSuccess;
+    if (a.out_f16)
+      hipLaunchKernelGGL(lookup_direct_kernel<_Float16>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+    else
+      hipLaunchKernelGGL(lookup_direct_kernel<float>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
     return hipGetLastError();
   }
   const int64_t blocks = (a.grid_waves + kWavesPerBlock - 1) / kWavesPerBlock;

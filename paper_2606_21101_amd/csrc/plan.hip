@@ -364,7 +364,7 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
   constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
   bool bad = plan_setup_block(pa, blk, nblocks);
 
-  int64_t v[3] = {0, 0, 0};   // items, cost, malformed offsets
+  int64_t v[4] = {0, 0, 0, 0};   // items, cost, malformed offsets, long bags
   if (p.TB > 0) {
     __shared__ FieldBytes s_f;
     stage_fields(pa, s_f);
@@ -381,18 +381,19 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
       for (int k = 0; k < CH; ++k) {
         v[0] += s.n[k];
         v[1] += s.c[k];
+        v[3] += s.n[k] > kDirectMaxItems ? 1 : 0;
       }
       bad |= s.bad;
     }
   }
   v[2] = bad ? 1 : 0;
-  __shared__ int64_t s_red[kWavesPerBlock][3];
-  block_sums<3>(v, s_red);
+  __shared__ int64_t s_red[kWavesPerBlock][4];
+  block_sums<4>(v, s_red);
   if (tid == 0) {
     const int64_t nb = p.nblk;
     d.block_sum[blk] = v[0];
     d.block_sum[nb + blk] = v[1];
-    d.block_sum[2 * nb + blk] = v[2];
+    d.block_sum[2 * nb + blk] = v[2] | (v[3] << 1);   // malformed flag, long bags above it
   }
 }
 
@@ -416,7 +417,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_tiles_kernel(const PlanArgs
     const bool in = i < nb;
     const int64_t ic = in ? i : nb - 1;
     const int64_t si = in ? bs[ic] : 0, sc = in ? bs[nb + ic] : 0;
-    err |= (in && bs[2 * nb + ic] != 0) ? 1 : 0;
+    err |= (in && (bs[2 * nb + ic] & 1) != 0) ? 1 : 0;
     const int64_t xi = wave_incl_scan(si, lane), xc = wave_incl_scan(sc, lane);
     if (lane == 63) {
       s_w[buf][0][wv] = xi;
@@ -560,11 +561,12 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
 
   // this tile's exclusive prefix and the totals
   int64_t pre_i, pre_c, N, S;
+  int64_t nlong = 1;   // bags of more than kDirectMaxItems items (not counted beyond kPlanDirectTiles tiles)
   bool err;
   if constexpr (SINGLE) {
     static_assert(V <= kPlanChunk, "one group of slabs");
     __syncthreads();   // field bytes
-    int64_t v[3] = {0, 0, setup_bad ? 1 : 0};
+    int64_t v[4] = {0, 0, setup_bad ? 1 : 0, 0};
     if (p.TB > 0) {
       SlabBags<CH> s0;
       slab_cost<CH>(pa, s_f, raw, s0);
@@ -572,19 +574,21 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
       for (int k = 0; k < CH; ++k) {
         v[0] += s0.n[k];
         v[1] += s0.c[k];
+        v[3] += s0.n[k] > kDirectMaxItems ? 1 : 0;
       }
       v[2] += s0.bad ? 1 : 0;
     }
-    __shared__ int64_t s_tot[kWavesPerBlock][3];
-    block_sums<3>(v, s_tot);
+    __shared__ int64_t s_tot[kWavesPerBlock][4];
+    block_sums<4>(v, s_tot);
     pre_i = 0;
     pre_c = 0;
     N = v[0];
     S = v[1];
     err = v[2] != 0;
+    nlong = v[3];
   } else if (nb <= kPlanDirectTiles) {
     // from the tile sums: every entry loaded at once, then block sums
-    int64_t v[5] = {0, 0, 0, 0, 0};   // prefix items, prefix cost, items, cost, malformed
+    int64_t v[6] = {0, 0, 0, 0, 0, 0};   // prefix items, prefix cost, items, cost, malformed, long bags
 #pragma unroll
     for (int j = 0; j < kPlanDirectTiles / kScanThreads; ++j) {
       const int64_t i = tid + (int64_t)j * kScanThreads;
@@ -595,15 +599,17 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
       v[1] += before ? sc : 0;
       v[2] += in ? si : 0;
       v[3] += in ? sc : 0;
-      v[4] += (in && se != 0) ? 1 : 0;
+      v[4] += (in && (se & 1) != 0) ? 1 : 0;
+      v[5] += in ? se >> 1 : 0;
     }
-    __shared__ int64_t s_red[kWavesPerBlock][5];
-    block_sums<5>(v, s_red);
+    __shared__ int64_t s_red[kWavesPerBlock][6];
+    block_sums<6>(v, s_red);
     pre_i = v[0];
     pre_c = v[1];
     N = v[2];
     S = v[3];
     err = v[4] != 0;
+    nlong = v[5];
   } else {
     // plan_tiles left exclusive prefixes in place and the totals after them
     pre_i = bs[blk];
@@ -634,8 +640,9 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     d.bcb[p.TB] = S;
     d.wib[0] = 0;
     d.wave_bag[0] = 0;
-    // the only writer of the status word during planning; lookups latch later
-    *d.status = err ? kStatusBadOffsets : 0;
+    // the only writer of the status words during planning; lookups latch later
+    d.status[0] = err ? kStatusBadOffsets : 0;
+    d.status[1] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
   }
   if (p.TB == 0) return;
 
@@ -812,7 +819,8 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     h[kHdrCost] = S;
     h[kHdrTotalIds] = p.total_ids;
     h[kHdrWaveReq] = p.waves_req;
-    *d.status = bad ? kStatusBadOffsets : 0;
+    d.status[0] = bad ? kStatusBadOffsets : 0;
+    d.status[1] = 0;   // every bag is one item
   }
   const int64_t first = (int64_t)blockIdx.x * kScanThreads + tid, stride = (int64_t)gridDim.x * kScanThreads;
   const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;

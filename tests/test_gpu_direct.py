@@ -1,0 +1,125 @@
+"""Small batches looked up bag by bag (no partition), against the oracle.
+
+With the wave count left to the library, a batch of at most 16,384 bags whose
+fields all take the 16-byte row path is pooled bag by bag; a bag of more than
+four chunks anywhere in the batch sends the same launch back to the plan's
+partition.  Every case is also run with an explicit wave count (the plan's
+partition) and both results are checked against the oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_21101_amd import dpi
+from test_gpu_edges import check, random_problem, run_case
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("B", [1, 2, 3, 5, 33, 100, 257])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.float16])
+def test_direct_mixed_classes(B, out_dtype):
+    # rows of 16 .. 1024 bytes: 64 down to 1 slots per wave, fp16 and fp32
+    dims = [4, 8, 16, 32, 64, 128, 256, 8, 64, 512]
+    dtypes = [0, 0, 0, 0, 0, 0, 0, 1, 1, 1]
+    rng = np.random.default_rng(1000 + B)
+    tables, ids, offs, pool = random_problem(rng, dims, dtypes, B, 40, rows=300)
+    out, st, _, _ = run_case(tables, ids, offs, pool, B, out_dtype)
+    assert st == dpi.DPI_OK
+    check(tables, ids, offs, pool, B, out)
+    out_p, st_p, _, _ = run_case(tables, ids, offs, pool, B, out_dtype, num_waves=7)
+    assert st_p == dpi.DPI_OK
+    check(tables, ids, offs, pool, B, out_p)
+
+
+@pytest.mark.parametrize("B", [1, 4, 64])
+def test_direct_one_field_long_bags_up_to_the_limit(B):
+    # bags of up to 4 chunks of 32 ids (128 rows) stay on the bag-by-bag path
+    rng = np.random.default_rng(7 + B)
+    tables, ids, offs, pool = random_problem(rng, [32], [1], B, 128, rows=1000, p_empty=0.2)
+    offs[0, 1:] = np.cumsum(np.r_[128, np.diff(offs[0])[1:]])   # the first bag has exactly 128 ids
+    ids = rng.integers(0, 1000, int(offs[0, -1])).astype(np.int32)
+    for pool_t in ([0], [1]):
+        out, st, _, _ = run_case(tables, ids, offs, pool_t, B)
+        assert st == dpi.DPI_OK
+        check(tables, ids, offs, pool_t, B, out)
+
+
+@pytest.mark.parametrize("long_len", [129, 1000, 20000])
+def test_direct_falls_back_for_a_long_bag(long_len):
+    rng = np.random.default_rng(long_len)
+    B = 20
+    tables, ids, offs, pool = random_problem(rng, [16, 64, 8], [0, 1, 0], B, 30, rows=500)
+    lens = np.diff(offs, axis=1)
+    lens[1, 7] = long_len
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    ids = np.concatenate([rng.integers(0, 500, int(offs[t, -1])) for t in range(3)]).astype(np.int32)
+    for od in (torch.float32, torch.float16):
+        out, st, _, _ = run_case(tables, ids, offs, pool, B, od)
+        assert st == dpi.DPI_OK
+        check(tables, ids, offs, pool, B, out)
+
+
+def test_direct_onehot_mixed_classes_bit_exact():
+    # NULL offsets with fields of different row classes take the bag-by-bag path
+    rng = np.random.default_rng(11)
+    dims, dtypes, B = [16, 8, 64, 4], [0, 1, 1, 0], 77
+    tables, _, _, pool = random_problem(rng, dims, dtypes, B, 1, rows=90)
+    ids = np.concatenate([rng.integers(0, 90, B) for _ in dims]).astype(np.int32)
+    for od in (torch.float32, torch.float16):
+        out, st, _, _ = run_case(tables, ids, None, pool, B, od)
+        assert st == dpi.DPI_OK
+        if od == torch.float32:
+            check(tables, ids, None, pool, B, out, exact=True)
+        else:
+            check(tables, ids, None, pool, B, out)
+
+
+def test_direct_empty_bags_and_signed_zero():
+    rng = np.random.default_rng(12)
+    tables, _, _, _ = random_problem(rng, [16, 32], [0, 1], 9, 3, rows=20)
+    tables[0][3] = -0.0
+    offs = np.array([[0, 0, 1, 1, 3, 3, 3, 4, 4, 4], [0, 0, 0, 0, 0, 0, 0, 0, 0, 2]], np.int32)
+    ids = np.array([3, 3, 3, 5, 1, 2], np.int32)
+    out, st, _, _ = run_case(tables, ids, offs, [0, 1], 9)
+    assert st == dpi.DPI_OK
+    check(tables, ids, offs, [0, 1], 9, out)
+    y = out.cpu().numpy()
+    assert np.all(y[[0, 2, 4, 5, 7, 8], :16] == 0)
+    assert not np.signbit(y[1, :16]).any()          # a pooled -0 row is +0, as on every path
+    assert np.all(y[:8, 16:] == 0)
+
+
+def test_direct_bad_ids_reported_and_skipped():
+    rng = np.random.default_rng(13)
+    tables, ids, offs, pool = random_problem(rng, [16, 8], [0, 0], 12, 6, p_empty=0.0)
+    bad_ids = ids.copy()
+    bad_ids[2] = -5
+    bad_ids[len(ids) - 1] = 50
+    out, st, _, _ = run_case(tables, bad_ids, offs, [0, 0], 12)
+    assert st == dpi.DPI_ERR_BAD_ID
+    fixed = bad_ids.copy()
+    fixed[fixed < 0] = 50
+    tables_z = [np.concatenate([t, np.zeros((1, t.shape[1]), t.dtype)]) for t in tables]
+    check(tables_z, fixed, offs, [0, 0], 12, out)
+
+
+def test_direct_bad_offsets_make_the_lookup_a_no_op():
+    tabs = [torch.zeros((10, 16), device="cuda"), torch.zeros((10, 8), device="cuda", dtype=torch.float16)]
+    from paper_2606_21101_amd.lookup import FusedLookup
+    fl = FusedLookup(tabs)
+    offs = torch.tensor([[0, 2, 1], [0, 1, 2]], dtype=torch.int32, device="cuda")
+    plan = fl.plan(offs, 2, 4)
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_OFFSETS
+    out = torch.full((2, 24), 7.0, device="cuda")
+    fl.lookup(plan, torch.zeros(4, dtype=torch.int32, device="cuda"), offs, out)
+    torch.cuda.synchronize()
+    assert torch.all(out == 7.0)
+
+
+def test_direct_repeated_lookups_deterministic():
+    rng = np.random.default_rng(14)
+    tables, ids, offs, pool = random_problem(rng, [64, 16, 8], [1, 0, 0], 50, 60)
+    a, _, _, _ = run_case(tables, ids, offs, pool, 50)
+    b, _, _, _ = run_case(tables, ids, offs, pool, 50)
+    assert torch.equal(a, b)
