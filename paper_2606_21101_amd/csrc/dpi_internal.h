@@ -27,7 +27,7 @@ constexpr int kDefaultWavesPerCU = 16;
 // longer ones) and the batch has at most kDirectMaxBags bags.
 constexpr int kDirectMaxItems = 4;
 constexpr int kDirectGroupRows = 8;   // rows in flight per slot
-constexpr int64_t kDirectMaxBags = 16384;
+constexpr int64_t kDirectMaxBags = 32768;
 
 // status word bits (device-latched errors)
 constexpr int kStatusBadOffsets = 1;

@@ -1,6 +1,6 @@
 """Small batches looked up bag by bag (no partition), against the oracle.
 
-With the wave count left to the library, a batch of at most 16,384 bags whose
+With the wave count left to the library, a batch of at most 32,768 bags whose
 fields all take the 16-byte row path is pooled bag by bag; a bag of more than
 four chunks anywhere in the batch sends the same launch back to the plan's
 partition.  Every case is also run with an explicit wave count (the plan's
