@@ -129,7 +129,8 @@ size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total
  * the bags' item counts and costs, their exclusive prefix sums over all
  * fields (field-major), and a partition of the items into W waves of nearly
  * equal cost.  The plan's arrays are defined step by step in the oracle's
- * documentation and exported by dpi_plan_export.
+ * documentation and exported by dpi_plan_export (which notes when the
+ * partition is computed).
  *   table_meta: host [num_tables]; offsets: device [T][B+1] or NULL;
  *   total_ids:  number of ids (sum of offsets[t][B], or T*B);
  *   opts:       NULL for defaults;
@@ -308,6 +309,12 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan);
  * bag_item_base[T*B+1], bag_cost_base[T*B+1], wave_item_begin[W+1] with W =
  * header16[3].  header16 = [abi, T, B, W, C, K, out_dtype, flags, total_dim,
  * items N, total cost S, total_ids, split bags, requested waves, 0, 0].
+ * For a batch that dpi_lookup pools bag by bag, the planning launch leaves
+ * out the wave partition (the lookup does not read it) unless some bag is
+ * longer than 4 items; the first export of such a plan then plans the batch
+ * again with the partition, on the plan's stream, from the offsets given to
+ * dpi_plan -- they must still hold the batch, and no lookup of this plan may
+ * be in flight on another stream.
  */
 dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
                            int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);

@@ -107,6 +107,9 @@ struct dpi_plan_s {
   bool onehot;
   int32_t uniform_class;   // shared row class of every field, or -1
   int32_t direct_jlog;     // small batches looked up bag by bag: log2 of bags per wave, or -1
+  int32_t sticky_status;   // status bits latched by lookups before a re-plan
+  bool partitioned;        // a lazy plan has been recomputed with its partition
+  PlanArgs args;           // the planning launch (re-run with the partition on export)
   hipStream_t stream;
   char* ws;
   Layout layout;
@@ -331,11 +334,13 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   p.waves_req = o.num_waves;
   p.total_d = total_d;
   p.offsets = offsets;
+  p.lazy_partition = plan->direct_jlog >= 0 ? 1 : 0;
   pa.d = d;
   for (int t = 0; t < num_tables; ++t) {
     pa.packed[t] = (uint32_t)table_meta[t].dim | ((uint32_t)row_class[t] << 17);
     pa.num_rows[t] = table_meta[t].num_rows;
   }
+  plan->args = pa;
   const hipError_t e = launch_plan(pa, plan->stream);
   if (e != hipSuccess) {
     delete plan;
@@ -503,6 +508,7 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
   int32_t status = 0;
   e = hipMemcpy(&status, plan->ws + plan->layout.status, sizeof(status), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+  status |= plan->sticky_status;
   if (status & kStatusBadOffsets) return fail(DPI_ERR_BAD_OFFSETS, "device rejected the offsets");
   if (status & kStatusBadId) return fail(DPI_ERR_BAD_ID, "a lookup met an id outside its table");
   return DPI_OK;
@@ -514,6 +520,24 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
   hipError_t e = hipStreamSynchronize(plan->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   const Layout& L = plan->layout;
+  if (plan->args.p.lazy_partition && !plan->partitioned) {
+    // the planning launch skipped the wave partition if no bag was long:
+    // plan again with it (from the offsets given to dpi_plan), keeping the
+    // status bits earlier lookups latched
+    int32_t status[2] = {0, 0};
+    e = hipMemcpy(status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+    if (status[1] == 0) {
+      plan->sticky_status |= status[0] & kStatusBadId;
+      PlanArgs full = plan->args;
+      full.p.lazy_partition = 0;
+      e = launch_plan(full, plan->stream);
+      if (e != hipSuccess) return hip_fail(e, "plan launch");
+      e = hipStreamSynchronize(plan->stream);
+      if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+    }
+    plan->partitioned = true;
+  }
   int64_t hdr[16];
   e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy header");

@@ -87,6 +87,7 @@ struct PlanParams {
   int32_t nblk;       // tiles of slabs * kScanThreads bags (at least 1)
   int32_t slabs;      // bags per thread: 1, 2, 4, ..., kPlanMaxSlabs
   int32_t c_shift;    // log2(C) when C is a power of two, else -1
+  int32_t lazy_partition;  // skip the wave partition when no bag is longer than kDirectMaxItems items
   int64_t B;
   int64_t TB;
   int64_t total_ids;

@@ -541,23 +541,30 @@ __device__ __forceinline__ void resolve_candidates(const BoundaryOut& o, const T
 // SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
 // its sums come straight from the block instead of from plan_reduce, and
 // setup_bad carries plan_setup_block's verdict.
+template <int V>
+constexpr int scan_chunk() { return V < kPlanChunk ? V : kPlanChunk; }
+
+// Field bytes to LDS and the loads of the tile's first group of slabs; the
+// caller issues them early so that they are in flight while the tile prefix
+// (and, for a single block, the setup) is formed.
+template <int V>
+__device__ __forceinline__ void plan_scan_prologue(PA pa, int64_t blk, FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw) {
+  if (pa->p.TB > 0) {
+    stage_fields(pa, s_f);
+    slab_load<scan_chunk<V>()>(pa, blk * (int64_t)kScanThreads * V + threadIdx.x, raw);
+  }
+}
+
 template <int V, bool SINGLE>
-__device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_bad) {
+__device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_bad, FieldBytes& s_f,
+                                                SlabRaw<scan_chunk<V>()>& raw) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int64_t nb = p.nblk;
   const int64_t* bs = d.block_sum;
-  constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
+  constexpr int CH = scan_chunk<V>();
   const int64_t tile0 = blk * (int64_t)kScanThreads * V;
-
-  // the first group's offsets, in flight while the tile prefix is formed
-  __shared__ FieldBytes s_f;
-  SlabRaw<CH> raw;
-  if (p.TB > 0) {
-    stage_fields(pa, s_f);
-    slab_load<CH>(pa, tile0 + tid, raw);
-  }
 
   // this tile's exclusive prefix and the totals
   int64_t pre_i, pre_c, N, S;
@@ -619,6 +626,10 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     err = bs[3 * nb + 2] != 0;
   }
   const int64_t W = p.waves_req < N ? p.waves_req : N;
+  // a batch the lookup pools bag by bag needs no partition unless it has a
+  // long bag (then the lookup falls back to the partition); the host
+  // recomputes the plan with the partition when it is exported
+  const bool partition = !(p.lazy_partition && nlong == 0);
 
   if (blk == 0 && tid == 0) {
     // the split counter was zeroed by plan_reduce; other blocks add to it
@@ -715,7 +726,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
         d.bib[bag] = ibase;
         d.bcb[bag] = E_lo;
       }
-      if (W == 0) continue;
+      if (W == 0 || !partition) continue;
       // filter in double: both products are within (x + 1) * 2^-50 of E*W/S,
       // so equal floors of the widened interval prove it holds no target
       const double x_lo = (double)E_lo * scale, x_hi = (double)E_hi * scale;
@@ -753,7 +764,11 @@ __global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArg
 template <int V>
 __global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs args) {
   (void)args;
-  plan_scan_block<V, false>((PA)__builtin_amdgcn_kernarg_segment_ptr(), blockIdx.x, false);
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  __shared__ FieldBytes s_f;
+  SlabRaw<scan_chunk<V>()> raw;
+  plan_scan_prologue<V>(pa, blockIdx.x, s_f, raw);
+  plan_scan_block<V, false>(pa, blockIdx.x, false, s_f, raw);
 }
 
 // A batch of one tile: one block, one launch; the bag sums never leave the
@@ -763,8 +778,11 @@ template <int V>
 __global__ __launch_bounds__(kScanThreads) void plan_single_kernel(const PlanArgs args) {
   (void)args;
   const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  __shared__ FieldBytes s_f;
+  SlabRaw<scan_chunk<V>()> raw;
+  plan_scan_prologue<V>(pa, 0, s_f, raw);   // the bags' offsets load during the setup
   const bool bad = plan_setup_block(pa, 0, 1);
-  plan_scan_block<V, true>(pa, 0, bad);
+  plan_scan_block<V, true>(pa, 0, bad, s_f, raw);
 }
 
 // ---------------------------------------------------------------------------

@@ -123,3 +123,74 @@ def test_direct_repeated_lookups_deterministic():
     a, _, _, _ = run_case(tables, ids, offs, pool, 50)
     b, _, _, _ = run_case(tables, ids, offs, pool, 50)
     assert torch.equal(a, b)
+
+
+# --- the plan of a bag-by-bag batch: partition computed on export -----------
+
+import oracle                                   # noqa: E402
+from parity import check_outputs, default_waves, oracle_ref, plan_args   # noqa: E402
+from synth import configs, generate as G        # noqa: E402
+from paper_2606_21101_amd.lookup import FusedLookup   # noqa: E402
+
+PLAN_KEYS = ("header", "col_base", "id_base", "bag_item_base", "bag_cost_base", "wave_item_begin")
+
+
+def assert_plan_equals_oracle(got, dims, dtypes, out_dtype, offs_np, B, total, W):
+    ref = oracle.plan(dims, dtypes, out_dtype, offs_np, B, total, 32, 64, W, 0)
+    for k in PLAN_KEYS:
+        assert np.array_equal(got[k], ref[k]), (k, got[k][:20], ref[k][:20])
+
+
+@pytest.mark.parametrize("batch", [1, 16, 128, 512])
+def test_lazy_partition_export_matches_oracle(batch):
+    cfg = configs.get(5, batch=batch)
+    tables = [G.make_table(cfg, t, "cuda") for t in range(cfg.num_tables)]
+    b = G.make_batch(cfg, device="cuda")
+    dims, dtypes, out_dtype = plan_args(cfg)
+    fl = FusedLookup(tables, None, torch.float32, num_rows=G.table_sizes(cfg))
+    offs_np = b.offsets.cpu().numpy()
+    total = int(b.total_ids)
+    W = default_waves(cfg, total)
+    # lookup first (no partition computed), then export, then a second lookup
+    plan = fl.plan(b.offsets, cfg.batch, total)
+    out1 = fl.lookup(plan, b.ids, b.offsets)
+    got = dpi.dpi_plan_export(plan)
+    assert_plan_equals_oracle(got, dims, dtypes, out_dtype, offs_np, cfg.batch, total, W)
+    out2 = fl.lookup(plan, b.ids, b.offsets)
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_OK
+    assert torch.equal(out1, out2)
+    # export straight after planning
+    plan2 = fl.plan(b.offsets, cfg.batch, total)
+    got2 = dpi.dpi_plan_export(plan2)
+    assert_plan_equals_oracle(got2, dims, dtypes, out_dtype, offs_np, cfg.batch, total, W)
+    assert torch.equal(fl.lookup(plan2, b.ids, b.offsets), out1)
+    p, ref, mag = oracle_ref(cfg)
+    y = out1[torch.from_numpy(p["samples"]).cuda()].double().cpu().numpy()
+    check_outputs(y, ref, mag, False, False)
+
+
+def test_lazy_partition_long_bag_export_matches_oracle():
+    rng = np.random.default_rng(21)
+    B, dims, dtypes = 30, [16, 64], [0, 1]
+    lengths = rng.integers(0, 20, size=(2, B))
+    lengths[0, 3] = 300                                  # more than 4 items: partition in the planning launch
+    offs_np = G.offsets_from_lengths(lengths)
+    total = int(lengths.sum())
+    tabs = [torch.zeros((5, d), dtype=torch.float16 if dt else torch.float32, device="cuda")
+            for d, dt in zip(dims, dtypes)]
+    fl = FusedLookup(tabs)
+    plan = fl.plan(torch.from_numpy(offs_np).cuda(), B, total)
+    got = dpi.dpi_plan_export(plan)
+    W = dpi.dpi_default_waves(2, B, total)
+    assert_plan_equals_oracle(got, dims, dtypes, 0, offs_np, B, total, W)
+
+
+def test_lazy_partition_export_keeps_bad_id_status():
+    rng = np.random.default_rng(22)
+    tables, ids, offs, pool = random_problem(rng, [16, 8], [0, 0], 12, 6, p_empty=0.0)
+    ids = ids.copy()
+    ids[1] = 77                                          # outside the 50-row table
+    out, st, fl, plan = run_case(tables, ids, offs, pool, 12)
+    assert st == dpi.DPI_ERR_BAD_ID
+    dpi.dpi_plan_export(plan)                            # plans again with the partition
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_ID
