@@ -460,15 +460,17 @@ def main():
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     setup_s = time.perf_counter() - t_setup
 
+    table_ptrs = dpi.table_array(tables)
+    pool_arr = None if pool is None else dpi.pooling_array(pool)
+
     def step(i, ev=None):
         bt = batches[i % len(batches)]
         if ev is not None:
             ev[0].record(stream)
-        plan = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, fl.opts(args.num_waves), ws,
-                            ws_bytes, stream=stream)
+        plan = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, opts, ws, ws_bytes, stream=stream)
         if ev is not None:
             ev[1].record(stream)
-        dpi.dpi_lookup(plan, tables, bt.ids, bt.offsets, pool, out, stream=stream)
+        dpi.dpi_lookup(plan, table_ptrs, bt.ids, bt.offsets, pool_arr, out, stream=stream)
         if ev is not None:
             ev[2].record(stream)
         return plan

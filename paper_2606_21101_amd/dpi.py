@@ -213,11 +213,24 @@ def dpi_plan(table_meta, offsets, batch: int, total_ids: int, opts: Optional[dpi
     return Plan(out.value, T, batch, (workspace, offsets, table_meta))
 
 
+def table_array(tables) -> ctypes.Array:
+    """Host array of the tables' device pointers, as dpi_lookup takes it (build it
+    once and pass it to every lookup over the same tables)."""
+    return (ctypes.c_void_p * len(tables))(*[_ptr(t) for t in tables])
+
+
+def pooling_array(pooling: Sequence[int]) -> ctypes.Array:
+    return (ctypes.c_int32 * len(pooling))(*[int(p) for p in pooling])
+
+
 def dpi_lookup(plan: Plan, tables, ids, offsets, pooling: Optional[Sequence[int]], out, stream=None) -> None:
+    """tables / pooling: sequences, or the arrays table_array / pooling_array built."""
     lib = load()
     T = plan.num_tables
-    ptrs = (ctypes.c_void_p * T)(*[_ptr(t) for t in tables])
-    pool = None if pooling is None else (ctypes.c_int32 * T)(*[int(p) for p in pooling])
+    ptrs = tables if isinstance(tables, ctypes.Array) else table_array(tables)
+    pool = pooling if (pooling is None or isinstance(pooling, ctypes.Array)) else pooling_array(pooling)
+    if len(ptrs) != T or (pool is not None and len(pool) != T):
+        raise DpiError(DPI_ERR_INVALID_ARG, "tables / pooling must have one entry per field")
     st = lib.dpi_lookup(ctypes.c_void_p(plan.handle), ptrs, _ptr(ids), _ptr(offsets), pool, _ptr(out),
                         _stream(stream))
     _check(st)

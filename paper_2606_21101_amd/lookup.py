@@ -30,6 +30,9 @@ class FusedLookup:
         self.chunk_rows, self.item_cost_k, self.flags = chunk_rows, item_cost_k, flags
         self.device = self.tables[0].device
         self._ws = None
+        # host arrays handed to every lookup (built once)
+        self._table_ptrs = dpi.table_array(self.tables)
+        self._pool = None if self.pooling is None else dpi.pooling_array(self.pooling)
 
     @property
     def total_dim(self) -> int:
@@ -56,7 +59,7 @@ class FusedLookup:
                out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
         if out is None:
             out = torch.empty((plan.batch, self.total_dim), dtype=self.out_dtype, device=self.device)
-        dpi.dpi_lookup(plan, self.tables, ids, offsets, self.pooling, out, stream=stream)
+        dpi.dpi_lookup(plan, self._table_ptrs, ids, offsets, self._pool, out, stream=stream)
         return out
 
     def __call__(self, ids: torch.Tensor, offsets: Optional[torch.Tensor], batch: int,
