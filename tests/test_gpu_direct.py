@@ -194,3 +194,18 @@ def test_lazy_partition_export_keeps_bad_id_status():
     assert st == dpi.DPI_ERR_BAD_ID
     dpi.dpi_plan_export(plan)                            # plans again with the partition
     assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_ID
+
+
+@pytest.mark.parametrize("B", [8192, 8193])
+def test_bag_limit_both_sides(B):
+    # 4 fields: 32768 bags (bag by bag) and 32772 bags (the partition), short bags
+    rng = np.random.default_rng(B)
+    dims, dtypes = [16, 8, 32, 64], [0, 1, 0, 1]
+    tables, ids, offs, pool = random_problem(rng, dims, dtypes, B, 6, rows=2000)
+    for od in (torch.float32, torch.float16):
+        out, st, _, plan = run_case(tables, ids, offs, pool, B, od)
+        assert st == dpi.DPI_OK
+        check(tables, ids, offs, pool, B, out)
+    got = dpi.dpi_plan_export(plan)
+    W = dpi.dpi_default_waves(4, B, len(ids))
+    assert_plan_equals_oracle(got, dims, dtypes, 1, offs, B, len(ids), W)
