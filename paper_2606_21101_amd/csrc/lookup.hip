@@ -646,14 +646,19 @@ __device__ __forceinline__ void wave_body(KA a) {
   int64_t blk = blockIdx.x;
   if (a->xcd_affine) blk = xcd_affine_block(blk, gridDim.x);
   const int64_t w = blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
+  if (w >= a->grid_waves) return;
+  // the plan's wave count and verdict and this wave's range, requested
+  // together (the arrays hold grid_waves + 1 entries; values past the plan's
+  // W are never used)
   const int64_t W = min(a->hdr[kHdrW], a->grid_waves);
-  if (w >= W) return;
-  if (*a->status & kStatusBadOffsets) return;   // the plan rejected the offsets
+  const int32_t st_err = *a->status;
   const int64_t i0 = a->wib[w], i1 = a->wib[w + 1];
+  const int64_t la = a->wave_bag[w], lz = a->wave_bag[w + 1];
+  if (w >= W) return;
+  if (st_err & kStatusBadOffsets) return;   // the plan rejected the offsets
   if (i0 >= i1) return;
   const int64_t TB = a->B * a->T;
   const int64_t C = a->C;
-  const int64_t la = a->wave_bag[w], lz = a->wave_bag[w + 1];
   const int64_t lb = (lz < TB && a->bib[lz] < i1) ? lz : lz - 1;
   const int64_t la_base = a->bib[la];
   const int64_t lb_base = a->bib[lb];
@@ -780,8 +785,15 @@ void lookup_onehot_kernel(const LookupArgs args) {
 // plan's partition (same kernel, wave_body), so one long bag never holds up
 // a whole lookup.
 // ---------------------------------------------------------------------------
+// Lane j < J of the wave holds the offsets of bag b0 + j (loaded before the
+// field's class is known); slots fetch theirs by a cross-lane read.
+struct DirectOffsets {
+  int32_t lo, hi;
+};
+
 template <typename TIN, typename TOUT, int LPR, bool BUF>
-__device__ __forceinline__ int direct_bags(KA a, int64_t t, int64_t b0, int jlog, int lane) {
+__device__ __forceinline__ int direct_bags(KA a, const TableInfo& ti, int64_t t, int64_t b0, int jlog,
+                                           DirectOffsets o, int lane) {
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
   constexpr int GLOG = __builtin_ctz(G);
@@ -789,11 +801,14 @@ __device__ __forceinline__ int direct_bags(KA a, int64_t t, int64_t b0, int jlog
   const int plog = GLOG - jlog;   // J <= G for every field (chosen on the host)
   const int P = 1 << plog;
   const int j = g >> plog, p = g & (P - 1);
-  const TableInfo ti = table_info(a, t);
   const int64_t b = b0 + j;
   const bool active = b < a->B;
-  int64_t s = 0, e = 0;
-  if (active) bag_span(a, ti, t, b, s, e);
+  // clamped to the field's id list as bag_span does
+  const int64_t nnz = ti.nnz;
+  int64_t s = __shfl(o.lo, j, kWaveSize), e = __shfl(o.hi, j, kWaveSize);
+  s = s < 0 ? 0 : (s > nnz ? nnz : s);
+  e = e < 0 ? 0 : (e > nnz ? nnz : e);
+  if (e < s || !active) e = s;
   const RowReader<BUF> rows(a->tables[t], ti, k);
   const int32_t* __restrict__ ids = a->ids + ti.id_base;
   const uint32_t nrows = id_limit(ti);
@@ -845,21 +860,18 @@ __device__ __forceinline__ int direct_bags(KA a, int64_t t, int64_t b0, int jlog
 }
 
 template <typename TOUT>
-__device__ __forceinline__ int direct_wave(KA a, int64_t w, int lane) {
-  const int64_t wpf = a->direct_wpf;
+__device__ __forceinline__ int direct_wave(KA a, const TableInfo& ti, int64_t t, int64_t b0, DirectOffsets o,
+                                           int lane) {
   const int jlog = a->direct_jlog;
-  const int64_t t = uni(w / wpf);
-  const int64_t b0 = (w - t * wpf) << jlog;
-  const TableInfo ti = table_info(a, t);
   const bool buf = use_buffer(ti), f16 = (ti.flags & kTiF16) != 0;
   switch ((ti.flags >> kTiLprShift) & 7) {
 #define DPI_CASE(L, LPR)                                                                          \
   case L:                                                                                         \
     if (f16)                                                                                      \
-      return buf ? direct_bags<_Float16, TOUT, LPR, true>(a, t, b0, jlog, lane)                   \
-                 : direct_bags<_Float16, TOUT, LPR, false>(a, t, b0, jlog, lane);                 \
-    return buf ? direct_bags<float, TOUT, LPR, true>(a, t, b0, jlog, lane)                        \
-               : direct_bags<float, TOUT, LPR, false>(a, t, b0, jlog, lane);
+      return buf ? direct_bags<_Float16, TOUT, LPR, true>(a, ti, t, b0, jlog, o, lane)            \
+                 : direct_bags<_Float16, TOUT, LPR, false>(a, ti, t, b0, jlog, o, lane);          \
+    return buf ? direct_bags<float, TOUT, LPR, true>(a, ti, t, b0, jlog, o, lane)                 \
+               : direct_bags<float, TOUT, LPR, false>(a, ti, t, b0, jlog, o, lane);
     DPI_FOR_LPR(DPI_CASE)
 #undef DPI_CASE
     default:
@@ -873,15 +885,35 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4
 void lookup_direct_kernel(const LookupArgs args) {
   (void)args;
   const KA a = (KA)__builtin_amdgcn_kernarg_segment_ptr();
-  if (a->status[0] & kStatusBadOffsets) return;   // the plan rejected the offsets
-  if (a->status[1] != 0) {                        // a long bag: the plan's partition
+  const int lane = threadIdx.x & (kWaveSize - 1);
+  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
+  // the plan's verdicts, the field's info and the wave's bag offsets are all
+  // requested before the first of them is needed (one round trip, not three)
+  const int32_t st_err = a->status[0], st_long = a->status[1];
+  const int64_t wpf = a->direct_wpf;
+  const bool mine = w < wpf * a->T;
+  const int64_t t = mine ? uni(w / wpf) : 0;
+  const int64_t b0 = (w - t * wpf) << a->direct_jlog;
+  DirectOffsets o{0, 0};
+  if (mine && lane < (1 << a->direct_jlog)) {
+    const int64_t bl = min(b0 + lane, a->B - 1);   // bags past the batch end are inactive
+    if (a->offsets) {
+      const int32_t* src = a->offsets + t * (a->B + 1) + bl;
+      o.lo = src[0];
+      o.hi = src[1];
+    } else {
+      o.lo = (int32_t)bl;
+      o.hi = (int32_t)bl + 1;
+    }
+  }
+  const TableInfo ti = table_info(a, t);
+  if (st_err & kStatusBadOffsets) return;   // the plan rejected the offsets
+  if (st_long != 0) {                       // a long bag: the plan's partition
     wave_body<Mixed<TOUT>>(a);
     return;
   }
-  const int lane = threadIdx.x & (kWaveSize - 1);
-  const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
-  if (w >= a->direct_wpf * a->T) return;
-  const int bad = direct_wave<TOUT>(a, w, lane);
+  if (!mine) return;
+  const int bad = direct_wave<TOUT>(a, ti, t, b0, o, lane);
   if (__any(bad) && lane == 0)
     __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
