@@ -153,13 +153,13 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
  *   pooling: host [T] of dpi_pooling, NULL = all sum;
  *   out:     device [B][sum dim] of the plan's out dtype.
  * A plan whose offsets were rejected on the device makes the lookup a no-op.
- * Small batches (at most 32768 bags, every row a multiple of 16 bytes and at
- * most 1024 bytes, wave count left at 0) are pooled bag by bag, without the
- * plan's partition: a wave takes a few bags of one field, each bag several
- * row slots.  If the plan counted a bag of more than 4 work items (4*C ids),
- * the same launch uses the partition instead.  An explicit wave count always
- * uses the partition.  Either way the results are within the same tolerance
- * and deterministic.
+ * Small and mid-size batches (at most 180000 bags, every row a multiple of
+ * 16 bytes and at most 1024 bytes, wave count left at 0) are pooled bag by
+ * bag, without the plan's partition: a wave takes a few bags of one field,
+ * each bag several row slots.  If the plan counted a bag of more than 4 work
+ * items (4*C ids), the same launch uses the partition instead.  An explicit
+ * wave count always uses the partition.  Either way the results are within
+ * the same tolerance and deterministic.
  */
 dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids,
                       const int32_t* offsets, const int32_t* pooling, void* out, void* stream);

@@ -121,7 +121,9 @@ struct dpi_plan_s {
 // library: a wave takes J = 2^jlog bags of one field, each pooled by G/J row
 // slots, where G = 64 / (row bytes / 16) is the field's slot count.  J is the
 // same for every field (at most the smallest G), chosen so that an average bag
-// needs about one group of 8 rows per slot, and no larger than the batch.
+// needs about one group of 8 rows per slot, then doubled while the grid holds
+// more than kDefaultWavesPerCU waves per compute unit, and no larger than the
+// batch.
 // Returns jlog, or -1 for the plan's partition (also the choice for one-hot
 // batches of one row class, which have their own kernel, and for the
 // input-first allocation).
@@ -139,6 +141,9 @@ int32_t direct_jlog(int32_t T, int64_t B, int64_t total_ids, const int32_t* row_
   int64_t slots = 1;                                          // slots an average bag fills with groups of 8
   while (slots * kDirectGroupRows < avg && slots < gmin) slots <<= 1;
   int64_t J = std::max<int64_t>(1, gmin / slots);
+  // larger batches: more bags per wave (up to one per slot) until the grid
+  // is no larger than the partition's default for mid-size batches
+  while (J < gmin && (int64_t)T * ((B + J - 1) / J) > (int64_t)kDefaultWavesPerCU * device_cus()) J <<= 1;
   while (J > 1 && J > B) J >>= 1;
   return ilog2((int)J);
 }

@@ -24,10 +24,12 @@ constexpr int kDefaultRowsPerWave = 2048;
 constexpr int kDefaultWavesPerCU = 16;
 // Small batches are looked up bag by bag, without the plan's partition, when
 // no bag holds more than kDirectMaxItems chunks of C ids (the plan counts the
-// longer ones) and the batch has at most kDirectMaxBags bags.
+// longer ones) and the batch has at most kDirectMaxBags bags (measured
+// crossover against the partition: bag by bag is 8-12 % faster per step at
+// 106 K and 160 K bags, 7 % slower at 213 K and 240 K).
 constexpr int kDirectMaxItems = 4;
 constexpr int kDirectGroupRows = 8;   // rows in flight per slot
-constexpr int64_t kDirectMaxBags = 32768;
+constexpr int64_t kDirectMaxBags = 180000;
 
 // status word bits (device-latched errors)
 constexpr int kStatusBadOffsets = 1;

@@ -1,6 +1,6 @@
 """Small batches looked up bag by bag (no partition), against the oracle.
 
-With the wave count left to the library, a batch of at most 32,768 bags whose
+With the wave count left to the library, a batch of at most 180,000 bags whose
 fields all take the 16-byte row path is pooled bag by bag; a bag of more than
 four chunks anywhere in the batch sends the same launch back to the plan's
 partition.  Every case is also run with an explicit wave count (the plan's
@@ -196,9 +196,9 @@ def test_lazy_partition_export_keeps_bad_id_status():
     assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_ID
 
 
-@pytest.mark.parametrize("B", [8192, 8193])
+@pytest.mark.parametrize("B", [45000, 45001])
 def test_bag_limit_both_sides(B):
-    # 4 fields: 32768 bags (bag by bag) and 32772 bags (the partition), short bags
+    # 4 fields: 180000 bags (bag by bag) and 180004 bags (the partition), short bags
     rng = np.random.default_rng(B)
     dims, dtypes = [16, 8, 32, 64], [0, 1, 0, 1]
     tables, ids, offs, pool = random_problem(rng, dims, dtypes, B, 6, rows=2000)
