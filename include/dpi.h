@@ -310,11 +310,11 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan);
  * header16[3].  header16 = [abi, T, B, W, C, K, out_dtype, flags, total_dim,
  * items N, total cost S, total_ids, split bags, requested waves, 0, 0].
  * For a batch that dpi_lookup pools bag by bag, the planning launch leaves
- * out the wave partition (the lookup does not read it) unless some bag is
- * longer than 4 items; the first export of such a plan then plans the batch
- * again with the partition, on the plan's stream, from the offsets given to
- * dpi_plan -- they must still hold the batch, and no lookup of this plan may
- * be in flight on another stream.
+ * out the bag prefixes and the wave partition (the lookup reads neither)
+ * unless some bag is longer than 4 items; the first export of such a plan
+ * then plans the batch again in full, on the plan's stream, from the offsets
+ * given to dpi_plan -- they must still hold the batch, and no lookup of this
+ * plan may be in flight on another stream.
  */
 dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
                            int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);

@@ -526,9 +526,9 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   const Layout& L = plan->layout;
   if (plan->args.p.lazy_partition && !plan->partitioned) {
-    // the planning launch skipped the wave partition if no bag was long:
-    // plan again with it (from the offsets given to dpi_plan), keeping the
-    // status bits earlier lookups latched
+    // the planning launch skipped the bag prefixes and the partition if no
+    // bag was long: plan again in full (from the offsets given to dpi_plan),
+    // keeping the status bits earlier lookups latched
     int32_t status[2] = {0, 0};
     e = hipMemcpy(status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");

@@ -626,9 +626,10 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     err = bs[3 * nb + 2] != 0;
   }
   const int64_t W = p.waves_req < N ? p.waves_req : N;
-  // a batch the lookup pools bag by bag needs no partition unless it has a
-  // long bag (then the lookup falls back to the partition); the host
-  // recomputes the plan with the partition when it is exported
+  // a batch the lookup pools bag by bag reads only the header, the status
+  // words and the field info unless it has a long bag (then the lookup falls
+  // back to the partition): no bag prefixes, no partition; the host plans
+  // again in full when the plan is exported
   const bool partition = !(p.lazy_partition && nlong == 0);
 
   if (blk == 0 && tid == 0) {
@@ -655,7 +656,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     d.status[0] = err ? kStatusBadOffsets : 0;
     d.status[1] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
   }
-  if (p.TB == 0) return;
+  if (p.TB == 0 || !partition) return;   // block-uniform
 
   __shared__ Targets g;
   __shared__ BoundaryOut o;
@@ -726,7 +727,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
         d.bib[bag] = ibase;
         d.bcb[bag] = E_lo;
       }
-      if (W == 0 || !partition) continue;
+      if (W == 0) continue;
       // filter in double: both products are within (x + 1) * 2^-50 of E*W/S,
       // so equal floors of the widened interval prove it holds no target
       const double x_lo = (double)E_lo * scale, x_hi = (double)E_hi * scale;
