@@ -309,9 +309,10 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan);
  * bag_item_base[T*B+1], bag_cost_base[T*B+1], wave_item_begin[W+1] with W =
  * header16[3].  header16 = [abi, T, B, W, C, K, out_dtype, flags, total_dim,
  * items N, total cost S, total_ids, split bags, requested waves, 0, 0].
- * For a batch that dpi_lookup pools bag by bag, the planning launch leaves
- * out the bag prefixes and the wave partition (the lookup reads neither)
- * unless some bag is longer than 4 items; the first export of such a plan
+ * When dpi_lookup will not read the partition (a batch pooled bag by bag,
+ * a one-hot batch of one row class, the input-first allocation), the
+ * planning launch leaves out the bag prefixes and the wave partition unless
+ * some bag is longer than 4 items; the first export of such a plan
  * then plans the batch again in full, on the plan's stream, from the offsets
  * given to dpi_plan -- they must still hold the batch, and no lookup of this
  * plan may be in flight on another stream.

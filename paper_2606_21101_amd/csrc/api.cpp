@@ -339,7 +339,12 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   p.waves_req = o.num_waves;
   p.total_d = total_d;
   p.offsets = offsets;
-  p.lazy_partition = plan->direct_jlog >= 0 ? 1 : 0;
+  // lookups that never read the partition: bag by bag, the one-hot kernel,
+  // the input-first allocation (the latter two never split a bag either)
+  const bool onehot_kernel = offsets == nullptr && uniform_class >= 0 && !(o.flags & DPI_FLAG_INPUT_FIRST);
+  const bool input_first = (o.flags & DPI_FLAG_INPUT_FIRST) != 0;
+  p.lazy_partition = (plan->direct_jlog >= 0 || onehot_kernel || input_first) ? 1 : 0;
+  p.no_split_state = (onehot_kernel || input_first) ? 1 : 0;
   pa.d = d;
   for (int t = 0; t < num_tables; ++t) {
     pa.packed[t] = (uint32_t)table_meta[t].dim | ((uint32_t)row_class[t] << 17);
@@ -536,6 +541,7 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
       plan->sticky_status |= status[0] & kStatusBadId;
       PlanArgs full = plan->args;
       full.p.lazy_partition = 0;
+      full.p.no_split_state = 0;
       e = launch_plan(full, plan->stream);
       if (e != hipSuccess) return hip_fail(e, "plan launch");
       e = hipStreamSynchronize(plan->stream);

@@ -89,7 +89,10 @@ struct PlanParams {
   int32_t nblk;       // tiles of slabs * kScanThreads bags (at least 1)
   int32_t slabs;      // bags per thread: 1, 2, 4, ..., kPlanMaxSlabs
   int32_t c_shift;    // log2(C) when C is a power of two, else -1
-  int32_t lazy_partition;  // skip the wave partition when no bag is longer than kDirectMaxItems items
+  int32_t lazy_partition;  // skip the bag prefixes and the wave partition when no bag is longer than
+                           // kDirectMaxItems items (the lookup kernel does not read them)
+  int32_t no_split_state;  // skip the reset of the per-wave split-bag state (the lookup kernel never
+                           // splits a bag between waves)
   int64_t B;
   int64_t TB;
   int64_t total_ids;

@@ -310,7 +310,8 @@ __device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk, int64_t nbl
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
-  for (int64_t w = blk * kScanThreads + tid; w < p.waves_req; w += nblocks * kScanThreads) {
+  const int64_t reset = p.no_split_state ? 0 : p.waves_req;
+  for (int64_t w = blk * kScanThreads + tid; w < reset; w += nblocks * kScanThreads) {
     d.head_first[w] = -1;
     d.split_pieces[w] = 0;
     d.split_last[w] = -1;
@@ -841,6 +842,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     d.status[0] = bad ? kStatusBadOffsets : 0;
     d.status[1] = 0;   // every bag is one item
   }
+  if (p.lazy_partition) return;   // the lookup reads neither the prefixes nor the partition
   const int64_t first = (int64_t)blockIdx.x * kScanThreads + tid, stride = (int64_t)gridDim.x * kScanThreads;
   const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
   for (int64_t l = first; l <= TB; l += stride) {
