@@ -108,8 +108,8 @@ struct dpi_plan_s {
   int32_t uniform_class;   // shared row class of every field, or -1
   int32_t direct_jlog;     // small batches looked up bag by bag: log2 of bags per wave, or -1
   int32_t sticky_status;   // status bits latched by lookups before a re-plan
-  bool partitioned;        // a lazy plan has been recomputed with its partition
-  PlanArgs args;           // the planning launch (re-run with the partition on export)
+  bool partitioned;        // a lazy plan has been planned again in full
+  PlanArgs args;           // the planning launch (re-run in full on export)
   hipStream_t stream;
   char* ws;
   Layout layout;

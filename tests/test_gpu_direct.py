@@ -209,3 +209,29 @@ def test_bag_limit_both_sides(B):
     got = dpi.dpi_plan_export(plan)
     W = dpi.dpi_default_waves(4, B, len(ids))
     assert_plan_equals_oracle(got, dims, dtypes, 1, offs, B, len(ids), W)
+
+
+@pytest.mark.parametrize("onehot", [False, True])
+def test_lazy_plan_of_input_first_and_onehot_exports_in_full(onehot):
+    # plans whose lookup kernel reads no partition: exported arrays still equal the oracle's
+    rng = np.random.default_rng(31 + onehot)
+    B, dims, dtypes = 300, [16, 16, 16], [0, 0, 0]
+    lengths = np.ones((3, B), np.int64) if onehot else rng.integers(0, 50, size=(3, B))
+    offs_np = G.offsets_from_lengths(lengths)
+    total = int(lengths.sum())
+    tabs = [torch.from_numpy((rng.standard_normal((40, 16)) * 0.01).astype(np.float32)).cuda() for _ in dims]
+    ids = torch.from_numpy(rng.integers(0, 40, total).astype(np.int32)).cuda()
+    offs = None if onehot else torch.from_numpy(offs_np).cuda()
+    for flags in (0, dpi.DPI_FLAG_INPUT_FIRST):
+        fl = FusedLookup(tabs, flags=flags)
+        plan = fl.plan(offs, B, total, num_waves=97)
+        out1 = fl.lookup(plan, ids, offs)
+        got = dpi.dpi_plan_export(plan)
+        ref = oracle.plan(dims, dtypes, 0, None if onehot else offs_np, B, total, 32, 64, 97, flags)
+        for k in PLAN_KEYS:
+            assert np.array_equal(got[k], ref[k]), (flags, k)
+        out2 = fl.lookup(plan, ids, offs)
+        assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_OK
+        assert torch.equal(out1, out2)
+        check([t.cpu().numpy() for t in tabs], ids.cpu().numpy(), None if onehot else offs_np, None, B, out1,
+              exact=onehot)
