@@ -107,6 +107,7 @@ struct dpi_plan_s {
   bool onehot;
   int32_t uniform_class;   // shared row class of every field, or -1
   int32_t direct_jlog;     // small batches looked up bag by bag: log2 of bags per wave, or -1
+  int32_t direct_jcap_log; // ... log2 of the most bags a wave of any field takes
   int32_t sticky_status;   // status bits latched by lookups before a re-plan
   bool partitioned;        // a lazy plan has been planned again in full
   PlanArgs args;           // the planning launch (re-run in full on export)
@@ -119,11 +120,13 @@ struct dpi_plan_s {
 // Small batches (at most kDirectMaxBags bags, every field on the 16-byte row
 // path) are looked up bag by bag when the caller left the wave count to the
 // library: a wave takes J = 2^jlog bags of one field, each pooled by G/J row
-// slots, where G = 64 / (row bytes / 16) is the field's slot count.  J is the
-// same for every field (at most the smallest G), chosen so that an average bag
-// needs about one group of 8 rows per slot, then doubled while the grid holds
-// more than kDefaultWavesPerCU waves per compute unit, and no larger than the
-// batch.
+// slots, where G = 64 / (row bytes / 16) is the field's slot count.  J (at
+// most the smallest G) is chosen so that an average bag needs about one group
+// of 8 rows per slot, then doubled while the grid holds more than
+// kDefaultWavesPerCU waves per compute unit, and no larger than the batch.
+// Every field gets the waves this J needs; when that grid is several times
+// what the GPU holds, fields with more slots take more bags per wave at the
+// same slots per bag (dpi_plan sets the cap) and leave their last waves idle.
 // Returns jlog, or -1 for the plan's partition (also the choice for one-hot
 // batches of one row class, which have their own kernel, and for the
 // input-first allocation).
@@ -299,6 +302,19 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   plan->uniform_class = uniform_class;
   plan->direct_jlog = direct_jlog(num_tables, batch, total_ids, row_class, offsets == nullptr, uniform_class,
                                   o.flags, opts && opts->num_waves != 0);
+  plan->direct_jcap_log = plan->direct_jlog;
+  if (plan->direct_jlog >= 0) {
+    // a grid of several times the waves the GPU holds: fields with more slots
+    // than the smallest take more bags per wave (up to the batch size), so
+    // fewer, fuller waves amortise their prologues; below that, spreading the
+    // bags over more waves is faster
+    const int64_t wpf = (batch + (1 << plan->direct_jlog) - 1) >> plan->direct_jlog;
+    if ((int64_t)num_tables * wpf > 4 * (int64_t)kDefaultWavesPerCU * device_cus()) {
+      int jcap_log = 0;
+      while (jcap_log < 6 && ((int64_t)2 << jcap_log) <= batch) ++jcap_log;
+      plan->direct_jcap_log = std::max(jcap_log, plan->direct_jlog);
+    }
+  }
   plan->stream = reinterpret_cast<hipStream_t>(stream);
   plan->ws = reinterpret_cast<char*>(workspace);
   plan->layout = L;
@@ -410,8 +426,18 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   // max(1, ceil(L / C)) <= ceil(total_ids / C) + T * B: launch no more
   a.grid_waves = std::min<int64_t>(plan->waves_req,
                                    (plan->total_ids + plan->C - 1) / plan->C + (int64_t)plan->T * plan->B);
-  a.direct_jlog = plan->direct_jlog;
-  a.direct_wpf = plan->direct_jlog >= 0 ? (plan->B + (1 << plan->direct_jlog) - 1) >> plan->direct_jlog : 0;
+  a.direct_plog = -1;
+  if (plan->direct_jlog >= 0) {
+    // J = 2^direct_jlog bags per wave in the field with the fewest slots
+    // (gmin), i.e. P = gmin / J slots per bag; a field with more slots takes
+    // more bags per wave at the same P, up to the batch size
+    int glog_min = 6;
+    for (int t = 0; t < plan->T; ++t) glog_min = std::min(glog_min, 6 - ((plan->row_class[t] >> kTiLprShift) & 7));
+    a.direct_plog = glog_min - plan->direct_jlog;
+    a.direct_jcap_log = plan->direct_jcap_log;
+    a.direct_wpf = (plan->B + (1 << plan->direct_jlog) - 1) >> plan->direct_jlog;
+    for (int t = 0; t < plan->T; ++t) a.lpr_log[t] = (uint8_t)((plan->row_class[t] >> kTiLprShift) & 7);
+  }
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lookup launch");
   return DPI_OK;

@@ -138,8 +138,14 @@ struct LookupArgs {
   int32_t input_first;     // one lane per bag instead of the plan's waves
   int32_t onehot;          // no offsets: every bag holds one id
   int64_t grid_waves;
-  int32_t direct_jlog;     // small batches: log2 of the bags a wave takes, or -1 (the plan's partition)
-  int64_t direct_wpf;      // ... and the waves per field, ceil(B / 2^direct_jlog)
+  // bag by bag (direct_plog >= 0; -1: the plan's partition): field t's waves
+  // take J_t = min(G_t >> direct_plog, 2^direct_jcap_log) bags each, G_t = 64
+  // >> lpr_log[t] slots per wave; every field has direct_wpf waves (enough for
+  // the field with the fewest slots; the others leave their last ones idle)
+  int32_t direct_plog;
+  int32_t direct_jcap_log;
+  int64_t direct_wpf;
+  uint8_t lpr_log[DPI_MAX_TABLES];
 };
 
 // Second-order FM term over a [B, row_stride] block of T fields of dim D.

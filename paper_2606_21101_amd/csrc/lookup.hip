@@ -860,9 +860,8 @@ __device__ __forceinline__ int direct_bags(KA a, const TableInfo& ti, int64_t t,
 }
 
 template <typename TOUT>
-__device__ __forceinline__ int direct_wave(KA a, const TableInfo& ti, int64_t t, int64_t b0, DirectOffsets o,
-                                           int lane) {
-  const int jlog = a->direct_jlog;
+__device__ __forceinline__ int direct_wave(KA a, const TableInfo& ti, int64_t t, int64_t b0, int jlog,
+                                           DirectOffsets o, int lane) {
   const bool buf = use_buffer(ti), f16 = (ti.flags & kTiF16) != 0;
   switch ((ti.flags >> kTiLprShift) & 7) {
 #define DPI_CASE(L, LPR)                                                                          \
@@ -891,11 +890,13 @@ void lookup_direct_kernel(const LookupArgs args) {
   // requested before the first of them is needed (one round trip, not three)
   const int32_t st_err = a->status[0], st_long = a->status[1];
   const int64_t wpf = a->direct_wpf;
-  const bool mine = w < wpf * a->T;
-  const int64_t t = mine ? uni(w / wpf) : 0;
-  const int64_t b0 = (w - t * wpf) << a->direct_jlog;
+  const int64_t t = w < wpf * a->T ? uni(w / wpf) : 0;
+  // this field's bags per wave (its slot count from the kernel arguments)
+  const int jlog = min(6 - (int)a->lpr_log[t] - a->direct_plog, a->direct_jcap_log);
+  const int64_t b0 = (w - t * wpf) << jlog;
+  const bool mine = w < wpf * a->T && b0 < a->B;
   DirectOffsets o{0, 0};
-  if (mine && lane < (1 << a->direct_jlog)) {
+  if (mine && lane < (1 << jlog)) {
     const int64_t bl = min(b0 + lane, a->B - 1);   // bags past the batch end are inactive
     if (a->offsets) {
       const int32_t* src = a->offsets + t * (a->B + 1) + bl;
@@ -913,7 +914,7 @@ void lookup_direct_kernel(const LookupArgs args) {
     return;
   }
   if (!mine) return;
-  const int bad = direct_wave<TOUT>(a, ti, t, b0, o, lane);
+  const int bad = direct_wave<TOUT>(a, ti, t, b0, jlog, o, lane);
   if (__any(bad) && lane == 0)
     __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -1050,7 +1051,7 @@ hipError_t launch_lookup(const LookupArgs& a, hipStream_t s) {
     }
     return hipGetLastError();
   }
-  if (a.direct_jlog >= 0) {
+  if (a.direct_plog >= 0) {
     // enough waves for either mode: bag groups, or the plan's waves
     const int64_t waves = std::max<int64_t>(a.direct_wpf * a.T, a.grid_waves);
     const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
