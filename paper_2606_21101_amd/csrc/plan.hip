@@ -539,9 +539,6 @@ __device__ __forceinline__ void resolve_candidates(const BoundaryOut& o, const T
   __builtin_amdgcn_wave_barrier();
 }
 
-// SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
-// its sums come straight from the block instead of from plan_reduce, and
-// setup_bad carries plan_setup_block's verdict.
 template <int V>
 constexpr int scan_chunk() { return V < kPlanChunk ? V : kPlanChunk; }
 
@@ -556,6 +553,10 @@ __device__ __forceinline__ void plan_scan_prologue(PA pa, int64_t blk, FieldByte
   }
 }
 
+// SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
+// its sums come straight from the block instead of from plan_reduce, and
+// setup_bad carries plan_setup_block's verdict.  s_f and raw come from
+// plan_scan_prologue.
 template <int V, bool SINGLE>
 __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_bad, FieldBytes& s_f,
                                                 SlabRaw<scan_chunk<V>()>& raw) {
