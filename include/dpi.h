@@ -309,13 +309,15 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan);
  * bag_item_base[T*B+1], bag_cost_base[T*B+1], wave_item_begin[W+1] with W =
  * header16[3].  header16 = [abi, T, B, W, C, K, out_dtype, flags, total_dim,
  * items N, total cost S, total_ids, split bags, requested waves, 0, 0].
- * When dpi_lookup will not read the partition (a batch pooled bag by bag,
- * a one-hot batch of one row class, the input-first allocation), the
- * planning launch leaves out the bag prefixes and the wave partition unless
- * some bag is longer than 4 items; the first export of such a plan
- * then plans the batch again in full, on the plan's stream, from the offsets
- * given to dpi_plan -- they must still hold the batch, and no lookup of this
- * plan may be in flight on another stream.
+ * The planning launch writes what lookups read: the per-bag prefixes
+ * (bag_item_base, bag_cost_base) are left out -- a lookup needs only the
+ * first item of each wave's first bag -- and so is the wave partition when
+ * dpi_lookup will not read it (a batch pooled bag by bag, a one-hot batch of
+ * one row class, the input-first allocation) unless some bag is longer than
+ * 4 items.  The first export of a plan therefore plans the batch again in
+ * full, on the plan's stream, from the offsets given to dpi_plan -- they must
+ * still hold the batch, and no lookup of this plan may be in flight on
+ * another stream.
  */
 dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
                            int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);

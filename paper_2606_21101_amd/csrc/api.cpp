@@ -33,7 +33,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 constexpr int64_t kSmallBagsPerWave = 8;   // default-wave rule for small batches
 
 struct Layout {
-  size_t hdr, status, tinfo, col_base, id_base, block_sum, bib, bcb, wib, wave_bag, head_first, split_pieces,
+  size_t hdr, status, tinfo, col_base, id_base, block_sum, bib, bcb, wib, wave_bag, wbase, head_first, split_pieces,
       split_last, tickets, partial, total;
 };
 
@@ -57,6 +57,7 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
   L.bcb = take((TB + 1) * sizeof(int64_t));
   L.wib = take((waves_req + 1) * sizeof(int64_t));
   L.wave_bag = take((waves_req + 1) * sizeof(int64_t));
+  L.wbase = take((waves_req + 1) * sizeof(int64_t));
   L.head_first = take(waves_req * sizeof(int32_t));
   L.split_pieces = take(waves_req * sizeof(int32_t));
   L.split_last = take(waves_req * sizeof(int32_t));
@@ -332,6 +333,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   d.bcb = reinterpret_cast<int64_t*>(ws + L.bcb);
   d.wib = reinterpret_cast<int64_t*>(ws + L.wib);
   d.wave_bag = reinterpret_cast<int64_t*>(ws + L.wave_bag);
+  d.wbase = reinterpret_cast<int64_t*>(ws + L.wbase);
   d.head_first = reinterpret_cast<int32_t*>(ws + L.head_first);
   d.split_pieces = reinterpret_cast<int32_t*>(ws + L.split_pieces);
   d.split_last = reinterpret_cast<int32_t*>(ws + L.split_last);
@@ -361,6 +363,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   const bool input_first = (o.flags & DPI_FLAG_INPUT_FIRST) != 0;
   p.lazy_partition = (plan->direct_jlog >= 0 || onehot_kernel || input_first) ? 1 : 0;
   p.no_split_state = (onehot_kernel || input_first) ? 1 : 0;
+  p.prefixes = 0;   // lookups read only the bases of the waves' first bags
   pa.d = d;
   for (int t = 0; t < num_tables; ++t) {
     pa.packed[t] = (uint32_t)table_meta[t].dim | ((uint32_t)row_class[t] << 17);
@@ -404,9 +407,9 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   a.hdr = reinterpret_cast<const int64_t*>(ws + L.hdr);
   a.status = reinterpret_cast<int32_t*>(ws + L.status);
   a.tinfo = reinterpret_cast<const TableInfo*>(ws + L.tinfo);
-  a.bib = reinterpret_cast<const int64_t*>(ws + L.bib);
   a.wib = reinterpret_cast<const int64_t*>(ws + L.wib);
   a.wave_bag = reinterpret_cast<const int64_t*>(ws + L.wave_bag);
+  a.wbase = reinterpret_cast<const int64_t*>(ws + L.wbase);
   a.head_first = reinterpret_cast<const int32_t*>(ws + L.head_first);
   a.split_pieces = reinterpret_cast<const int32_t*>(ws + L.split_pieces);
   a.split_last = reinterpret_cast<const int32_t*>(ws + L.split_last);
@@ -556,23 +559,23 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
   hipError_t e = hipStreamSynchronize(plan->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   const Layout& L = plan->layout;
-  if (plan->args.p.lazy_partition && !plan->partitioned) {
-    // the planning launch skipped the bag prefixes and the partition if no
-    // bag was long: plan again in full (from the offsets given to dpi_plan),
-    // keeping the status bits earlier lookups latched
-    int32_t status[2] = {0, 0};
-    e = hipMemcpy(status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
+  if (!plan->partitioned) {
+    // the planning launch wrote no per-bag prefixes (and, for a lookup that
+    // reads no partition, no partition unless a bag was long): plan again in
+    // full from the offsets given to dpi_plan, keeping the status bits
+    // earlier lookups latched
+    int32_t status = 0;
+    e = hipMemcpy(&status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
-    if (status[1] == 0) {
-      plan->sticky_status |= status[0] & kStatusBadId;
-      PlanArgs full = plan->args;
-      full.p.lazy_partition = 0;
-      full.p.no_split_state = 0;
-      e = launch_plan(full, plan->stream);
-      if (e != hipSuccess) return hip_fail(e, "plan launch");
-      e = hipStreamSynchronize(plan->stream);
-      if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-    }
+    plan->sticky_status |= status & kStatusBadId;
+    PlanArgs full = plan->args;
+    full.p.lazy_partition = 0;
+    full.p.no_split_state = 0;
+    full.p.prefixes = 1;
+    e = launch_plan(full, plan->stream);
+    if (e != hipSuccess) return hip_fail(e, "plan launch");
+    e = hipStreamSynchronize(plan->stream);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
     plan->partitioned = true;
   }
   int64_t hdr[16];

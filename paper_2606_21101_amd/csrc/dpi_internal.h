@@ -73,6 +73,7 @@ struct PlanDev {
   int64_t* bcb;          // bag_cost_base [TB+1]
   int64_t* wib;          // wave_item_begin [Wreq+1]
   int64_t* wave_bag;     // bag holding wib[w], [Wreq+1]
+  int64_t* wbase;        // first item of bag wave_bag[w], [Wreq+1] (what a lookup needs of bib)
   int32_t* head_first;   // [Wreq] first wave of the bag this wave starts inside, or -1
   int32_t* split_pieces; // [Wreq] for the first wave of a split bag: nonempty waves covering it
   int32_t* split_last;   // [Wreq] ... and the last of them
@@ -93,6 +94,7 @@ struct PlanParams {
                            // kDirectMaxItems items (the lookup kernel does not read them)
   int32_t no_split_state;  // skip the reset of the per-wave split-bag state (the lookup kernel never
                            // splits a bag between waves)
+  int32_t prefixes;        // write the per-bag prefixes bib / bcb (read only by an export)
   int64_t B;
   int64_t TB;
   int64_t total_ids;
@@ -119,7 +121,7 @@ struct LookupArgs {
   const int64_t* hdr;
   int32_t* status;
   const TableInfo* tinfo;
-  const int64_t* bib;
+  const int64_t* wbase;
   const int64_t* wib;
   const int64_t* wave_bag;
   const int32_t* head_first;

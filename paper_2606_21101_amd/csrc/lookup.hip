@@ -667,16 +667,18 @@ __device__ __forceinline__ void wave_body(KA a) {
   const int32_t st_err = *a->status;
   const int64_t i0 = a->wib[w], i1 = a->wib[w + 1];
   const int64_t la = a->wave_bag[w], lz = a->wave_bag[w + 1];
+  const int64_t la_base = a->wbase[w], lz_base = a->wbase[w + 1];
   if (w >= W) return;
   if (st_err & kStatusBadOffsets) return;   // the plan rejected the offsets
   if (i0 >= i1) return;
   const int64_t TB = a->B * a->T;
   const int64_t C = a->C;
-  const int64_t lb = (lz < TB && a->bib[lz] < i1) ? lz : lz - 1;
-  const int64_t la_base = a->bib[la];
-  const int64_t lb_base = a->bib[lb];
+  // item i1 lies in bag lz: the wave ends inside lz (a tail piece, lz is the
+  // last bag) exactly when lz starts before i1, else its last bag is lz - 1
+  const bool tail = lz < TB && lz_base < i1;
+  const int64_t lb = tail ? lz : lz - 1;
+  const int64_t lb_base = lz_base;   // read only with tail
   const bool head = la_base < i0;
-  const bool tail = a->bib[lb + 1] > i1;
   int bad = 0;
   if (la == lb && (head || tail)) {
     const int64_t slot = head ? 2 * w : 2 * w + 1;

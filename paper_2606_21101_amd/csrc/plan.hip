@@ -474,6 +474,7 @@ struct BoundaryOut {
   int64_t* hdr;
   int64_t* wib;
   int64_t* wave_bag;
+  int64_t* wbase;
   int32_t* head_first;
   int32_t* split_pieces;
   int32_t* split_last;
@@ -509,6 +510,7 @@ __device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targe
     }
     o.wib[w] = begin;
     o.wave_bag[w] = inside ? cd.bag : cd.bag + 1;
+    o.wbase[w] = inside ? cd.ibase : cd.ibase + n;   // first item of that bag
     if (inside && w < W) {
       if (w_first < 0) w_first = w - 1;   // the wave holding the bag's first item
       o.head_first[w] = (int32_t)w_first;
@@ -654,6 +656,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     d.bcb[p.TB] = S;
     d.wib[0] = 0;
     d.wave_bag[0] = 0;
+    d.wbase[0] = 0;
     // the only writer of the status words during planning; lookups latch later
     d.status[0] = err ? kStatusBadOffsets : 0;
     d.status[1] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
@@ -672,6 +675,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     o.hdr = d.hdr;
     o.wib = d.wib;
     o.wave_bag = d.wave_bag;
+    o.wbase = d.wbase;
     o.head_first = d.head_first;
     o.split_pieces = d.split_pieces;
     o.split_last = d.split_last;
@@ -725,7 +729,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
       run_c += ac;
       const int64_t bag = tile0 + (int64_t)(c0 + k) * kScanThreads + tid;
       const bool valid = bag < p.TB;
-      if (valid) {
+      if (valid && p.prefixes) {
         d.bib[bag] = ibase;
         d.bcb[bag] = E_lo;
       }
@@ -876,6 +880,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     }
     d.wib[w] = start;
     d.wave_bag[w] = start;
+    d.wbase[w] = start;   // one item per bag
   }
 }
 
