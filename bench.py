@@ -509,9 +509,8 @@ def main():
 
         def step_on(i, k):
             bt = batches[i % len(batches)]
-            p = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, fl.opts(args.num_waves), wss[k],
-                             ws_bytes, stream=streams[k])
-            dpi.dpi_lookup(p, tables, bt.ids, bt.offsets, pool, outs[k], stream=streams[k])
+            p = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, opts, wss[k], ws_bytes, stream=streams[k])
+            dpi.dpi_lookup(p, table_ptrs, bt.ids, bt.offsets, pool_arr, outs[k], stream=streams[k])
             keep.append(p)
 
         for i in range(args.warmup):
