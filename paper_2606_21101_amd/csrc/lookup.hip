@@ -131,6 +131,38 @@ __device__ __forceinline__ void accumulate(float* acc, const raw16_t r) {
   }
 }
 
+// acc[i] / fl for the N sums of one lane, each rounded as IEEE binary32
+// division.  One correctly rounded reciprocal y = 1/fl serves the whole bag;
+// per element q = a*y, the remainder a - q*fl (exact, one fma) and the
+// corrected quotient q + r*y (one fma).  With y correctly rounded and q within
+// one ulp of a/fl, that is the correctly rounded a/fl (Markstein's correction
+// theorem) while no step leaves the normal range, which holds for
+// 2^-64 <= |a| <= FLT_MAX and fl < 2^31; a lane with an element outside that
+// range (zero, tiny, infinite, NaN) divides instead.  The three
+// instructions per element replace an eleven-instruction division.
+template <int N>
+__device__ __forceinline__ void mean_divide(float* acc, float fl) {
+  // magnitudes as unsigned integers order like the floats, NaN above infinity
+  uint32_t lo = 0xffffffffu, hi = 0;
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    const uint32_t m = __builtin_bit_cast(uint32_t, acc[i]) & 0x7fffffffu;
+    lo = min(lo, m);
+    hi = max(hi, m);
+  }
+  if (lo >= (63u << 23) && hi <= 0x7f7fffffu) {
+    const float y = 1.0f / fl;
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      const float q = acc[i] * y;
+      acc[i] = __builtin_fmaf(__builtin_fmaf(-q, fl, acc[i]), y, q);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < N; ++i) acc[i] = acc[i] / fl;
+  }
+}
+
 // Store EPL pooled values of one lane: one vector store when allowed.
 template <typename TOUT, int EPL>
 __device__ __forceinline__ void store_lane(TOUT* dst, const float* v, bool vec) {
@@ -194,6 +226,14 @@ template <> struct RowReader<true> {
   __device__ __forceinline__ raw16_t load(int32_t id) const {
     return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)((uint32_t)id * row_bytes + koff), 0, 0);
   }
+  // Row `id` when `take`, else zeros without a branch: the load goes to an
+  // offset no table of this kind reaches (its byte size is a multiple of 16
+  // below 2^32, so at most 2^32 - 16), and a raw buffer load outside the
+  // descriptor's range returns zeros and touches no memory.
+  __device__ __forceinline__ raw16_t load_if(int32_t id, bool take) const {
+    const uint32_t o = take ? (uint32_t)id * row_bytes + koff : 0xfffffff0u;
+    return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)o, 0, 0);
+  }
 };
 template <> struct RowReader<false> {
   const char* base;
@@ -202,6 +242,11 @@ template <> struct RowReader<false> {
       : base(reinterpret_cast<const char*>(table)), row_bytes((uint32_t)ti.row_bytes), koff((uint32_t)k * 16u) {}
   __device__ __forceinline__ raw16_t load(int32_t id) const {
     return *reinterpret_cast<const raw16_t*>(base + (uint64_t)(uint32_t)id * row_bytes + koff);
+  }
+  __device__ __forceinline__ raw16_t load_if(int32_t id, bool take) const {
+    raw16_t v = {0, 0, 0, 0};
+    if (take) v = load(id);
+    return v;
   }
 };
 
@@ -250,7 +295,7 @@ __device__ __forceinline__ void pool_rows_coop(KA a, const TableInfo& ti, int64_
 }
 
 // Whole bags [b_lo, b_hi) of field t, the wave pooling one bag at a time.
-template <typename TIN, typename TOUT, int LPR, bool BUF>
+template <typename TIN, typename TOUT, int LPR, bool BUF, bool LEAN>
 __device__ __forceinline__ int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
   constexpr int EPL = In<TIN>::EPL;
   a = uni(a);
@@ -270,8 +315,12 @@ __device__ __forceinline__ int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int
     pool_rows_coop<TIN, LPR, BUF>(a, ti, t, s, e, lane, acc, bad);
     if (mean && e > s) {
       const float L = (float)(e - s);
+      if constexpr (LEAN) {
+        mean_divide<EPL>(acc, L);
+      } else {
 #pragma unroll
-      for (int q = 0; q < EPL; ++q) acc[q] = acc[q] / L;
+        for (int q = 0; q < EPL; ++q) acc[q] = acc[q] / L;
+      }
     }
     if (g == 0 && col) store_lane<TOUT, EPL>(out_row<TOUT>(a, ti, b) + k * EPL, acc, vec);
   }
@@ -279,7 +328,11 @@ __device__ __forceinline__ int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int
 }
 
 // Whole bags [b_lo, b_hi) of field t.
-template <typename TIN, typename TOUT, int LPR, bool BUF>
+// LEAN (the single-row-class kernel): rows not taken read zeros through the
+// buffer range check instead of a branch per row, ids are checked once per
+// group, and mean bags divide by reciprocal and correction; the other kernels
+// keep the branch-per-row form, which holds their registers lower.
+template <typename TIN, typename TOUT, int LPR, bool BUF, bool LEAN = false>
 __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
@@ -306,7 +359,7 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
         (int64_t)(bag_offset(a, ti, t, tb0 + nb) - bag_offset(a, ti, t, tb0)) >= (int64_t)nb * G) {
       // few bags, each at least G rows long on average: the whole wave pools
       // one bag at a time (short bags are faster one per slot, in parallel)
-      bad |= pool_bags_coop<TIN, TOUT, LPR, BUF>(a, t, tb0, tb0 + nb, lane);
+      bad |= pool_bags_coop<TIN, TOUT, LPR, BUF, LEAN>(a, t, tb0, tb0 + nb, lane);
       continue;
     }
     // stage the tile's bag boundaries (wave-private LDS; LDS operations of
@@ -332,6 +385,7 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
     const int32_t r_end = off[endb];
     int32_t bstart = r;
     int32_t bend = cur < endb ? off[cur + 1] : r;
+    TOUT* optr = out_lane + (tb0 + cur) * ostride;   // output row of bag cur
     float acc[EPL];
 #pragma unroll
     for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
@@ -343,14 +397,19 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
       while (cur < endb && r >= bend) {
         const int32_t L = bend - bstart;
         if (mean && L > 0) {
-          const float fl = (float)L;
+          if constexpr (LEAN) {
+            mean_divide<EPL>(acc, (float)L);
+          } else {
+            const float fl = (float)L;
 #pragma unroll
-          for (int q = 0; q < EPL; ++q) acc[q] = acc[q] / fl;
+            for (int q = 0; q < EPL; ++q) acc[q] = acc[q] / fl;
+          }
         }
-        if (col) store_lane<TOUT, EPL>(out_lane + (tb0 + cur) * ostride, acc, vec);
+        if (col) store_lane<TOUT, EPL>(LEAN ? optr : out_lane + (tb0 + cur) * ostride, acc, vec);
 #pragma unroll
         for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
         ++cur;
+        if constexpr (LEAN) optr += ostride;
         bstart = bend;
         if (cur < endb) bend = off[cur + 1];
       }
@@ -362,11 +421,13 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
     // costs ceil(kUnroll / LPR) id loads per lane instead of kUnroll
     constexpr int IPL = (kUnroll + LPR - 1) / LPR;
     int32_t idm[IPL];
+    bool idv[IPL];   // idm[j] holds an id of this slot's run
     auto fetch_ids = [&](int32_t p) {
 #pragma unroll
       for (int j = 0; j < IPL; ++j) {
         const int q = k + j * LPR;
-        idm[j] = (q < kUnroll && p + q < r_end) ? ids[p + q] : -1;
+        idv[j] = q < kUnroll && p + q < r_end;
+        idm[j] = idv[j] ? ids[p + q] : -1;
       }
     };
     fetch_ids(r);
@@ -377,16 +438,28 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
         idn[u] = LPR == 1 ? idm[u] : __shfl(idm[u / LPR], g * LPR + u % LPR, kWaveSize);
-      const int32_t ge = min(r + kUnroll, bend);
+      // every id of the run passes through some lane's idm (a group reads
+      // from its first row on), so checking the fetched ids once per group
+      // finds every id outside the table
+      const int32_t n_in = min(r + kUnroll, bend) - r;   // rows of this group
       raw16_t raw[kUnroll];
+      if constexpr (LEAN) {
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) {
-        raw[u] = raw16_t{0, 0, 0, 0};
-        const bool in_group = r + u < ge;
-        const bool ok = in_group && (uint32_t)idn[u] < nrows;
-        bad |= (in_group && !ok);
-        if (ok && col) raw[u] = rows.load(idn[u]);
+        for (int j = 0; j < IPL; ++j) bad |= idv[j] && (uint32_t)idm[j] >= nrows;
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+          raw[u] = rows.load_if(idn[u], u < n_in && (uint32_t)idn[u] < nrows && col);
+      } else {
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          raw[u] = raw16_t{0, 0, 0, 0};
+          const bool in_group = u < n_in;
+          const bool ok = in_group && (uint32_t)idn[u] < nrows;
+          bad |= (in_group && !ok);
+          if (ok && col) raw[u] = rows.load(idn[u]);
+        }
       }
+      const int32_t ge = r + n_in;
       // the next group starts at ge: prefetch its ids
       fetch_ids(ge);
 #pragma unroll
@@ -539,7 +612,7 @@ __device__ __forceinline__ void finish_piece(KA a, int64_t w_first, int64_t bag,
 template <typename TIN, typename TOUT, int LPR>
 struct Uniform {
   static __device__ __forceinline__ int segment(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
-    return pool_segment_fast<TIN, TOUT, LPR, true>(a, t, b_lo, b_hi, lane);
+    return pool_segment_fast<TIN, TOUT, LPR, true, true>(a, t, b_lo, b_hi, lane);
   }
   static __device__ __forceinline__ int partial(KA a, int64_t t, int64_t b, int64_t lo, int64_t hi, int64_t slot,
                                                 int lane) {
