@@ -13,8 +13,9 @@
  * multi-hot fields are delimited by offsets (last paragraph of §IV-B).
  * Pooling, empty bags and accumulation precision are not defined by the
  * paper; this library's reading: per-field sum or mean, an empty bag yields
- * zeros, accumulation in fp32 for fp32 and fp16 tables, one round-to-
- * nearest-even conversion to the output dtype.
+ * zeros, accumulation in fp32 for fp32 and fp16 tables, a mean equal to the
+ * correctly rounded fp32 quotient of that sum and the bag length, one
+ * round-to-nearest-even conversion to the output dtype.
  *
  * Memory and streams
  *   - The caller owns every device buffer (tables, ids, offsets, out,
