@@ -211,3 +211,47 @@ def test_rows_beyond_2gib_of_a_table():
         check_outputs(out.double().cpu().numpy(), ref, mag, dtype == torch.float16, False)
         del big
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dim,dtype", [(4, torch.float32), (128, torch.float16)])
+def test_largest_buffer_table_masked_rows_read_zeros(dim, dtype):
+    """A table of the largest size read through a buffer descriptor (2^32 - 16
+    bytes of 16-byte rows; 2^32 - 256 bytes of 256-byte rows), pooled by the
+    single-row-class kernel with bags of 3 ids, so that most row slots of a
+    group are masked and loaded at the offset past the range.  The row right
+    after the table (same allocation, outside the table's range) holds a
+    marker that would show in every output if such a load returned data."""
+    rb = dim * (4 if dtype == torch.float32 else 2)
+    rows = (2 ** 32 - 16) // rb if rb == 16 else (2 ** 32) // rb - 1
+    assert rows * rb <= 2 ** 32 - 16
+    rng = np.random.default_rng(31)
+    store = torch.empty((rows + 1, dim), dtype=dtype, device="cuda")
+    store[rows] = 1000.0                                   # marker past the table
+    n_set = 3000
+    hi = torch.arange(rows - n_set, rows, device="cuda")
+    lo = torch.arange(0, n_set, device="cuda")
+    vals_hi = torch.from_numpy(rng.integers(-64, 64, size=(n_set, dim)) / 64.0).to(dtype).cuda()
+    vals_lo = torch.from_numpy(rng.integers(-64, 64, size=(n_set, dim)) / 64.0).to(dtype).cuda()
+    store[hi] = vals_hi
+    store[lo] = vals_lo
+    table = store[:rows]
+    B, L = 2000, 3
+    ids_np = np.concatenate([rng.integers(rows - n_set, rows, size=L * B // 2),
+                             rng.integers(0, n_set, size=L * B - L * B // 2)]).astype(np.int32)
+    rng.shuffle(ids_np)
+    ids = torch.from_numpy(ids_np).cuda()
+    offs_np = np.arange(0, L * B + 1, L, dtype=np.int32).reshape(1, -1)
+    offs = torch.from_numpy(offs_np).cuda()
+    fl = FusedLookup([table], [0], torch.float32)
+    plan = fl.plan(offs, B, len(ids_np), num_waves=64)   # the partition: single-row-class kernel
+    out = fl.lookup(plan, ids, offs)
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_OK
+    small = np.zeros((2 * n_set, dim), np.float32)
+    small[:n_set] = vals_lo.float().cpu().numpy()
+    small[n_set:] = vals_hi.float().cpu().numpy()
+    remap = np.where(ids_np >= rows - n_set, ids_np - (rows - n_set) + n_set, ids_np).astype(np.int32)
+    ref, mag = oracle.lookup([dim], [small.astype(np.float16 if dtype == torch.float16 else np.float32)],
+                             remap, offs_np, [0], B)
+    check_outputs(out.double().cpu().numpy(), ref, mag, dtype == torch.float16, False)
+    del store, table
+    torch.cuda.empty_cache()
