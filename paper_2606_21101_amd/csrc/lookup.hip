@@ -426,7 +426,7 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
 #pragma unroll
       for (int j = 0; j < IPL; ++j) {
         const int q = k + j * LPR;
-        idv[j] = q < kUnroll && p + q < r_end;
+        idv[j] = q < kUnroll && (uint32_t)p + q < (uint32_t)r_end;
         idm[j] = idv[j] ? ids[p + q] : -1;
       }
     };
@@ -441,7 +441,9 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
       // every id of the run passes through some lane's idm (a group reads
       // from its first row on), so checking the fetched ids once per group
       // finds every id outside the table
-      const int32_t n_in = min(r + kUnroll, bend) - r;   // rows of this group
+      // rows of this group; positions are below 2^31, so unsigned sums of a
+      // position and at most kUnroll cannot overflow
+      const int32_t n_in = (int32_t)(min((uint32_t)r + kUnroll, (uint32_t)bend) - (uint32_t)r);
       raw16_t raw[kUnroll];
       if constexpr (LEAN) {
 #pragma unroll
@@ -472,8 +474,8 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
 #pragma unroll
         for (int j = 0; j < IPL; ++j) {
           const int q = k + j * LPR;
-          idv[j] = ge + q < r_end;
-          idm[j] = ids[min(ge + q, r_end - 1)];
+          idv[j] = (uint32_t)ge + q < (uint32_t)r_end;
+          idm[j] = ids[min((uint32_t)ge + q, (uint32_t)r_end - 1u)];
         }
       } else {
         fetch_ids(ge);
