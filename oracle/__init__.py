@@ -34,6 +34,8 @@ def _load(path: Optional[str] = None):
                                     ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                     ctypes.c_uint32, p, p, p, p, p, p]
         lib.oracle_plan.restype = ctypes.c_int
+        lib.oracle_plan_waves.argtypes = [ctypes.c_int64, p, ctypes.c_int64, p, p, p, p, p, p]
+        lib.oracle_plan_waves.restype = ctypes.c_int
         lib.oracle_fm_second_order.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int64,
                                                ctypes.c_int32, p, p, p]
         lib.oracle_fm_second_order.restype = ctypes.c_int
@@ -100,8 +102,31 @@ def plan(dims: Sequence[int], dtypes: Sequence[int], out_dtype: int, offsets: Op
     if st != OK:
         raise OracleError(st)
     W = int(hdr[3])
-    return {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib,
-            "bag_cost_base": bcb, "wave_item_begin": wib[: W + 1]}
+    wib = np.ascontiguousarray(wib[: W + 1])
+    res = {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib,
+           "bag_cost_base": bcb, "wave_item_begin": wib}
+    res.update(plan_waves(bib, wib, lib_path=lib_path))
+    return res
+
+
+def plan_waves(bag_item_base: np.ndarray, wave_item_begin: np.ndarray, lib_path: Optional[str] = None):
+    """The per-wave arrays a lookup reads of a plan (closed forms of the wave starts
+    and the bags' first items): wave_bag, wave_bag_base [W+1]; head_first,
+    split_pieces, split_last [W] (int32)."""
+    lib = _load(lib_path)
+    bib = np.ascontiguousarray(bag_item_base, dtype=np.int64)
+    wib = np.ascontiguousarray(wave_item_begin, dtype=np.int64)
+    TB, W = len(bib) - 1, len(wib) - 1
+    wb = np.zeros(W + 1, np.int64)
+    wbb = np.zeros(W + 1, np.int64)
+    hf = np.zeros(max(W, 1), np.int32)
+    sp = np.zeros(max(W, 1), np.int32)
+    sl = np.zeros(max(W, 1), np.int32)
+    st = lib.oracle_plan_waves(TB, _ptr(bib), W, _ptr(wib), _ptr(wb), _ptr(wbb), _ptr(hf), _ptr(sp), _ptr(sl))
+    if st != OK:
+        raise OracleError(st)
+    return {"wave_bag": wb, "wave_bag_base": wbb, "head_first": hf[:W], "split_pieces": sp[:W],
+            "split_last": sl[:W]}
 
 
 def fm_second_order(emb: np.ndarray, num_fields: int, dim: int, with_mag: bool = True,

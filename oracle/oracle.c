@@ -284,6 +284,64 @@ int oracle_plan(int32_t num_tables, int64_t batch, const int32_t* dims, const in
 }
 
 /* ---------------------------------------------------------------------------------- */
+/* What a wave of the lookup reads of the plan besides its item range.  Closed forms   */
+/* of wave_item_begin (i_w) and bag_item_base (first item of each bag), following the  */
+/* partition's definition above:                                                      */
+/*  - wave_bag[w]: the bag that holds item i_w (T*B when i_w = N); wave_bag_base[w]:   */
+/*    that bag's first item (N for T*B).                                              */
+/*  - An inner boundary w (0 < w < W, i_w < N) lies strictly inside its bag when      */
+/*    i_w > wave_bag_base[w].  The bag is then cut between waves; the wave holding its */
+/*    first item is v = the largest v < w with i_v <= wave_bag_base[w], and           */
+/*    head_first[w] = v.                                                              */
+/*  - For such a v: split_last[v] = the largest inner boundary inside that bag (the   */
+/*    wave holding the bag's last items), split_pieces[v] = the number of waves u in  */
+/*    [v, split_last[v]] whose item range [i_u, i_{u+1}) is not empty.                */
+/*  - Every other entry: head_first = -1, split_pieces = 0, split_last = -1.          */
+/* ---------------------------------------------------------------------------------- */
+int oracle_plan_waves(int64_t num_bags, const int64_t* bag_item_base, int64_t num_waves,
+                      const int64_t* wave_item_begin, int64_t* wave_bag, int64_t* wave_bag_base,
+                      int32_t* head_first, int32_t* split_pieces, int32_t* split_last) {
+  if (num_bags < 0 || num_waves < 0 || !bag_item_base || !wave_item_begin || !wave_bag || !wave_bag_base)
+    return ORACLE_BAD_ARG;
+  if (num_waves > 0 && (!head_first || !split_pieces || !split_last)) return ORACLE_BAD_ARG;
+  const int64_t TB = num_bags, W = num_waves, N = bag_item_base[TB];
+  /* the bag of each boundary: bags are visited in order, boundaries are non-decreasing */
+  int64_t bag = 0;
+  for (int64_t w = 0; w <= W; ++w) {
+    const int64_t i = wave_item_begin[w];
+    if (i >= N) {
+      wave_bag[w] = TB;
+    } else {
+      while (bag_item_base[bag + 1] <= i) ++bag;
+      while (bag > 0 && bag_item_base[bag] > i) --bag;
+      wave_bag[w] = bag;
+    }
+    wave_bag_base[w] = bag_item_base[wave_bag[w]];
+  }
+  for (int64_t w = 0; w < W; ++w) {
+    head_first[w] = -1;
+    split_pieces[w] = 0;
+    split_last[w] = -1;
+  }
+  for (int64_t w = 1; w < W; ++w) {
+    const int64_t i = wave_item_begin[w];
+    if (i >= N || i <= wave_bag_base[w]) continue;
+    int64_t v = w - 1;
+    while (wave_item_begin[v] > wave_bag_base[w]) --v;   /* i_0 = 0 ends the search */
+    head_first[w] = (int32_t)v;
+    split_last[v] = (int32_t)w;
+  }
+  for (int64_t v = 0; v < W; ++v) {
+    if (split_last[v] < 0) continue;
+    int32_t pieces = 0;
+    for (int64_t u = v; u <= split_last[v]; ++u)
+      if (wave_item_begin[u] < wave_item_begin[u + 1]) ++pieces;
+    split_pieces[v] = pieces;
+  }
+  return ORACLE_OK;
+}
+
+/* ---------------------------------------------------------------------------------- */
 /* Second-order FM term (§IV-D: the explicit interaction of DeepFM holds the element- */
 /* wise square and reduce-sum operators fused there).  Written from the term's       */
 /* square-of-sum form; the tests check it against the pairwise dot-product form.     */

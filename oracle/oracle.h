@@ -9,9 +9,12 @@
  * index map of the paper's multi-table lookup algorithm (§IV-B, Algorithm 1)
  * for one-hot fields, by per-field embedding_bag + concatenation, and by
  * invariants.  oracle_plan is pinned by brute-force enumeration of the work
- * items and by invariants.  oracle_fm_second_order is pinned by the pairwise
- * dot-product form of the term, closed forms and a hand-typed example.  The plan's format is this library's own design
- * (the paper prints none), so no paper value pins it.
+ * items, hand-computed plans and invariants; oracle_plan_waves by hand-computed
+ * plans and by a brute-force assignment of every item to its wave.
+ * oracle_fm_second_order (value and magnitude) is pinned by the pairwise forms
+ * of the term and of its magnitude, closed forms and a hand-typed example.  The
+ * plan's format is this library's own design (the paper prints none), so no
+ * paper value pins it.
  */
 #ifndef DPI_ORACLE_H
 #define DPI_ORACLE_H
@@ -65,6 +68,20 @@ int oracle_plan(int32_t num_tables, int64_t batch, const int32_t* dims, const in
                 int32_t chunk_rows, int32_t item_cost_k, int64_t waves_requested,
                 uint32_t flags, int64_t* header16, int64_t* col_base, int64_t* id_base,
                 int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);
+
+/*
+ * The per-wave arrays a lookup reads of a plan, as closed forms of wave_item_begin
+ * and bag_item_base (both from oracle_plan): for w in [0, W] the bag holding the
+ * wave's first item and that bag's first item; for w in [0, W) the split-bag
+ * bookkeeping (head_first: for a boundary strictly inside a bag, the wave holding the
+ * bag's first item; for that wave, split_last: the last wave holding items of the
+ * bag, split_pieces: the number of nonempty waves from it to split_last).  See
+ * oracle.c for the step-by-step definition.
+ *   wave_bag[W+1], wave_bag_base[W+1], head_first[W], split_pieces[W], split_last[W].
+ */
+int oracle_plan_waves(int64_t num_bags, const int64_t* bag_item_base, int64_t num_waves,
+                      const int64_t* wave_item_begin, int64_t* wave_bag, int64_t* wave_bag_base,
+                      int32_t* head_first, int32_t* split_pieces, int32_t* split_last);
 
 /* bit of `flags`: boundaries are never moved to a bag end */
 #define ORACLE_FLAG_EXACT_SPLIT (1u << 1)

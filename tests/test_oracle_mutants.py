@@ -14,6 +14,7 @@ from oracle.build import HERE, build
 import test_fm_oracle as FP
 import test_oracle_pins as LP
 import test_plan_oracle as PP
+import test_sched_oracle as SP
 
 MUTANTS = {
     "mean_divisor": ("o[c] /= (double)len;", "o[c] /= (double)(len + 1);"),
@@ -43,6 +44,29 @@ MUTANTS = {
     "fm_field_stride": ("b * row_stride + (int64_t)t * dim + c", "b * row_stride + (int64_t)t + c"),
     "fm_sample_stride": ("b * row_stride + (int64_t)t * dim + c", "b * num_fields * dim + (int64_t)t * dim + c"),
     "fm_abs_sum": ("s += e;", "s += fabs(e);"),
+    "fm_mag_signed": ("sa += fabs(e);", "sa += e;"),
+    "fm_mag_no_half": ("if (mag) mag[b] = 0.5 * m;", "if (mag) mag[b] = m;"),
+    "fm_mag_minus_squares": ("m += sa * sa + q;", "m += sa * sa - q;"),
+    "fm_mag_no_squares": ("m += sa * sa + q;", "m += sa * sa;"),
+    "waves_head_first_previous": ("head_first[w] = (int32_t)v;", "head_first[w] = (int32_t)(w - 1);"),
+    "waves_pieces_count_empty": ("if (wave_item_begin[u] < wave_item_begin[u + 1]) ++pieces;", "++pieces;"),
+    "waves_inside_at_bag_start": ("if (i >= N || i <= wave_bag_base[w]) continue;",
+                                  "if (i >= N || i < wave_bag_base[w]) continue;"),
+    "waves_base_of_next_bag": ("wave_bag_base[w] = bag_item_base[wave_bag[w]];",
+                               "wave_bag_base[w] = bag_item_base[wave_bag[w] + (wave_bag[w] < TB)];"),
+    "waves_split_last_first": ("split_last[v] = (int32_t)w;", "if (split_last[v] < 0) split_last[v] = (int32_t)w;"),
+}
+
+# Mistakes planted in the oracle's Python interaction head (dcn_forward's magnitudes).
+PY_MUTANTS = {
+    "dcn_mag_signed_weights": ("ax = ax0 * (ax @ np.abs(W).T + np.abs(b)) + ax",
+                               "ax = ax0 * (ax @ W.T + np.abs(b)) + ax"),
+    "dcn_mag_no_bias": ("ax = ax0 * (ax @ np.abs(W).T + np.abs(b)) + ax", "ax = ax0 * (ax @ np.abs(W).T) + ax"),
+    "dcn_mag_signed_x0": ("ax = ax0 * (ax @ np.abs(W).T + np.abs(b)) + ax",
+                          "ax = x0 * (ax @ np.abs(W).T + np.abs(b)) + ax"),
+    "mlp_mag_signed_bias": ("ah = ah @ np.abs(V).T + np.abs(c)", "ah = ah @ np.abs(V).T + c"),
+    "mlp_mag_from_cross": ("h, ah = x0.copy(), ax0.copy()", "h, ah = x0.copy(), ax.copy()"),
+    "mag_scaled": ("return x, h, ax, ah", "return x, h, 0.5 * ax, ah"),
 }
 
 
@@ -60,6 +84,10 @@ def _pins():
     for seed in range(8):
         yield (lambda s: (lambda: PP.test_random_small_plans(s)))(seed)
     yield FP.test_golden_fm
+    yield FP.test_golden_fm_magnitude
+    yield lambda: FP.test_magnitude_equals_pairwise_form(3, 5, np.float32)
+    yield FP.test_magnitude_closed_forms
+    yield PP.test_wave_arrays_brute_force
     yield lambda: FP.test_equals_pairwise_dot_products(3, 5, np.float32)
     yield lambda: FP.test_equals_pairwise_dot_products(7, 16, np.float16)
     yield FP.test_closed_forms
@@ -92,4 +120,37 @@ def test_unmutated_copy_passes(tmp_path, monkeypatch):
     lib = build(source=str(path), out=str(tmp_path / "liboracle_copy.so"))
     monkeypatch.setattr(oracle, "LIB", lib)
     for pin in _pins():
+        pin()
+
+
+def _py_pins():
+    yield SP.test_dcn_magnitude_hand_typed
+    yield SP.test_dcn_magnitude_identity_on_nonnegative_inputs
+    yield SP.test_dcn_magnitude_sign_invariance_and_bound
+
+
+@pytest.mark.parametrize("name", sorted(PY_MUTANTS))
+def test_python_mutant_is_caught(name, monkeypatch):
+    """The oracle's dcn_forward with one planted mistake (its source edited and
+    compiled into a function that replaces it for this test only)."""
+    import inspect
+    import textwrap
+    old, new = PY_MUTANTS[name]
+    src = textwrap.dedent(inspect.getsource(oracle.dcn_forward))
+    assert src.count(old) >= 1, f"mutation anchor for {name} not found"
+    ns = dict(vars(oracle))
+    exec(compile(src.replace(old, new, 1), f"<mutant {name}>", "exec"), ns)
+    monkeypatch.setattr(oracle, "dcn_forward", ns["dcn_forward"])
+    caught = False
+    for pin in _py_pins():
+        try:
+            pin()
+        except AssertionError:
+            caught = True
+            break
+    assert caught, f"no pin catches mutant {name}"
+
+
+def test_python_pins_pass_unmutated():
+    for pin in _py_pins():
         pin()

@@ -13,7 +13,8 @@ def test_golden_plan(name):
     c = load_plan(name)
     p = oracle.plan(list(c["dims"]), c["dtypes"], c["out_dtype"], c["offsets"], c["batch"], c["total_ids"],
                     c["chunk_rows"], c["item_cost"], c["waves"], c["flags"])
-    for key in ("header", "col_base", "id_base", "bag_item_base", "bag_cost_base", "wave_item_begin"):
+    for key in ("header", "col_base", "id_base", "bag_item_base", "bag_cost_base", "wave_item_begin",
+                "wave_bag", "wave_bag_base", "head_first", "split_pieces", "split_last"):
         assert np.array_equal(p[key], c[key]), key
 
 
@@ -118,3 +119,53 @@ def test_bad_offsets_rejected():
 def test_empty_batch_plan():
     p = oracle.plan([4], [0], 0, np.zeros((1, 1), np.int32), 0, 0, 32, 64, 8)
     assert p["header"][3] == 0 and p["header"][9] == 0 and list(p["wave_item_begin"]) == [0]
+
+
+def waves_from_items(bib, wib):
+    """The per-wave arrays by brute force: every item is assigned to the wave whose
+    range holds it, and every bag to the set of waves holding its items.  A bag held
+    by several waves is split: its first wave records the last one and how many
+    waves hold items of it, and every boundary after the first wave up to the last
+    one starts inside the bag and points back to the first wave."""
+    bib = [int(x) for x in bib]
+    wib = [int(x) for x in wib]
+    TB, W, N = len(bib) - 1, len(wib) - 1, bib[-1]
+    item_bag = []
+    for bag in range(TB):
+        item_bag += [bag] * (bib[bag + 1] - bib[bag])
+    item_wave = []
+    for i in range(N):
+        item_wave.append(next(w for w in range(W) if wib[w] <= i < wib[w + 1]))
+    wave_bag = [item_bag[wib[w]] if wib[w] < N else TB for w in range(W + 1)]
+    wave_bag_base = [bib[b] for b in wave_bag]
+    hf, sp, sl = [-1] * W, [0] * W, [-1] * W
+    for bag in range(TB):
+        held = sorted({item_wave[i] for i in range(bib[bag], bib[bag + 1])})
+        if len(held) > 1:
+            first, last = held[0], held[-1]
+            sp[first], sl[first] = len(held), last
+            for w in range(first + 1, last + 1):
+                hf[w] = first
+    return {"wave_bag": wave_bag, "wave_bag_base": wave_bag_base, "head_first": hf, "split_pieces": sp,
+            "split_last": sl}
+
+
+def test_wave_arrays_brute_force():
+    """The oracle's per-wave arrays (closed forms of the wave starts) against the
+    item-by-item assignment, on random small plans of every kind: snapped and
+    exact boundaries, empty waves (W close to or above N), one-row chunks."""
+    rng = np.random.default_rng(23)
+    checked = 0
+    for _ in range(300):
+        T, B, dims, dtypes, lengths = _rand_plan_case(rng)
+        offs = G.offsets_from_lengths(lengths) if B else np.zeros((T, 1), np.int32)
+        total = int(lengths.sum())
+        C, K = int(rng.choice([1, 2, 5, 32])), int(rng.choice([1, 7, 64]))
+        Wr = int(rng.choice([1, 2, 3, 9, 40, 400]))
+        flags = int(rng.choice([0, 2]))
+        p = oracle.plan(dims, dtypes, int(rng.integers(0, 2)), offs, B, total, C, K, Wr, flags)
+        ref = waves_from_items(p["bag_item_base"], p["wave_item_begin"])
+        for k, v in ref.items():
+            assert list(p[k]) == v, (k, list(p[k]), v)
+        checked += int(np.count_nonzero(p["split_pieces"]))
+    assert checked > 100     # many split bags were exercised
