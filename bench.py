@@ -359,6 +359,11 @@ def main():
     ap.add_argument("--num-waves", type=int, default=0)
     ap.add_argument("--cpu-samples", type=int, default=6144)
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads for cpu_baseline (0: all cores)")
+    ap.add_argument("--cpu-samples-1t", type=int, default=1024,
+                    help="samples of the single-thread oracle leg of cpu_baseline")
+    ap.add_argument("--second-config", type=int, default=None,
+                    help="also measure this workload in the same run (default: the multi-hot workload when the "
+                         "large one is the headline); 0: none")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
     ap.add_argument("--flush-mib", type=int, default=1024)
@@ -425,7 +430,114 @@ def main():
         print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4, "launches": 3}))
         return
 
+    if args.second_config is None:
+        args.second_config = 3 if args.config == 4 else 0
     cfg = configs.get(args.config, batch=args.batch, out_dtype=args.out_dtype, dim=args.dim)
+    m = measure(cfg, args, dev, steps=args.steps, warmup=args.warmup, fm=args.fm, inflight=args.inflight)
+    roof = roofline(m["alg_mean"], m["look_mean_ms"], read_profile(cfg.key)["traffic"])
+    roof_cold = None if m["cold"] is None else roofline(m["alg_mean"], m["cold"]["mean_lookup_ms"], None)
+    prof = read_profile(cfg.key)
+    hdr = m["header"]
+
+    line = {
+        "metric": "pooled embedding rows/s",
+        "value": m["value"],
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup, "warm_seconds": args.warm_seconds,
+        "ms_per_step": m["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded generator; stands in for Criteo-scale CTR fields)",
+        "config": {
+            "workload": f"config {cfg.key} " + WORKLOAD_TEXT[cfg.key]
+                        + (f" [B={cfg.batch}]" if args.batch else "") + (f" [D={args.dim}]" if args.dim else ""),
+            "global_batch": cfg.batch,
+            "fields": cfg.num_tables,
+            "table_dtype": cfg.dtype,
+            "out_dtype": cfg.out_dtype,
+            "id_mapping": args.mapping,
+            "plan_flags": args.flags,
+            "allocation": "input-first" if args.flags & 8 else "output-first",
+            "rotating_batches": m["rotations"],
+            "waves": int(hdr[3]),
+            "items": int(hdr[9]),
+            "split_bags": int(hdr[12]),
+            "parallelism": "single GPU",
+        },
+        "p50_lookup_ms": m["p50_lookup_ms"],
+        "p90_lookup_ms": m["p90_lookup_ms"],
+        "p50_plan_ms": m["p50_plan_ms"],
+        "p50_step_ms": m["p50_step_ms"],
+        "wall_ms_per_step": m["wall_ms_per_step"],
+        "pooled_ids_per_batch": m["nnz_mean"],
+        "algorithmic_bytes_per_batch": m["alg_mean"],
+        "gathered_bytes_per_batch": m["gathered_mean"],
+        "hbm_gbs": roof["achieved"],
+        "hbm_frac": roof["frac"],
+        "gathered_gbs": m["gathered_mean"] / (m["look_mean_ms"] / 1e3) / 1e9,
+        "roofline": roof,
+        "roofline_cold": roof_cold,
+        "l2_hit_rate": prof["l2_hit_rate"],
+        "cold": m["cold"],
+        "fm_second_order": m["fm"],
+        "inflight": m["inflight"],
+        "setup_s": m["setup_s"],
+        "kernel_source_hash": kernel_source_hash(),
+    }
+    if args.second_config and not args.batch and not args.dim and not args.flags and not args.num_waves:
+        # the other workload of the bandwidth target, measured in the same run
+        cfg2 = configs.get(args.second_config, out_dtype=args.out_dtype)
+        del m
+        torch.cuda.empty_cache()
+        m2 = measure(cfg2, args, dev, steps=max(args.steps, 50), warmup=args.warmup)
+        prof2 = read_profile(cfg2.key)
+        line[f"config{cfg2.key}"] = {
+            "workload": f"config {cfg2.key} " + WORKLOAD_TEXT[cfg2.key],
+            "steps": max(args.steps, 50),
+            "value": m2["value"], "unit": "rows/s", "ms_per_step": m2["ms_per_step"],
+            "p50_lookup_ms": m2["p50_lookup_ms"], "p90_lookup_ms": m2["p90_lookup_ms"],
+            "p50_plan_ms": m2["p50_plan_ms"], "p50_step_ms": m2["p50_step_ms"],
+            "cold": m2["cold"],
+            "pooled_ids_per_batch": m2["nnz_mean"],
+            "algorithmic_bytes_per_batch": m2["alg_mean"],
+            "waves": int(m2["header"][3]), "split_bags": int(m2["header"][12]),
+            "roofline": roofline(m2["alg_mean"], m2["look_mean_ms"], prof2["traffic"]),
+            "roofline_cold": None if m2["cold"] is None else
+            roofline(m2["alg_mean"], m2["cold"]["mean_lookup_ms"], None),
+            "l2_hit_rate": prof2["l2_hit_rate"],
+        }
+    if not args.no_cpu_baseline:
+        cb = cpu_baseline(cfg, args.cpu_samples, args.cpu_threads)
+        one = cpu_baseline(cfg, args.cpu_samples_1t, 1)
+        cb["single_thread"] = {"value": one["value"], "unit": one["unit"], "cores": 1, "sample": one["sample"]}
+        line["cpu_baseline"] = cb
+    print(json.dumps(line), flush=True)
+
+
+def roofline(alg_bytes: float, mean_ms: float, traffic) -> dict:
+    """HBM roofline of the lookup kernel: algorithmic bytes per launch over its
+    mean duration, against the 8 TB/s peak."""
+    achieved = alg_bytes / (mean_ms / 1e3) / 1e9
+    return {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "mean_lookup_ms": mean_ms}
+
+
+def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight: int = 1) -> dict:
+    """Tables and R rotating batches of one workload resident on the device, then
+    untimed clock-ramp steps, warm-up steps, the timed warm series (HIP events on
+    the launch stream around each dpi_plan and dpi_lookup), optional series (FM
+    epilogue, batches in flight) and the cold series."""
+    import numpy as np
+    import torch
+
+    from paper_2606_21101_amd import dpi
+    from paper_2606_21101_amd.lookup import FusedLookup
+    from synth import configs, generate as G
+
     t_setup = time.perf_counter()
     tables = [G.make_table(cfg, t, dev) for t in range(cfg.num_tables)]
     batches = G.make_batches(cfg, range(args.rotations), dev, mapping=args.mapping)
@@ -484,24 +596,25 @@ def main():
         if i % 8 == 0:
             torch.cuda.synchronize()
     torch.cuda.synchronize()
-    for i in range(args.warmup):
+    for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
     plans = []
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        plans.append(step(args.warmup + i, evs[i]))
+    for i in range(steps):
+        plans.append(step(warmup + i, evs[i]))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
-    inflight = None
-    if args.inflight > 1:
+    hdr = dpi.dpi_plan_export(plans[-1])["header"]   # before later steps plan into the same workspace
+    inflight_res = None
+    if inflight > 1:
         # steps dealt round-robin to `inflight` streams, each with its own
         # workspace and output; one batch's plan overlaps another's lookup
-        n = args.inflight
+        n = inflight
         streams = [torch.cuda.Stream() for _ in range(n)]
         wss = [torch.empty(ws_bytes, dtype=torch.uint8, device=dev) for _ in range(n)]
         outs = [torch.empty_like(out) for _ in range(n)]
@@ -513,15 +626,15 @@ def main():
             dpi.dpi_lookup(p, table_ptrs, bt.ids, bt.offsets, pool_arr, outs[k], stream=streams[k])
             keep.append(p)
 
-        for i in range(args.warmup):
+        for i in range(warmup):
             step_on(i, i % n)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for st in streams:
             st.wait_stream(stream)
-        for i in range(args.steps):
-            step_on(args.warmup + i, i % n)
+        for i in range(steps):
+            step_on(warmup + i, i % n)
         for st in streams:
             stream.wait_stream(st)
         e1.record(stream)
@@ -530,29 +643,29 @@ def main():
         for p in keep[-n:]:
             if dpi.dpi_plan_sync_status(p) != dpi.DPI_OK:
                 raise SystemExit("device reported an error in the in-flight series")
-        inflight = {"batches_in_flight": n, "ms_per_step": span / args.steps,
-                    "value": sum(nnz_list[(args.warmup + i) % len(batches)] for i in range(args.steps)) / (span / 1e3)}
+        inflight_res = {"batches_in_flight": n, "ms_per_step": span / steps,
+                        "value": sum(nnz_list[(warmup + i) % len(batches)] for i in range(steps)) / (span / 1e3)}
         del keep
-    fm = None
-    if args.fm:
+    fm_res = None
+    if fm:
         dims = {cfg.dim(t) for t in range(cfg.num_tables)}
         if len(dims) != 1:
             raise SystemExit("--fm needs fields of one dim")
         D = dims.pop()
         y = torch.empty(cfg.batch, dtype=torch.float32, device=dev)
         odt = dpi.DPI_F16 if out_dt == torch.float16 else dpi.DPI_F32
-        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps + args.warmup)]
-        for i in range(args.steps + args.warmup):
+        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps + warmup)]
+        for i in range(steps + warmup):
             fev[i][0].record(stream)
             dpi.dpi_fm_second_order(out, odt, cfg.batch, cfg.num_tables, D, total_d, y, stream=stream)
             fev[i][1].record(stream)
         torch.cuda.synchronize()
-        fm_ms = np.array([e[0].elapsed_time(e[1]) for e in fev[args.warmup:]])
+        fm_ms = np.array([e[0].elapsed_time(e[1]) for e in fev[warmup:]])
         fm_bytes = cfg.batch * total_d * osize + 4 * cfg.batch
         fm_gbs = fm_bytes / (float(fm_ms.mean()) / 1e3) / 1e9
-        fm = {"kernel": "fm_kernel", "p50_ms": float(np.median(fm_ms)), "bytes_per_launch": fm_bytes,
-              "roofline": {"bound": "hbm", "achieved": fm_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                           "frac": fm_gbs / HBM_PEAK_GBS}}
+        fm_res = {"kernel": "fm_kernel", "p50_ms": float(np.median(fm_ms)), "bytes_per_launch": fm_bytes,
+                  "roofline": {"bound": "hbm", "achieved": fm_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                               "frac": fm_gbs / HBM_PEAK_GBS}}
     cold = None
     if args.cold_steps > 0:
         # cold series: the L2s and the 256 MB Infinity Cache are overwritten
@@ -561,84 +674,43 @@ def main():
         cev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.cold_steps)]
         for i in range(args.cold_steps):
             flush.fill_(i & 0xFF)
-            step(args.warmup + args.steps + i, cev[i])
+            step(warmup + steps + i, cev[i])
         torch.cuda.synchronize()
         del flush
+        c_look = np.array([e[1].elapsed_time(e[2]) for e in cev])
+        c_alg = float(np.mean([alg_bytes[(warmup + steps + i) % len(batches)] for i in range(args.cold_steps)]))
         cold = {"steps": args.cold_steps, "flush_bytes": args.flush_mib << 20,
-                "p50_lookup_ms": float(np.median([e[1].elapsed_time(e[2]) for e in cev])),
-                "p50_plan_ms": float(np.median([e[0].elapsed_time(e[1]) for e in cev]))}
-    plan_ms = np.array([evs[i][0].elapsed_time(evs[i][1]) for i in range(args.steps)])
-    look_ms = np.array([evs[i][1].elapsed_time(evs[i][2]) for i in range(args.steps)])
+                "p50_lookup_ms": float(np.median(c_look)), "mean_lookup_ms": float(c_look.mean()),
+                "p50_plan_ms": float(np.median([e[0].elapsed_time(e[1]) for e in cev])),
+                "algorithmic_bytes_per_batch": c_alg}
+    plan_ms = np.array([evs[i][0].elapsed_time(evs[i][1]) for i in range(steps)])
+    look_ms = np.array([evs[i][1].elapsed_time(evs[i][2]) for i in range(steps)])
     span_ms = evs[0][0].elapsed_time(evs[-1][2])
-    rot = [(args.warmup + i) % len(batches) for i in range(args.steps)]
+    rot = [(warmup + i) % len(batches) for i in range(steps)]
     steps_nnz = sum(nnz_list[r] for r in rot)
     steps_alg = np.array([alg_bytes[r] for r in rot], dtype=np.float64)
     steps_gath = np.array([gathered[r] for r in rot], dtype=np.float64)
-    ms_per_step = span_ms / args.steps
-    value = steps_nnz / (span_ms / 1e3)
-    look_mean_s = float(look_ms.mean()) / 1e3
-    achieved = float(steps_alg.mean()) / look_mean_s / 1e9
-    hdr = dpi.dpi_plan_export(plans[-1])["header"]
-    prof = read_profile(cfg.key)
-
-    line = {
-        "metric": "pooled embedding rows/s",
-        "value": value,
-        "unit": "rows/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup, "warm_seconds": args.warm_seconds,
-        "ms_per_step": ms_per_step,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic (seeded generator; stands in for Criteo-scale CTR fields)",
-        "config": {
-            "workload": f"config {cfg.key} " + WORKLOAD_TEXT[cfg.key]
-                        + (f" [B={cfg.batch}]" if args.batch else "") + (f" [D={args.dim}]" if args.dim else ""),
-            "global_batch": cfg.batch,
-            "fields": cfg.num_tables,
-            "table_dtype": cfg.dtype,
-            "out_dtype": cfg.out_dtype,
-            "id_mapping": args.mapping,
-            "plan_flags": args.flags,
-            "allocation": "input-first" if args.flags & dpi.DPI_FLAG_INPUT_FIRST else "output-first",
-            "rotating_batches": len(batches),
-            "waves": int(hdr[3]),
-            "items": int(hdr[9]),
-            "split_bags": int(hdr[12]),
-            "parallelism": "single GPU",
-        },
+    res = {
+        "value": steps_nnz / (span_ms / 1e3),
+        "ms_per_step": span_ms / steps,
         "p50_lookup_ms": float(np.median(look_ms)),
         "p90_lookup_ms": float(np.percentile(look_ms, 90)),
+        "look_mean_ms": float(look_ms.mean()),
         "p50_plan_ms": float(np.median(plan_ms)),
         "p50_step_ms": float(np.median(plan_ms + look_ms)),
-        "wall_ms_per_step": wall * 1e3 / args.steps,
-        "pooled_ids_per_batch": float(np.mean(nnz_list)),
-        "algorithmic_bytes_per_batch": float(np.mean(alg_bytes)),
-        "gathered_bytes_per_batch": float(np.mean(gathered)),
-        "hbm_gbs": achieved,
-        "hbm_frac": achieved / HBM_PEAK_GBS,
-        "gathered_gbs": float(steps_gath.mean()) / look_mean_s / 1e9,
-        "roofline": {
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBS,
-            "traffic": prof["traffic"],
-        },
-        "l2_hit_rate": prof["l2_hit_rate"],
+        "wall_ms_per_step": wall * 1e3 / steps,
+        "nnz_mean": float(np.mean(nnz_list)),
+        "alg_mean": float(steps_alg.mean()),
+        "gathered_mean": float(steps_gath.mean()),
+        "rotations": len(batches),
+        "header": hdr,
         "cold": cold,
-        "fm_second_order": fm,
-        "inflight": inflight,
+        "fm": fm_res,
+        "inflight": inflight_res,
         "setup_s": setup_s,
-        "kernel_source_hash": kernel_source_hash(),
     }
-    if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_samples, args.cpu_threads)
-    print(json.dumps(line), flush=True)
+    del plans, tables, batches, out, ws
+    return res
 
 
 if __name__ == "__main__":

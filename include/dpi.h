@@ -323,6 +323,29 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan);
 dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
                            int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);
 
+/*
+ * Copy what a lookup reads of the plan besides the wave starts (synchronizes
+ * the plan's stream; plans again in full on the first export, as
+ * dpi_plan_export does).  With W = header16[3] of dpi_plan_export:
+ *   wave_bag[W+1]      bag (t*B + b) holding wave w's first item (T*B at the end);
+ *   wave_bag_base[W+1] that bag's first item;
+ *   head_first[W]      for a wave that starts strictly inside a bag, the wave
+ *                      holding the bag's first item, else -1;
+ *   split_pieces[W]    for that first wave, the number of nonempty waves holding
+ *                      items of the bag, else 0;
+ *   split_last[W]      ... and the last of them, else -1.
+ * These follow from wave_item_begin and bag_item_base (§IV-C: the work is
+ * spread over threads after the whole workload is known).  *source receives 1
+ * when the arrays (and dpi_plan_export's wave_item_begin) are the ones the
+ * planning launch wrote, copied before the first re-plan -- the arrays a
+ * lookup of this plan reads -- and 0 when the planning launch wrote no
+ * partition (the plan's lookup reads none: a batch pooled bag by bag without a
+ * long bag, a one-hot batch of one row class, the input-first allocation) and
+ * the export's re-plan computed them.  Any pointer may be NULL.
+ */
+dpi_status dpi_plan_export_waves(dpi_plan_t plan, int64_t* wave_bag, int64_t* wave_bag_base, int32_t* head_first,
+                                 int32_t* split_pieces, int32_t* split_last, int32_t* source);
+
 /* Free the host object (not the workspace).  NULL is ignored. */
 void dpi_plan_destroy(dpi_plan_t plan);
 

@@ -3,10 +3,12 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <vector>
 
 #include "dpi_internal.h"
 
@@ -37,7 +39,9 @@ struct Layout {
       split_last, tickets, partial, total;
 };
 
-Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
+// prefixes: room for the per-bag prefixes, which only an export writes (the
+// no-allocation entry point never exports, and leaves them out)
+Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax, bool prefixes = true) {
   Layout L{};
   const int64_t TB = T * B;
   const int64_t nblk = plan_tiles(TB);
@@ -48,13 +52,13 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax) {
     return at;
   };
   L.hdr = take(16 * sizeof(int64_t));
-  L.status = take(2 * sizeof(int32_t));
+  L.status = take(2 * sizeof(int32_t) + sizeof(int64_t));
   L.tinfo = take(T * sizeof(TableInfo));
   L.col_base = take((T + 1) * sizeof(int64_t));
   L.id_base = take((T + 1) * sizeof(int64_t));
   L.block_sum = take((3 * nblk + 3) * sizeof(int64_t));
-  L.bib = take((TB + 1) * sizeof(int64_t));
-  L.bcb = take((TB + 1) * sizeof(int64_t));
+  L.bib = take(prefixes ? (TB + 1) * sizeof(int64_t) : 0);
+  L.bcb = take(prefixes ? (TB + 1) * sizeof(int64_t) : 0);
   L.wib = take((waves_req + 1) * sizeof(int64_t));
   L.wave_bag = take((waves_req + 1) * sizeof(int64_t));
   L.wbase = take((waves_req + 1) * sizeof(int64_t));
@@ -109,8 +113,14 @@ struct dpi_plan_s {
   int32_t uniform_class;   // shared row class of every field, or -1
   int32_t direct_jlog;     // small batches looked up bag by bag: log2 of bags per wave, or -1
   int32_t direct_jcap_log; // ... log2 of the most bags a wave of any field takes
+  int64_t plan_id;         // unique in the process; the planning launch stores it in the workspace
   int32_t sticky_status;   // status bits latched by lookups before a re-plan
-  bool partitioned;        // a lazy plan has been planned again in full
+  bool partitioned;        // the plan has been planned again in full (first export)
+  // the partition as the planning launch wrote it (what lookups read), copied
+  // before the first export plans again; empty when that launch wrote none
+  bool snap_valid;
+  std::vector<int64_t> snap_wib, snap_wave_bag, snap_wbase;
+  std::vector<int32_t> snap_head_first, snap_split_pieces, snap_split_last;
   PlanArgs args;           // the planning launch (re-run in full on export)
   hipStream_t stream;
   char* ws;
@@ -214,11 +224,14 @@ size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total
   return make_layout(num_tables, batch, o.num_waves, max_dim).total;
 }
 
-dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const int32_t* offsets, int64_t batch,
-                    int64_t total_ids, const dpi_plan_opts* opts, void* workspace, size_t workspace_bytes,
-                    void* stream, dpi_plan_t* plan_out) {
-  if (!plan_out) return fail(DPI_ERR_INVALID_ARG, "plan_out is NULL");
-  *plan_out = nullptr;
+}  // extern "C"
+
+// Validate a batch, fill *plan (caller-owned storage) and enqueue the planning
+// launch into `workspace`; allocates nothing.  prefixes: the workspace has room
+// for the per-bag prefixes (plans that may be exported).
+static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, int32_t num_tables,
+                            const int32_t* offsets, int64_t batch, int64_t total_ids, const dpi_plan_opts* opts,
+                            void* workspace, size_t workspace_bytes, void* stream, bool prefixes) {
   if (!table_meta) return fail(DPI_ERR_INVALID_ARG, "table_meta is NULL");
   if (num_tables < 1 || num_tables > DPI_MAX_TABLES)
     return fail(DPI_ERR_INVALID_ARG, "num_tables %d outside [1, %d]", num_tables, DPI_MAX_TABLES);
@@ -281,14 +294,12 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
       uniform_class = -1;
   }
 
-  const Layout L = make_layout(num_tables, batch, o.num_waves, dmax);
+  const Layout L = make_layout(num_tables, batch, o.num_waves, dmax, prefixes);
   if (!workspace) return fail(DPI_ERR_INVALID_ARG, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 15) return fail(DPI_ERR_MISALIGNED, "workspace not 16-byte aligned");
   if (workspace_bytes < L.total)
     return fail(DPI_ERR_WORKSPACE_TOO_SMALL, "workspace %zu bytes, need %zu", workspace_bytes, L.total);
 
-  dpi_plan_s* plan = new (std::nothrow) dpi_plan_s{};
-  if (!plan) return fail(DPI_ERR_INVALID_ARG, "out of host memory");
   plan->T = num_tables;
   plan->B = batch;
   plan->total_ids = total_ids;
@@ -356,6 +367,9 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   p.total_ids = total_ids;
   p.waves_req = o.num_waves;
   p.total_d = total_d;
+  static std::atomic<int64_t> next_plan_id{1};
+  plan->plan_id = next_plan_id.fetch_add(1, std::memory_order_relaxed);
+  p.plan_id = plan->plan_id;
   p.offsets = offsets;
   // lookups that never read the partition: bag by bag, the one-hot kernel,
   // the input-first allocation (the latter two never split a bag either)
@@ -371,17 +385,13 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
   }
   plan->args = pa;
   const hipError_t e = launch_plan(pa, plan->stream);
-  if (e != hipSuccess) {
-    delete plan;
-    return hip_fail(e, "plan launch");
-  }
-  *plan_out = plan;
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
   return DPI_OK;
 }
 
-dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids, const int32_t* offsets,
-                      const int32_t* pooling, void* out, void* stream) {
-  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+// Enqueue the fused lookup of a plan; allocates nothing.
+static dpi_status lookup_enqueue(const dpi_plan_s* plan, const void* const* tables, const int32_t* ids,
+                                 const int32_t* offsets, const int32_t* pooling, void* out, void* stream) {
   if (!tables) return fail(DPI_ERR_INVALID_ARG, "tables is NULL");
   if ((offsets == nullptr) != plan->onehot)
     return fail(DPI_ERR_INVALID_ARG, "offsets must be NULL exactly when the plan was built without offsets");
@@ -444,6 +454,31 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lookup launch");
   return DPI_OK;
+}
+
+extern "C" {
+
+dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const int32_t* offsets, int64_t batch,
+                    int64_t total_ids, const dpi_plan_opts* opts, void* workspace, size_t workspace_bytes,
+                    void* stream, dpi_plan_t* plan_out) {
+  if (!plan_out) return fail(DPI_ERR_INVALID_ARG, "plan_out is NULL");
+  *plan_out = nullptr;
+  dpi_plan_s* plan = new (std::nothrow) dpi_plan_s{};
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "out of host memory");
+  const dpi_status st = plan_init(plan, table_meta, num_tables, offsets, batch, total_ids, opts, workspace,
+                                  workspace_bytes, stream, true);
+  if (st != DPI_OK) {
+    delete plan;
+    return st;
+  }
+  *plan_out = plan;
+  return DPI_OK;
+}
+
+dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids, const int32_t* offsets,
+                      const int32_t* pooling, void* out, void* stream) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  return lookup_enqueue(plan, tables, ids, offsets, pooling, out, stream);
 }
 
 dpi_status dpi_fm_second_order(const void* emb, int32_t emb_dtype, int64_t batch, int32_t num_fields,
@@ -553,33 +588,77 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
   return DPI_OK;
 }
 
-dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
-                           int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin) {
-  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+}  // extern "C"
+
+namespace {
+
+template <typename V>
+hipError_t copy_out(std::vector<V>& v, const char* src, int64_t count) {
+  v.resize((size_t)std::max<int64_t>(count, 0));
+  if (count <= 0) return hipSuccess;
+  return hipMemcpy(v.data(), src, (size_t)count * sizeof(V), hipMemcpyDeviceToHost);
+}
+
+// First export of a plan: keep the partition the planning launch wrote (the
+// arrays lookups read), then plan again in full -- the planning launch wrote no
+// per-bag prefixes, and for a lookup that reads no partition no partition
+// either unless a bag was long -- from the offsets given to dpi_plan, keeping
+// the status bits earlier lookups latched.
+dpi_status replan_for_export(dpi_plan_t plan) {
   hipError_t e = hipStreamSynchronize(plan->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   const Layout& L = plan->layout;
-  if (!plan->partitioned) {
-    // the planning launch wrote no per-bag prefixes (and, for a lookup that
-    // reads no partition, no partition unless a bag was long): plan again in
-    // full from the offsets given to dpi_plan, keeping the status bits
-    // earlier lookups latched
-    int32_t status = 0;
-    e = hipMemcpy(&status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
-    plan->sticky_status |= status & kStatusBadId;
-    PlanArgs full = plan->args;
-    full.p.lazy_partition = 0;
-    full.p.no_split_state = 0;
-    full.p.prefixes = 1;
-    e = launch_plan(full, plan->stream);
-    if (e != hipSuccess) return hip_fail(e, "plan launch");
-    e = hipStreamSynchronize(plan->stream);
-    if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
-    plan->partitioned = true;
+  int32_t status[4] = {0, 0, 0, 0};
+  e = hipMemcpy(status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+  int64_t holder = 0;
+  std::memcpy(&holder, status + 2, sizeof(holder));
+  if (holder != plan->plan_id)
+    return fail(DPI_ERR_INVALID_ARG, "the plan's workspace holds a later plan: export a plan before planning "
+                                     "into its workspace again");
+  if (plan->partitioned) return DPI_OK;
+  plan->sticky_status |= status[0] & kStatusBadId;
+  const bool written = !(plan->args.p.lazy_partition && status[1] == 0);
+  plan->snap_valid = false;
+  if (written && plan->B > 0) {
+    int64_t hdr[16];
+    e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy header");
+    const int64_t W = hdr[kHdrW];
+    if (W < 0 || W > plan->waves_req) return fail(DPI_ERR_HIP, "plan header holds %lld waves", (long long)W);
+    if ((e = copy_out(plan->snap_wib, plan->ws + L.wib, W + 1)) != hipSuccess ||
+        (e = copy_out(plan->snap_wave_bag, plan->ws + L.wave_bag, W + 1)) != hipSuccess ||
+        (e = copy_out(plan->snap_wbase, plan->ws + L.wbase, W + 1)) != hipSuccess ||
+        (e = copy_out(plan->snap_head_first, plan->ws + L.head_first, W)) != hipSuccess ||
+        (e = copy_out(plan->snap_split_pieces, plan->ws + L.split_pieces, W)) != hipSuccess ||
+        (e = copy_out(plan->snap_split_last, plan->ws + L.split_last, W)) != hipSuccess)
+      return hip_fail(e, "hipMemcpy partition");
+    plan->snap_valid = true;
   }
+  PlanArgs full = plan->args;
+  full.p.lazy_partition = 0;
+  full.p.no_split_state = 0;
+  full.p.prefixes = 1;
+  e = launch_plan(full, plan->stream);
+  if (e != hipSuccess) return hip_fail(e, "plan launch");
+  e = hipStreamSynchronize(plan->stream);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
+  plan->partitioned = true;
+  return DPI_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
+                           int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  dpi_status st = replan_for_export(plan);
+  if (st != DPI_OK) return st;
+  const Layout& L = plan->layout;
   int64_t hdr[16];
-  e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
+  hipError_t e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy header");
   const int64_t T = plan->T, TB = (int64_t)plan->T * plan->B, W = hdr[kHdrW];
   struct Part {
@@ -591,10 +670,53 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
                {wave_item_begin, L.wib, W + 1}};
   for (const Part& p : parts) {
     if (!p.dst) continue;
+    if (p.dst == wave_item_begin && plan->snap_valid) {
+      if ((int64_t)plan->snap_wib.size() != W + 1) return fail(DPI_ERR_HIP, "partition changed on re-plan");
+      std::memcpy(p.dst, plan->snap_wib.data(), (W + 1) * sizeof(int64_t));
+      continue;
+    }
     e = hipMemcpy(p.dst, plan->ws + p.off, p.count * sizeof(int64_t), hipMemcpyDeviceToHost);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpy plan array");
   }
   if (header16) std::memcpy(header16, hdr, sizeof(hdr));
+  return DPI_OK;
+}
+
+dpi_status dpi_plan_export_waves(dpi_plan_t plan, int64_t* wave_bag, int64_t* wave_bag_base, int32_t* head_first,
+                                 int32_t* split_pieces, int32_t* split_last, int32_t* source) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  dpi_status st = replan_for_export(plan);
+  if (st != DPI_OK) return st;
+  const Layout& L = plan->layout;
+  int64_t hdr[16];
+  hipError_t e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy header");
+  const int64_t W = hdr[kHdrW];
+  if (source) *source = plan->snap_valid ? 1 : 0;
+  if (plan->snap_valid) {
+    if ((int64_t)plan->snap_wave_bag.size() != W + 1) return fail(DPI_ERR_HIP, "partition changed on re-plan");
+    if (wave_bag) std::memcpy(wave_bag, plan->snap_wave_bag.data(), (W + 1) * sizeof(int64_t));
+    if (wave_bag_base) std::memcpy(wave_bag_base, plan->snap_wbase.data(), (W + 1) * sizeof(int64_t));
+    if (W > 0) {
+      if (head_first) std::memcpy(head_first, plan->snap_head_first.data(), W * sizeof(int32_t));
+      if (split_pieces) std::memcpy(split_pieces, plan->snap_split_pieces.data(), W * sizeof(int32_t));
+      if (split_last) std::memcpy(split_last, plan->snap_split_last.data(), W * sizeof(int32_t));
+    }
+    return DPI_OK;
+  }
+  struct Part {
+    void* dst;
+    size_t off, bytes;
+  } parts[] = {{wave_bag, L.wave_bag, (size_t)(W + 1) * sizeof(int64_t)},
+               {wave_bag_base, L.wbase, (size_t)(W + 1) * sizeof(int64_t)},
+               {head_first, L.head_first, (size_t)W * sizeof(int32_t)},
+               {split_pieces, L.split_pieces, (size_t)W * sizeof(int32_t)},
+               {split_last, L.split_last, (size_t)W * sizeof(int32_t)}};
+  for (const Part& p : parts) {
+    if (!p.dst || p.bytes == 0) continue;
+    e = hipMemcpy(p.dst, plan->ws + p.off, p.bytes, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy plan array");
+  }
   return DPI_OK;
 }
 

@@ -63,7 +63,8 @@ struct alignas(16) TableInfo {
 // Device pointers of a plan inside the caller's workspace.
 struct PlanDev {
   int64_t* hdr;          // [16]
-  int32_t* status;       // [2]: error bits; bags of more than kDirectMaxItems items
+  int32_t* status;       // [4]: error bits; bags of more than kDirectMaxItems items; then the int64
+                         // id of the plan that last planned into this workspace
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
@@ -100,6 +101,8 @@ struct PlanParams {
   int64_t total_ids;
   int64_t waves_req;
   int64_t total_d;
+  int64_t plan_id;         // written next to the status words: tells a plan whether its workspace
+                           // still holds it
   const int32_t* offsets;  // device [T][B+1] or nullptr
 };
 

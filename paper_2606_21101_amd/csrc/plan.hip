@@ -652,14 +652,17 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     h[kHdrCost] = S;
     h[kHdrTotalIds] = p.total_ids;
     h[kHdrWaveReq] = p.waves_req;
-    d.bib[p.TB] = N;
-    d.bcb[p.TB] = S;
+    if (p.prefixes) {
+      d.bib[p.TB] = N;
+      d.bcb[p.TB] = S;
+    }
     d.wib[0] = 0;
     d.wave_bag[0] = 0;
     d.wbase[0] = 0;
     // the only writer of the status words during planning; lookups latch later
     d.status[0] = err ? kStatusBadOffsets : 0;
     d.status[1] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
+    *reinterpret_cast<int64_t*>(d.status + 2) = p.plan_id;
   }
   if (p.TB == 0 || !partition) return;   // block-uniform
 
@@ -846,11 +849,12 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     h[kHdrWaveReq] = p.waves_req;
     d.status[0] = bad ? kStatusBadOffsets : 0;
     d.status[1] = 0;   // every bag is one item
+    *reinterpret_cast<int64_t*>(d.status + 2) = p.plan_id;
   }
   if (p.lazy_partition) return;   // the lookup reads neither the prefixes nor the partition
   const int64_t first = (int64_t)blockIdx.x * kScanThreads + tid, stride = (int64_t)gridDim.x * kScanThreads;
   const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
-  for (int64_t l = first; l <= TB; l += stride) {
+  for (int64_t l = first; p.prefixes && l <= TB; l += stride) {
     if (l == TB) {
       d.bib[l] = N;
       d.bcb[l] = S;

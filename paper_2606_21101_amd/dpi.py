@@ -102,6 +102,9 @@ def load() -> ctypes.CDLL:
     p64 = ctypes.POINTER(i64)
     lib.dpi_plan_export.restype = ctypes.c_int
     lib.dpi_plan_export.argtypes = [vp, p64, p64, p64, p64, p64, p64]
+    p32 = ctypes.POINTER(i32)
+    lib.dpi_plan_export_waves.restype = ctypes.c_int
+    lib.dpi_plan_export_waves.argtypes = [vp, p64, p64, p32, p32, p32, p32]
     lib.dpi_fm_second_order.restype = ctypes.c_int
     lib.dpi_fm_second_order.argtypes = [vp, i32, i64, i32, i32, i64, vp, vp]
     lib.dpi_stage_onehot.restype = ctypes.c_int
@@ -187,16 +190,28 @@ def dpi_plan_workspace_bytes(num_tables: int, batch: int, total_ids: int, max_di
 
 @dataclass
 class Plan:
-    """Handle of a device plan; keeps the borrowed buffers alive."""
+    """Handle of a device plan; keeps the borrowed buffers alive.  A workspace
+    holds one plan at a time: planning into it again supersedes the plan before,
+    which then refuses lookups and exports."""
     handle: int
     num_tables: int
     batch: int
     keep: tuple
+    workspace_ptr: int = 0
+    serial: int = 0
+
+    def check_current(self):
+        if _workspace_holder.get(self.workspace_ptr) != self.serial:
+            raise DpiError(DPI_ERR_INVALID_ARG, "plan superseded: its workspace holds a later plan")
 
     def __del__(self):
         if self.handle and _lib is not None:
             _lib.dpi_plan_destroy(ctypes.c_void_p(self.handle))
             self.handle = 0
+
+
+_workspace_holder = {}   # workspace address -> serial of the plan that last planned into it
+_plan_serial = [0]
 
 
 def dpi_plan(table_meta, offsets, batch: int, total_ids: int, opts: Optional[dpi_plan_opts], workspace,
@@ -210,7 +225,10 @@ def dpi_plan(table_meta, offsets, batch: int, total_ids: int, opts: Optional[dpi
                       ctypes.byref(opts) if opts is not None else None, _ptr(workspace), workspace_bytes,
                       _stream(stream), ctypes.byref(out))
     _check(st)
-    return Plan(out.value, T, batch, (workspace, offsets, table_meta))
+    _plan_serial[0] += 1
+    ws_ptr = _ptr(workspace) or 0
+    _workspace_holder[ws_ptr] = _plan_serial[0]
+    return Plan(out.value, T, batch, (workspace, offsets, table_meta), ws_ptr, _plan_serial[0])
 
 
 def table_array(tables) -> ctypes.Array:
@@ -226,6 +244,7 @@ def pooling_array(pooling: Sequence[int]) -> ctypes.Array:
 def dpi_lookup(plan: Plan, tables, ids, offsets, pooling: Optional[Sequence[int]], out, stream=None) -> None:
     """tables / pooling: sequences, or the arrays table_array / pooling_array built."""
     lib = load()
+    plan.check_current()
     T = plan.num_tables
     ptrs = tables if isinstance(tables, ctypes.Array) else table_array(tables)
     pool = pooling if (pooling is None or isinstance(pooling, ctypes.Array)) else pooling_array(pooling)
@@ -243,6 +262,7 @@ def dpi_plan_sync_status(plan: Plan) -> int:
 
 def dpi_plan_export(plan: Plan) -> dict:
     lib = load()
+    plan.check_current()
     hdr = np.zeros(16, dtype=np.int64)
     p64 = ctypes.POINTER(ctypes.c_int64)
     _check(lib.dpi_plan_export(ctypes.c_void_p(plan.handle), hdr.ctypes.data_as(p64), None, None, None, None, None))
@@ -257,6 +277,29 @@ def dpi_plan_export(plan: Plan) -> dict:
                                wib.ctypes.data_as(p64)))
     return {"header": hdr, "col_base": col, "id_base": idb, "bag_item_base": bib, "bag_cost_base": bcb,
             "wave_item_begin": wib}
+
+
+def dpi_plan_export_waves(plan: Plan) -> dict:
+    """What a lookup reads of the plan besides the wave starts; "source" is 1 when
+    these are the arrays the planning launch wrote (see include/dpi.h)."""
+    lib = load()
+    plan.check_current()
+    hdr = np.zeros(16, dtype=np.int64)
+    p64 = ctypes.POINTER(ctypes.c_int64)
+    p32 = ctypes.POINTER(ctypes.c_int32)
+    _check(lib.dpi_plan_export(ctypes.c_void_p(plan.handle), hdr.ctypes.data_as(p64), None, None, None, None, None))
+    W = int(hdr[3])
+    wb = np.zeros(W + 1, np.int64)
+    wbb = np.zeros(W + 1, np.int64)
+    hf = np.zeros(max(W, 1), np.int32)
+    sp = np.zeros(max(W, 1), np.int32)
+    sl = np.zeros(max(W, 1), np.int32)
+    src = ctypes.c_int32(-1)
+    _check(lib.dpi_plan_export_waves(ctypes.c_void_p(plan.handle), wb.ctypes.data_as(p64), wbb.ctypes.data_as(p64),
+                                     hf.ctypes.data_as(p32), sp.ctypes.data_as(p32), sl.ctypes.data_as(p32),
+                                     ctypes.byref(src)))
+    return {"wave_bag": wb, "wave_bag_base": wbb, "head_first": hf[:W], "split_pieces": sp[:W],
+            "split_last": sl[:W], "source": int(src.value)}
 
 
 def dpi_fm_second_order(emb, emb_dtype: int, batch: int, num_fields: int, dim: int, row_stride: int, out,

@@ -16,6 +16,11 @@ _TORCH = {dpi.DPI_F32: torch.float32, dpi.DPI_F16: torch.float16}
 
 
 class FusedLookup:
+    """The tables of a set of fields and one workspace, reused by every plan():
+    each plan supersedes the one before it (a lookup or export with an earlier
+    plan raises).  To keep several plans in flight, give each its own
+    workspace through dpi.dpi_plan."""
+
     def __init__(self, tables: Sequence[torch.Tensor], pooling: Optional[Sequence[int]] = None,
                  out_dtype: torch.dtype = torch.float32, num_rows: Optional[Sequence[int]] = None,
                  chunk_rows: int = 0, item_cost_k: int = 0, flags: int = 0):

@@ -1,8 +1,9 @@
 """Fused gather-pool on the GPU vs the CPU oracle on the five workloads.
 
-Small workloads are compared element by element in full; the 100-table
-workload is compared on sampled contiguous sample ranges (all fields) that
-the oracle recomputes from regenerated rows.
+Every workload is compared element by element in full; the 100-table
+workload streams sample blocks through the oracle over the rows the batch
+references (regenerated from the seeded generator), and is also compared on
+sampled sample ranges against per-range sub-problems.
 """
 import numpy as np
 import pytest
@@ -139,6 +140,52 @@ def test_large_sampled(large):
     cfg, tables, batch = large
     out = run_gpu(cfg, tables, batch)
     compare(cfg, out, ranges=LARGE_RANGES)
+
+
+@pytest.mark.timeout(1200)
+def test_large_full_batch(large):
+    """All 65,536 samples x 100 fields of the large workload against the oracle,
+    bag by bag.  The oracle's inputs come from the seeded generator only: the
+    batch's ids, and each field's distinct referenced rows regenerated from the
+    counter-based value generator (evaluated on the device for speed, spot-checked
+    against the same generator on the CPU); ids are renumbered into those compact
+    tables.  The output is compared in blocks of samples so the fp64 reference
+    never holds more than one block."""
+    import oracle
+    from parity import check_outputs
+    cfg, tables, batch = large
+    out = run_gpu(cfg, tables, batch)
+    T, B = cfg.num_tables, cfg.batch
+    offs = batch.offsets_host.astype(np.int64)
+    base = batch.id_base
+    dims = [cfg.dim(t) for t in range(T)]
+    pooling = pooling_codes(cfg)
+    rows_c, ids_c = [], []
+    rng = np.random.default_rng(4)
+    for t in range(T):
+        seg = batch.ids[int(base[t]):int(base[t + 1])]
+        uniq, inv = torch.unique(seg.long(), return_inverse=True)
+        rows = G.table_rows(cfg, t, uniq)                        # the generator, evaluated on the device
+        if t % 25 == 0:
+            pick = torch.from_numpy(rng.integers(0, len(uniq), size=16))
+            assert torch.equal(rows[pick.cuda()].cpu(), G.table_rows(cfg, t, uniq[pick.cuda()].cpu()))
+        rows_c.append(rows.cpu().numpy())
+        ids_c.append(inv.to(torch.int32).cpu().numpy())
+        del rows, uniq, inv
+    print(f"  large full batch: {sum(len(r) for r in rows_c)} distinct rows regenerated", flush=True)
+    chunk = 4096
+    worst = 0.0
+    for b0 in range(0, B, chunk):
+        b1 = min(B, b0 + chunk)
+        ids = np.concatenate([ids_c[t][offs[t, b0]:offs[t, b1]] for t in range(T)])
+        sub_offs = np.stack([offs[t, b0:b1 + 1] - offs[t, b0] for t in range(T)]).astype(np.int32)
+        ref, mag = oracle.lookup(dims, rows_c, ids, sub_offs, pooling, b1 - b0)
+        y = out[b0:b1].double().cpu().numpy()
+        st = check_outputs(y, ref, mag, True, True, where=f"large samples [{b0}, {b1})")
+        worst = max(worst, st["max_comp_rel"])
+        print(f"  large full batch: samples [{b0}, {b1}) within tolerance "
+              f"(max componentwise {st['max_comp_rel']:.2e})", flush=True)
+    print(f"cfg4 full batch, fp16 out: every bag within tolerance, max componentwise {worst:.2e}")
 
 
 @pytest.mark.timeout(600)

@@ -11,6 +11,16 @@ from synth import configs, generate as G
 
 pytestmark = pytest.mark.gpu
 KEYS = ("header", "col_base", "id_base", "bag_item_base", "bag_cost_base", "wave_item_begin")
+WAVE_KEYS = ("wave_bag", "wave_bag_base", "head_first", "split_pieces", "split_last")
+
+
+def check_waves(plan, ref):
+    """The per-wave arrays a lookup reads, bit for bit against the oracle's closed
+    forms; returns 1 when they are the planning launch's own arrays."""
+    got = dpi.dpi_plan_export_waves(plan)
+    for k in WAVE_KEYS:
+        assert np.array_equal(got[k], ref[k]), (k, got[k][:20], ref[k][:20])
+    return got["source"]
 
 
 def run_plan(dims, dtypes, out_dtype, rows, lengths, onehot, C=0, K=0, W=0, flags=0):
@@ -34,6 +44,7 @@ def run_plan(dims, dtypes, out_dtype, rows, lengths, onehot, C=0, K=0, W=0, flag
                       flags)
     for k in KEYS:
         assert np.array_equal(got[k], ref[k]), (k, got[k][:20], ref[k][:20])
+    got["source"] = check_waves(plan, ref)
     return got
 
 
@@ -47,7 +58,10 @@ def test_plan_parity_configs(key, batch):
     W = default_waves(cfg, int(lengths.sum()))
     got = run_plan(dims, dtypes, out_dtype, rows, lengths, cfg.all_onehot, W=W)
     print(f"cfg{key} B={cfg.batch}: W={got['header'][3]} N={got['header'][9]} S={got['header'][10]} "
-          f"split={got['header'][12]}")
+          f"split={got['header'][12]} partition from the planning launch: {got['source']}")
+    # an explicit wave count: the planning launch writes the partition (one-hot
+    # batches of one row class excepted: their lookup kernel reads none)
+    assert got["source"] == (0 if (cfg.all_onehot and len(set(dims)) == 1) else 1)
     for W2, flags in ((7, 0), (1000, dpi.DPI_FLAG_EXACT_SPLIT)):
         run_plan(dims, dtypes, out_dtype, rows, lengths, cfg.all_onehot, W=W2, flags=flags)
 
@@ -175,3 +189,66 @@ def test_bad_offsets_detected():
         fl_if.lookup(plan_if, ids, offs, out)
         torch.cuda.synchronize()
         assert torch.all(out == 7.0)
+
+
+@pytest.mark.parametrize("key", [3, 4])
+def test_lookup_reads_the_exported_partition(key):
+    """The default plan of the multi-hot and large workloads, as the planning
+    launch wrote it and a lookup then read it: wave starts and every per-wave
+    array bit for bit against the oracle, before the export plans again."""
+    cfg = configs.get(key)
+    lengths = G.bag_lengths(cfg)
+    dims, dtypes, out_dtype = plan_args(cfg)
+    offs_np = G.offsets_from_lengths(lengths)
+    total = int(lengths.sum())
+    tabs = [torch.empty((1, d), dtype=torch.float16, device="cuda") for d in dims]
+    fl = FusedLookup(tabs, None, torch.float16, num_rows=G.table_sizes(cfg))
+    plan = fl.plan(torch.from_numpy(offs_np).cuda(), cfg.batch, total)   # default wave count
+    waves = dpi.dpi_plan_export_waves(plan)
+    assert waves["source"] == 1
+    got = dpi.dpi_plan_export(plan)
+    W = int(got["header"][3])
+    assert W == default_waves(cfg, total)
+    ref = oracle.plan(dims, dtypes, out_dtype, offs_np, cfg.batch, total, 32, 64, W, 0)
+    for k in KEYS:
+        assert np.array_equal(got[k], ref[k]), k
+    for k in WAVE_KEYS:
+        assert np.array_equal(waves[k], ref[k]), k
+    print(f"cfg{key}: W={W}, split bags {int(got['header'][12])}, "
+          f"{int(np.count_nonzero(waves['head_first'] >= 0))} boundaries inside bags")
+
+
+@pytest.mark.parametrize("W", [997, 20_000])
+def test_exact_split_partition_as_written(W):
+    """EXACT_SPLIT plans of the multi-hot workload (many bags cut between waves):
+    the planning launch's own per-wave arrays against the oracle."""
+    cfg = configs.get(3)
+    lengths = G.bag_lengths(cfg)
+    dims, dtypes, out_dtype = plan_args(cfg)
+    got = run_plan(dims, dtypes, out_dtype, G.table_sizes(cfg), lengths, False, C=8, W=W,
+                   flags=dpi.DPI_FLAG_EXACT_SPLIT)
+    assert got["source"] == 1
+    assert got["header"][12] > W // 2
+
+
+def test_superseded_plan_is_refused():
+    """Planning into a workspace again supersedes the plan before: the binding
+    refuses a lookup or export with it, and so does the C ABI's export (the
+    workspace records which plan planned into it last)."""
+    import ctypes
+    tabs = [torch.zeros((10, 16), device="cuda")]
+    fl = FusedLookup(tabs)
+    offs = torch.tensor([[0, 1, 3]], dtype=torch.int32, device="cuda")
+    ids = torch.zeros(3, dtype=torch.int32, device="cuda")
+    first = fl.plan(offs, 2, 3, num_waves=4)
+    second = fl.plan(offs, 2, 3, num_waves=4)
+    with pytest.raises(dpi.DpiError):
+        fl.lookup(first, ids, offs)
+    with pytest.raises(dpi.DpiError):
+        dpi.dpi_plan_export(first)
+    hdr = np.zeros(16, np.int64)
+    st = dpi.load().dpi_plan_export(ctypes.c_void_p(first.handle),
+                                    hdr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), None, None, None, None, None)
+    assert st == dpi.DPI_ERR_INVALID_ARG and "later plan" in dpi.dpi_last_error()
+    fl.lookup(second, ids, offs)
+    assert dpi.dpi_plan_export(second)["header"][2] == 2
