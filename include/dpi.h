@@ -299,6 +299,36 @@ dpi_status dpi_dcn_forward(dpi_dcn_t head, const float* x0, float* out_cross, fl
                            void* stream_explicit, void* stream_implicit, void* after, uint64_t* marks);
 void dpi_dcn_destroy(dpi_dcn_t head);
 
+/*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: dpi_plan
+ * followed by dpi_lookup in one call, with the plan's workspace taken from a
+ * fixed device array of this library (DPI_NOALLOC_SCRATCH_BYTES per GPU,
+ * held by each GPU the library runs on until the process ends) instead of a
+ * caller's buffer.  Calls no allocating routine, host or device.
+ *   Arguments as for dpi_plan (with opts) and dpi_lookup; `out` receives the
+ *   same values, bit for bit, as that pair with a caller workspace.
+ *   device_status: NULL, or device int32 receiving (asynchronously, after the
+ *   lookup) the call's device-detected errors: DPI_DEVSTAT_BAD_OFFSETS,
+ *   DPI_DEVSTAT_BAD_ID, 0 when none.
+ *   stream: a stream of the current device.
+ * Every call on a GPU shares that GPU's array, which keeps the last call's
+ * contents (each call resets what it reads): calls that overlap on one GPU --
+ * on different streams, or from different host threads -- race, and must be
+ * serialized by the caller.  A batch whose plan needs more than the array
+ * holds (per-wave state and split-bag partials, about 12 + 8 * max dim bytes
+ * per wave, plus 48 bytes per field and 24 bytes per tile of bags) returns
+ * DPI_ERR_WORKSPACE_TOO_SMALL and enqueues nothing; other errors as for
+ * dpi_plan and dpi_lookup.
+ */
+#define DPI_NOALLOC_SCRATCH_BYTES (64u << 20)
+#define DPI_DEVSTAT_BAD_OFFSETS 1
+#define DPI_DEVSTAT_BAD_ID 2
+dpi_status dpi_lookup_noalloc(const dpi_table_meta* table_meta, int32_t num_tables, const void* const* tables,
+                              const int32_t* ids, const int32_t* offsets, int64_t batch, int64_t total_ids,
+                              const int32_t* pooling, const dpi_plan_opts* opts, void* out, int32_t* device_status,
+                              void* stream);
+
 /* Synchronize the plan's stream and report device-detected errors
  * (BAD_OFFSETS before BAD_ID).  Lookups on other streams must be
  * synchronized by the caller first. */

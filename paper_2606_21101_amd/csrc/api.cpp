@@ -456,6 +456,42 @@ static dpi_status lookup_enqueue(const dpi_plan_s* plan, const void* const* tabl
   return DPI_OK;
 }
 
+// The no-allocation entry point's work (csrc/noalloc.hip supplies the device
+// scratch): plan into the scratch without room for per-bag prefixes, then
+// look up, then copy the status word out.  Not part of the C ABI.
+__attribute__((visibility("hidden"))) dpi_status dpi_plan_lookup_into(
+    const dpi_table_meta* table_meta, int32_t num_tables, const void* const* tables, const int32_t* ids,
+    const int32_t* offsets, int64_t batch, int64_t total_ids, const int32_t* pooling, const dpi_plan_opts* opts,
+    void* out, int32_t* device_status, void* scratch, size_t scratch_bytes, void* stream) {
+  if (!table_meta) return fail(DPI_ERR_INVALID_ARG, "table_meta is NULL");
+  if (num_tables < 1 || num_tables > DPI_MAX_TABLES)
+    return fail(DPI_ERR_INVALID_ARG, "num_tables %d outside [1, %d]", num_tables, DPI_MAX_TABLES);
+  if (device_status && (reinterpret_cast<uintptr_t>(device_status) & 3))
+    return fail(DPI_ERR_MISALIGNED, "device_status not 4-byte aligned");
+  int32_t dmax = 1;
+  for (int t = 0; t < num_tables; ++t) dmax = std::max(dmax, std::min(table_meta[t].dim, (int32_t)DPI_MAX_DIM));
+  dpi_plan_opts o;
+  if (batch >= 0 && total_ids >= 0 && resolve_opts(opts, num_tables, batch, total_ids, o) == DPI_OK) {
+    const size_t need = make_layout(num_tables, batch, o.num_waves, dmax, false).total;
+    if (need > scratch_bytes)
+      return fail(DPI_ERR_WORKSPACE_TOO_SMALL,
+                  "this batch needs %zu bytes of scratch (%lld waves), the no-allocation entry point holds %zu",
+                  need, (long long)o.num_waves, scratch_bytes);
+  }
+  dpi_plan_s plan{};
+  dpi_status st = plan_init(&plan, table_meta, num_tables, offsets, batch, total_ids, opts, scratch, scratch_bytes,
+                            stream, false);
+  if (st != DPI_OK) return st;
+  st = lookup_enqueue(&plan, tables, ids, offsets, pooling, out, stream);
+  if (st != DPI_OK) return st;
+  if (device_status) {
+    const hipError_t e = hipMemcpyAsync(device_status, plan.ws + plan.layout.status, sizeof(int32_t),
+                                        hipMemcpyDeviceToDevice, plan.stream);
+    if (e != hipSuccess) return hip_fail(e, "status copy");
+  }
+  return DPI_OK;
+}
+
 extern "C" {
 
 dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const int32_t* offsets, int64_t batch,

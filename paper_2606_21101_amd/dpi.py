@@ -40,6 +40,9 @@ DPI_SCHED_ONE_STREAM = 2
 DPI_ABI_VERSION = 1
 DPI_MAX_TABLES = 256
 DPI_MAX_DIM = 65536
+DPI_NOALLOC_SCRATCH_BYTES = 64 << 20
+DPI_DEVSTAT_BAD_OFFSETS = 1
+DPI_DEVSTAT_BAD_ID = 2
 
 
 class dpi_table_meta(ctypes.Structure):
@@ -125,6 +128,9 @@ def load() -> ctypes.CDLL:
     lib.dpi_dcn_forward.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp, vp]
     lib.dpi_dcn_destroy.restype = None
     lib.dpi_dcn_destroy.argtypes = [vp]
+    lib.dpi_lookup_noalloc.restype = ctypes.c_int
+    lib.dpi_lookup_noalloc.argtypes = [ctypes.POINTER(dpi_table_meta), i32, ctypes.POINTER(vp), vp, vp, i64, i64,
+                                       ctypes.POINTER(i32), ctypes.POINTER(dpi_plan_opts), vp, vp, vp]
     lib.dpi_plan_destroy.restype = None
     lib.dpi_plan_destroy.argtypes = [vp]
     _lib = lib
@@ -253,6 +259,23 @@ def dpi_lookup(plan: Plan, tables, ids, offsets, pooling: Optional[Sequence[int]
     st = lib.dpi_lookup(ctypes.c_void_p(plan.handle), ptrs, _ptr(ids), _ptr(offsets), pool, _ptr(out),
                         _stream(stream))
     _check(st)
+
+
+def dpi_lookup_noalloc(table_meta, tables, ids, offsets, batch: int, total_ids: int,
+                       pooling: Optional[Sequence[int]], opts: Optional[dpi_plan_opts], out, device_status=None,
+                       stream=None) -> None:
+    """dpi_plan + dpi_lookup in one call with the library's fixed device scratch as the
+    workspace (no allocation; see include/dpi.h).  tables / pooling: sequences, or the
+    arrays table_array / pooling_array built."""
+    lib = load()
+    T = len(table_meta)
+    ptrs = tables if isinstance(tables, ctypes.Array) else table_array(tables)
+    pool = pooling if (pooling is None or isinstance(pooling, ctypes.Array)) else pooling_array(pooling)
+    if len(ptrs) != T or (pool is not None and len(pool) != T):
+        raise DpiError(DPI_ERR_INVALID_ARG, "tables / pooling must have one entry per field")
+    _check(lib.dpi_lookup_noalloc(table_meta, T, ptrs, _ptr(ids), _ptr(offsets), batch, total_ids, pool,
+                                  ctypes.byref(opts) if opts is not None else None, _ptr(out), _ptr(device_status),
+                                  _stream(stream)))
 
 
 def dpi_plan_sync_status(plan: Plan) -> int:
