@@ -216,7 +216,9 @@ __device__ __forceinline__ void bag_span(KA a, const TableInfo& ti, int64_t t, i
 template <bool BUF> struct RowReader;
 template <> struct RowReader<true> {
   // raw buffer: the descriptor's record count and the per-lane offset are
-  // unsigned 32-bit byte values, so tables up to 4 GiB - 1 bytes qualify
+  // unsigned 32-bit byte values, so tables up to 4 GiB - 1 bytes qualify.
+  // (An indexed descriptor with the row bytes as stride, letting the load
+  // form id * row_bytes itself, measured 5 % slower on the multi-hot batch.)
   __amdgpu_buffer_rsrc_t rsrc;
   uint32_t row_bytes, koff;
   __device__ RowReader(const void* table, const TableInfo& ti, int k)
@@ -234,7 +236,18 @@ template <> struct RowReader<true> {
     const uint32_t o = take ? (uint32_t)id * row_bytes + koff : 0xfffffff0u;
     return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)o, 0, 0);
   }
+  // The row starting at byte `row_off` (a masked row: masked_row_offset).
+  __device__ __forceinline__ raw16_t load_at(uint32_t row_off) const {
+    return __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)(row_off + koff), 0, 0);
+  }
 };
+
+// Start of a row no buffer-read table of rows of RB bytes (a power of two)
+// reaches: such a table's byte size is a multiple of RB below 2^32, so at most
+// 2^32 - RB, and every piece of the "row" from here lies past it.
+template <int RB>
+constexpr uint32_t masked_row_offset() { return (uint32_t)(0x100000000ull - RB); }
+
 template <> struct RowReader<false> {
   const char* base;
   uint32_t row_bytes, koff;
@@ -332,7 +345,7 @@ __device__ __forceinline__ int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int
 // buffer range check instead of a branch per row, ids are checked once per
 // group, and mean bags divide by reciprocal and correction; the other kernels
 // keep the branch-per-row form, which holds their registers lower.
-template <typename TIN, typename TOUT, int LPR, bool BUF, bool LEAN = false>
+template <typename TIN, typename TOUT, int LPR, bool BUF, bool LEAN = false, int U = kUnroll>
 __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
@@ -418,42 +431,62 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
     close_bags();   // leading empty bags
     // ids of a group: lane k of a slot loads ids k, k + LPR, ... of the group
     // and the slot's lanes exchange them by cross-lane permutes, so a group
-    // costs ceil(kUnroll / LPR) id loads per lane instead of kUnroll
-    constexpr int IPL = (kUnroll + LPR - 1) / LPR;
+    // costs ceil(U / LPR) id loads per lane instead of U
+    constexpr int IPL = (U + LPR - 1) / LPR;
     int32_t idm[IPL];
     bool idv[IPL];   // idm[j] holds an id of this slot's run
     auto fetch_ids = [&](int32_t p) {
 #pragma unroll
       for (int j = 0; j < IPL; ++j) {
         const int q = k + j * LPR;
-        idv[j] = q < kUnroll && (uint32_t)p + q < (uint32_t)r_end;
+        idv[j] = q < U && (uint32_t)p + q < (uint32_t)r_end;
         idm[j] = idv[j] ? ids[p + q] : -1;
       }
     };
     fetch_ids(r);
     while (cur < endb) {
-      // one group of up to kUnroll rows of the current bag; the lanes of a
+      // one group of up to U rows of the current bag; the lanes of a
       // slot are active together, so every permute reads an active lane
-      int32_t idn[kUnroll];
-#pragma unroll
-      for (int u = 0; u < kUnroll; ++u)
-        idn[u] = LPR == 1 ? idm[u] : __shfl(idm[u / LPR], g * LPR + u % LPR, kWaveSize);
       // every id of the run passes through some lane's idm (a group reads
       // from its first row on), so checking the fetched ids once per group
       // finds every id outside the table
       // rows of this group; positions are below 2^31, so unsigned sums of a
-      // position and at most kUnroll cannot overflow
-      const int32_t n_in = (int32_t)(min((uint32_t)r + kUnroll, (uint32_t)bend) - (uint32_t)r);
-      raw16_t raw[kUnroll];
+      // position and at most U cannot overflow
+      const int32_t n_in = (int32_t)(min((uint32_t)r + U, (uint32_t)bend) - (uint32_t)r);
+      raw16_t raw[U];
       if constexpr (LEAN) {
+        static_assert(BUF, "the single-row-class kernel reads tables through buffer descriptors");
+        // A slot's lanes cover whole rows (LPR * 16 = row bytes, a power of
+        // two): each lane turns the ids it fetched into row offsets, masking
+        // the rows past the group's end and ids outside the table, and the
+        // slot exchanges offsets, so a row costs one add per lane, not a
+        // compare, a multiply and a select.
+        constexpr uint32_t RB = LPR * 16;
+        uint32_t roff[IPL];
 #pragma unroll
-        for (int j = 0; j < IPL; ++j) bad |= idv[j] && (uint32_t)idm[j] >= nrows;
+        for (int j = 0; j < IPL; ++j) {
+          const bool id_ok = (uint32_t)idm[j] < nrows;
+          bad |= idv[j] && !id_ok;
+          roff[j] = (k + j * LPR < n_in && id_ok) ? (uint32_t)idm[j] * RB : masked_row_offset<RB>();
+        }
+        uint32_t ro[U];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
-          raw[u] = rows.load_if(idn[u], u < n_in && (uint32_t)idn[u] < nrows && col);
+        for (int u = 0; u < U; ++u)
+          ro[u] = LPR == 1 ? roff[u] : (uint32_t)__shfl((int)roff[u / LPR], g * LPR + u % LPR, kWaveSize);
+#pragma unroll
+        for (int u = 0; u < U; ++u) raw[u] = rows.load_at(ro[u]);
+        // all of the group's loads leave before the first add waits for one:
+        // left to itself the scheduler moves adds between the loads, and each
+        // add's wait then holds back the loads after it (multi-hot batch:
+        // 81 -> 64 us)
+        __builtin_amdgcn_sched_barrier(0);
       } else {
+        int32_t idn[U];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < U; ++u)
+          idn[u] = LPR == 1 ? idm[u] : __shfl(idm[u / LPR], g * LPR + u % LPR, kWaveSize);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
           raw[u] = raw16_t{0, 0, 0, 0};
           const bool in_group = u < n_in;
           const bool ok = in_group && (uint32_t)idn[u] < nrows;
@@ -463,14 +496,14 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
       }
       const int32_t ge = r + n_in;
       // the next group starts at ge: prefetch its ids
-      if constexpr (LEAN && LPR <= kUnroll) {
+      if constexpr (LEAN && LPR <= U) {
         // inside the loop the run still holds a row (r < r_end), so the
         // clamped index is an id of the run and the load needs no branch;
         // with every load of the group issued unconditionally the adds wait
         // for the rows only, not for this prefetch (multi-hot batch of
         // 128-byte rows: -2 %; with 16 or more lanes per row, where lanes
         // past the group's ids load too, the large batch ran 4 % slower)
-        static_assert(IPL * LPR == kUnroll, "every lane fetches one id of the group");
+        static_assert(IPL * LPR == U, "every lane fetches one id of the group");
 #pragma unroll
         for (int j = 0; j < IPL; ++j) {
           const int q = k + j * LPR;
@@ -481,7 +514,7 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
         fetch_ids(ge);
       }
 #pragma unroll
-      for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
+      for (int u = 0; u < U; ++u) accumulate<TIN, EPL>(acc, raw[u]);
       r = ge;
       close_bags();
     }
@@ -627,10 +660,10 @@ __device__ __forceinline__ void finish_piece(KA a, int64_t w_first, int64_t bag,
 #define DPI_FOR_LPR(MACRO) \
   MACRO(0, 1) MACRO(1, 2) MACRO(2, 4) MACRO(3, 8) MACRO(4, 16) MACRO(5, 32) MACRO(6, 64)
 
-template <typename TIN, typename TOUT, int LPR>
+template <typename TIN, typename TOUT, int LPR, int U = kUnroll>
 struct Uniform {
   static __device__ __forceinline__ int segment(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
-    return pool_segment_fast<TIN, TOUT, LPR, true, true>(a, t, b_lo, b_hi, lane);
+    return pool_segment_fast<TIN, TOUT, LPR, true, true, U>(a, t, b_lo, b_hi, lane);
   }
   static __device__ __forceinline__ int partial(KA a, int64_t t, int64_t b, int64_t lo, int64_t hi, int64_t slot,
                                                 int lane) {
