@@ -56,7 +56,7 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax, bool p
   L.tinfo = take(T * sizeof(TableInfo));
   L.col_base = take((T + 1) * sizeof(int64_t));
   L.id_base = take((T + 1) * sizeof(int64_t));
-  L.block_sum = take((3 * nblk + 3) * sizeof(int64_t));
+  L.block_sum = take((10 * nblk + 3) * sizeof(int64_t));
   L.bib = take(prefixes ? (TB + 1) * sizeof(int64_t) : 0);
   L.bcb = take(prefixes ? (TB + 1) * sizeof(int64_t) : 0);
   L.wib = take((waves_req + 1) * sizeof(int64_t));
@@ -376,7 +376,6 @@ static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, 
   const bool onehot_kernel = offsets == nullptr && uniform_class >= 0 && !(o.flags & DPI_FLAG_INPUT_FIRST);
   const bool input_first = (o.flags & DPI_FLAG_INPUT_FIRST) != 0;
   p.lazy_partition = (plan->direct_jlog >= 0 || onehot_kernel || input_first) ? 1 : 0;
-  p.no_split_state = (onehot_kernel || input_first) ? 1 : 0;
   p.prefixes = 0;   // lookups read only the bases of the waves' first bags
   pa.d = d;
   for (int t = 0; t < num_tables; ++t) {
@@ -673,7 +672,6 @@ dpi_status replan_for_export(dpi_plan_t plan) {
   }
   PlanArgs full = plan->args;
   full.p.lazy_partition = 0;
-  full.p.no_split_state = 0;
   full.p.prefixes = 1;
   e = launch_plan(full, plan->stream);
   if (e != hipSuccess) return hip_fail(e, "plan launch");
@@ -696,6 +694,16 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
   int64_t hdr[16];
   hipError_t e = hipMemcpy(hdr, plan->ws + L.hdr, sizeof(hdr), hipMemcpyDeviceToHost);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpy header");
+  {
+    // split bags are counted per tile of bags
+    const int64_t nb = plan->args.p.nblk;
+    std::vector<int64_t> splits((size_t)nb);
+    e = hipMemcpy(splits.data(), plan->ws + L.block_sum + (3 * nb + 3) * sizeof(int64_t), nb * sizeof(int64_t),
+                  hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy split counts");
+    hdr[kHdrSplit] = 0;
+    for (int64_t v : splits) hdr[kHdrSplit] += v;
+  }
   const int64_t T = plan->T, TB = (int64_t)plan->T * plan->B, W = hdr[kHdrW];
   struct Part {
     int64_t* dst;

@@ -68,8 +68,9 @@ struct PlanDev {
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
-  int64_t* block_sum;    // [3 * nblk + 3]: per tile items, then costs, then malformed-offset flags; the
-                         // last three: totals (when the tiles are scanned by their own launch)
+  int64_t* block_sum;    // [10 * nblk + 3]: per tile items, then costs, then malformed-offset flags; three
+                         // totals (when the tiles are scanned by their own launch); per tile split bags;
+                         // per tile six words of published sums (one-launch planning)
   int64_t* bib;          // bag_item_base [TB+1]
   int64_t* bcb;          // bag_cost_base [TB+1]
   int64_t* wib;          // wave_item_begin [Wreq+1]
@@ -93,8 +94,6 @@ struct PlanParams {
   int32_t c_shift;    // log2(C) when C is a power of two, else -1
   int32_t lazy_partition;  // skip the bag prefixes and the wave partition when no bag is longer than
                            // kDirectMaxItems items (the lookup kernel does not read them)
-  int32_t no_split_state;  // skip the reset of the per-wave split-bag state (the lookup kernel never
-                           // splits a bag between waves)
   int32_t prefixes;        // write the per-bag prefixes bib / bcb (read only by an export)
   int64_t B;
   int64_t TB;

@@ -7,17 +7,18 @@
 // plan on the device from the per-field offsets:
 //   plan_reduce    per tile of bags: sums of item counts and costs, offset
 //                  validation; tile 0 also writes the per-field table info,
-//                  column bases and id bases; every block resets a share of
-//                  the per-wave arrays.
+//                  column bases and id bases.
 //   plan_tiles     only when the batch has more than kPlanDirectTiles tiles:
 //                  one block turns the tile sums into exclusive prefixes and
 //                  totals, so the next launch reads one entry per tile.
 //   plan_scan      per tile: its exclusive prefix, the per-bag exclusive
 //                  prefixes of items and cost, and every wave boundary that
 //                  falls in a bag's cost interval.
-// A batch of one tile runs both steps in a single block (one launch), and a
-// one-hot batch (no offsets) takes plan_onehot, which writes the closed forms
-// of the same arrays in one fully parallel launch.
+// A batch of one tile runs both steps in a single block (one launch); a batch
+// of at most kPlanDirectTiles tiles, all resident at once, runs both in one
+// launch whose blocks exchange their tile sums (plan_fused); a one-hot batch
+// (no offsets) takes plan_onehot, which writes the closed forms of the same
+// arrays in one fully parallel launch.
 //
 // A tile is V slabs of kScanThreads consecutive bags; thread i holds bag i of
 // every slab, so the offset loads and prefix stores are coalesced.  The loads
@@ -301,23 +302,16 @@ __device__ __forceinline__ void slab_cost(PA pa, const FieldBytes& f, const Slab
 }
 
 // ---------------------------------------------------------------------------
-// Launch 1: tile sums, validation, field info, wave-array reset.
+// Launch 1: tile sums, validation, field info.
 // ---------------------------------------------------------------------------
-// Duties outside the bag sums: this block's share of the per-wave reset and,
-// in block 0, the per-field info and the zeroed header.  Returns whether the
-// id counts are malformed.
-__device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk, int64_t nblocks) {
+// Duties outside the bag sums, in block 0: the per-field info.  (Nothing here
+// has to precede another block's work: the header and every per-wave entry
+// are written once, by the block that resolves them.)  Returns whether the id
+// counts are malformed.
+__device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
-  const int64_t reset = p.no_split_state ? 0 : p.waves_req;
-  for (int64_t w = blk * kScanThreads + tid; w < reset; w += nblocks * kScanThreads) {
-    d.head_first[w] = -1;
-    d.split_pieces[w] = 0;
-    d.split_last[w] = -1;
-    d.tickets[w] = 0;
-  }
-
   bool bad = false;
   if (blk == 0) {
     // per-field info: dims -> column bases, id counts -> id bases
@@ -352,18 +346,19 @@ __device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk, int64_t nbl
       d.id_base[p.T] = tot_ids;
       if (tot_ids != p.total_ids) bad = true;
     }
-    if (tid < 16) d.hdr[tid] = 0;
   }
   return bad;
 }
 
+// sums (optional): receives the tile's items, cost and malformed | long << 1
+// on every thread.
 template <int V>
-__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks) {
+__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks, int64_t* sums = nullptr) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
   constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
-  bool bad = plan_setup_block(pa, blk, nblocks);
+  bool bad = plan_setup_block(pa, blk);
 
   int64_t v[4] = {0, 0, 0, 0};   // items, cost, malformed offsets, long bags
   if (p.TB > 0) {
@@ -390,11 +385,17 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
   v[2] = bad ? 1 : 0;
   __shared__ int64_t s_red[kWavesPerBlock][4];
   block_sums<4>(v, s_red);
+  const int64_t flags = (v[2] != 0 ? 1 : 0) | (v[3] << 1);   // malformed flag, long bags above it
+  if (sums) {
+    sums[0] = v[0];
+    sums[1] = v[1];
+    sums[2] = flags;
+  }
   if (tid == 0) {
     const int64_t nb = p.nblk;
     d.block_sum[blk] = v[0];
     d.block_sum[nb + blk] = v[1];
-    d.block_sum[2 * nb + blk] = v[2] | (v[3] << 1);   // malformed flag, long bags above it
+    d.block_sum[2 * nb + blk] = flags;
   }
 }
 
@@ -471,19 +472,24 @@ struct Cand {
 
 // Plan arrays the boundary writes go to, staged in LDS.
 struct BoundaryOut {
-  int64_t* hdr;
   int64_t* wib;
   int64_t* wave_bag;
   int64_t* wbase;
   int32_t* head_first;
   int32_t* split_pieces;
   int32_t* split_last;
+  int32_t* tickets;
   int64_t C, K;
+  unsigned long long splits;   // bags of this tile cut between waves
 };
 
 // Wave boundaries whose targets fall in the cost interval (E_lo, E_hi] of a
 // bag with n items whose first item is number ibase.  Target c_w lies in it
-// exactly when floor(E_lo*W/S) < w <= floor(E_hi*W/S).
+// exactly when floor(E_lo*W/S) < w <= floor(E_hi*W/S).  Every boundary w in
+// [1, W] is resolved here by exactly one bag, which writes all of what a
+// lookup reads of it: the wave start, its bag and the bag's first item, the
+// head link of wave w, and the split entries of wave w - 1 (the wave ending
+// at it), whose arrival counter it also clears.
 // Returns whether the bag is split between waves.
 __device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targets& g, const FieldBytes& f,
                                                const Cand& cd) {
@@ -511,12 +517,19 @@ __device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targe
     o.wib[w] = begin;
     o.wave_bag[w] = inside ? cd.bag : cd.bag + 1;
     o.wbase[w] = inside ? cd.ibase : cd.ibase + n;   // first item of that bag
+    o.tickets[w - 1] = 0;
+    bool first_inside = false;
     if (inside && w < W) {
-      if (w_first < 0) w_first = w - 1;   // the wave holding the bag's first item
-      o.head_first[w] = (int32_t)w_first;
+      first_inside = w_first < 0;
+      if (first_inside) w_first = w - 1;   // the wave holding the bag's first item
       if (begin_prev >= 0 && begin_prev < begin) ++pieces;   // previous inside wave was nonempty
       begin_prev = begin;
       w_last = w;
+    }
+    if (w < W) o.head_first[w] = inside ? (int32_t)w_first : -1;
+    if (!first_inside) {   // wave w - 1 is not the first wave of a split bag
+      o.split_pieces[w - 1] = 0;
+      o.split_last[w - 1] = -1;
     }
   }
   if (w_first >= 0) {
@@ -529,14 +542,14 @@ __device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targe
 }
 
 // Lanes [0, count) of the wave each resolve one collected candidate.
-__device__ __forceinline__ void resolve_candidates(const BoundaryOut& o, const Targets& g, const FieldBytes& f,
+__device__ __forceinline__ void resolve_candidates(BoundaryOut& o, const Targets& g, const FieldBytes& f,
                                                    const Cand* list, int count, int lane) {
   // the list was written by other lanes of this wave: keep the reads after the writes
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   __builtin_amdgcn_wave_barrier();
   const bool split = lane < count && bag_boundaries(o, g, f, list[lane]);
   const uint64_t m = __ballot(split);
-  if (m != 0 && lane == 0) atomicAdd((unsigned long long*)&o.hdr[kHdrSplit], (unsigned long long)__popcll(m));
+  if (m != 0 && lane == 0) atomicAdd(&o.splits, (unsigned long long)__popcll(m));
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   __builtin_amdgcn_wave_barrier();
 }
@@ -555,6 +568,11 @@ __device__ __forceinline__ void plan_scan_prologue(PA pa, int64_t blk, FieldByte
   }
 }
 
+template <int V>
+__device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i, int64_t pre_c, int64_t N,
+                                               int64_t S, bool err, int64_t nlong, FieldBytes& s_f,
+                                               SlabRaw<scan_chunk<V>()>& raw);
+
 // SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
 // its sums come straight from the block instead of from plan_reduce, and
 // setup_bad carries plan_setup_block's verdict.  s_f and raw come from
@@ -564,11 +582,10 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
                                                 SlabRaw<scan_chunk<V>()>& raw) {
   PPR p = pa->p;
   PDR d = pa->d;
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int tid = threadIdx.x;
   const int64_t nb = p.nblk;
   const int64_t* bs = d.block_sum;
   constexpr int CH = scan_chunk<V>();
-  const int64_t tile0 = blk * (int64_t)kScanThreads * V;
 
   // this tile's exclusive prefix and the totals
   int64_t pre_i, pre_c, N, S;
@@ -629,6 +646,23 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     S = bs[3 * nb + 1];
     err = bs[3 * nb + 2] != 0;
   }
+  plan_scan_core<V>(pa, blk, pre_i, pre_c, N, S, err, nlong, s_f, raw);
+}
+
+// The scan and partition of tile blk, its exclusive prefix (pre_i items,
+// pre_c cost) and the batch's totals (N items, S cost, malformed offsets,
+// bags longer than kDirectMaxItems items) known.  Block 0 also writes the
+// header and the status words.
+template <int V>
+__device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i, int64_t pre_c, int64_t N,
+                                               int64_t S, bool err, int64_t nlong, FieldBytes& s_f,
+                                               SlabRaw<scan_chunk<V>()>& raw) {
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t nb = p.nblk;
+  constexpr int CH = scan_chunk<V>();
+  const int64_t tile0 = blk * (int64_t)kScanThreads * V;
   const int64_t W = p.waves_req < N ? p.waves_req : N;
   // a batch the lookup pools bag by bag reads only the header, the status
   // words and the field info unless it has a long bag (then the lookup falls
@@ -637,7 +671,6 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
   const bool partition = !(p.lazy_partition && nlong == 0);
 
   if (blk == 0 && tid == 0) {
-    // the split counter was zeroed by plan_reduce; other blocks add to it
     int64_t* h = d.hdr;
     h[kHdrAbi] = DPI_ABI_VERSION;
     h[kHdrT] = p.T;
@@ -652,6 +685,9 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     h[kHdrCost] = S;
     h[kHdrTotalIds] = p.total_ids;
     h[kHdrWaveReq] = p.waves_req;
+    h[kHdrSplit] = 0;   // the split bags are counted per tile (an export adds them up)
+    h[14] = 0;
+    h[15] = 0;
     if (p.prefixes) {
       d.bib[p.TB] = N;
       d.bcb[p.TB] = S;
@@ -659,12 +695,17 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     d.wib[0] = 0;
     d.wave_bag[0] = 0;
     d.wbase[0] = 0;
+    if (W > 0 && partition) d.head_first[0] = -1;   // wave 0 starts at the first bag
     // the only writer of the status words during planning; lookups latch later
     d.status[0] = err ? kStatusBadOffsets : 0;
     d.status[1] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
     *reinterpret_cast<int64_t*>(d.status + 2) = p.plan_id;
   }
-  if (p.TB == 0 || !partition) return;   // block-uniform
+  int64_t* const tile_splits = d.block_sum + 3 * nb + 3;
+  if (p.TB == 0 || !partition) {   // block-uniform
+    if (tid == 0) tile_splits[blk] = 0;
+    return;
+  }
 
   __shared__ Targets g;
   __shared__ BoundaryOut o;
@@ -675,15 +716,16 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     g.scale = W > 0 ? (double)W / (double)S : 0.0;
     g.inv_w = W > 0 ? 1.0 / (double)W : 0.0;
     g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
-    o.hdr = d.hdr;
     o.wib = d.wib;
     o.wave_bag = d.wave_bag;
     o.wbase = d.wbase;
     o.head_first = d.head_first;
     o.split_pieces = d.split_pieces;
     o.split_last = d.split_last;
+    o.tickets = d.tickets;
     o.C = p.C;
     o.K = p.K;
+    o.splits = 0;
   }
   __syncthreads();   // publishes the field bytes, g and o
   const double scale = g.scale;
@@ -763,6 +805,8 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     }
   }
   if (ncand > 0) resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
+  __syncthreads();
+  if (tid == 0) tile_splits[blk] = (int64_t)o.splits;
 }
 
 template <int V>
@@ -791,7 +835,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_single_kernel(const PlanArg
   __shared__ FieldBytes s_f;
   SlabRaw<scan_chunk<V>()> raw;
   plan_scan_prologue<V>(pa, 0, s_f, raw);   // the bags' offsets load during the setup
-  const bool bad = plan_setup_block(pa, 0, 1);
+  const bool bad = plan_setup_block(pa, 0);
   plan_scan_block<V, true>(pa, 0, bad, s_f, raw);
 }
 
@@ -810,7 +854,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
-  const bool bad = __syncthreads_or(plan_setup_block(pa, blockIdx.x, gridDim.x) ? 1 : 0) != 0;
+  const bool bad = __syncthreads_or(plan_setup_block(pa, blockIdx.x) ? 1 : 0) != 0;
 
   // per-field bag cost and the cost prefix over fields
   __shared__ int64_t s_cost[DPI_MAX_TABLES];
@@ -847,12 +891,16 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     h[kHdrCost] = S;
     h[kHdrTotalIds] = p.total_ids;
     h[kHdrWaveReq] = p.waves_req;
+    h[kHdrSplit] = 0;
+    h[14] = 0;
+    h[15] = 0;
     d.status[0] = bad ? kStatusBadOffsets : 0;
     d.status[1] = 0;   // every bag is one item
     *reinterpret_cast<int64_t*>(d.status + 2) = p.plan_id;
   }
-  if (p.lazy_partition) return;   // the lookup reads neither the prefixes nor the partition
   const int64_t first = (int64_t)blockIdx.x * kScanThreads + tid, stride = (int64_t)gridDim.x * kScanThreads;
+  for (int64_t j = first; j < p.nblk; j += stride) d.block_sum[3 * (int64_t)p.nblk + 3 + j] = 0;   // no split bags
+  if (p.lazy_partition) return;   // the lookup reads neither the prefixes nor the partition
   const double inv_b = p.B > 0 ? 1.0 / (double)p.B : 0.0;
   for (int64_t l = first; p.prefixes && l <= TB; l += stride) {
     if (l == TB) {
@@ -885,7 +933,152 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     d.wib[w] = start;
     d.wave_bag[w] = start;
     d.wbase[w] = start;   // one item per bag
+    if (w < W) {          // and never cut between waves
+      d.head_first[w] = -1;
+      d.split_pieces[w] = 0;
+      d.split_last[w] = -1;
+      d.tickets[w] = 0;
+    }
   }
+}
+
+// ---------------------------------------------------------------------------
+// One launch for batches of several tiles (at most kPlanDirectTiles, every
+// block resident): each block sums its tile and publishes the sums, then
+// gathers every tile's sums -- the partition needs the batch's total cost,
+// so a block waits for the tiles after it as well as those before -- and
+// scans and partitions its tile.  A published sum travels as two 64-bit
+// words, each holding the low 32 bits of the plan's id above 32 bits of the
+// value, stored and loaded with device-scope atomics: a word is valid exactly
+// when its id matches, so no fence (no write-back or invalidation of the
+// L2s) is needed.  The wait is bounded: a tile whose words do not appear in
+// time (its block not yet resident) is summed by the waiting thread itself
+// from the offsets, so every block finishes whatever the residency.  No block
+// relies on another block's writes other than the published sums: the header
+// and each per-wave entry have a single writer.
+// ---------------------------------------------------------------------------
+constexpr int kTileWords = 6;   // items, cost, malformed | long << 1: two words each
+constexpr int kPlanSpinLimit = 4096;   // polls of a tile's flag before summing the tile here
+
+// Sums of tile j computed by one thread: items, cost, and the malformed and
+// long-bag flags in the layout the blocks publish (malformed | long << 1).
+template <int V>
+__device__ int64_t tile_sums_serial(PA pa, const FieldBytes& f, int64_t j, int64_t& items, int64_t& cost) {
+  PPR p = pa->p;
+  const int64_t B = p.B, TB = p.TB;
+  const uint32_t C = (uint32_t)p.C;
+  const int64_t l0 = j * (int64_t)kScanThreads * V;
+  const int64_t l1 = min(TB, l0 + (int64_t)kScanThreads * V);
+  int64_t bad = 0, nlong = 0;
+  items = 0;
+  cost = 0;
+  if (j == 0) {   // the id counts, as block 0's setup checks them
+    int64_t tot = 0;
+    for (int t = 0; t < p.T; ++t) {
+      const int64_t nnz = p.offsets[(int64_t)t * (B + 1) + B];
+      bad |= nnz < 0 ? 1 : 0;
+      tot += nnz < 0 ? 0 : nnz;
+    }
+    bad |= tot != p.total_ids ? 1 : 0;
+  }
+  int64_t t = l0 / B;
+  for (int64_t l = l0; l < l1; ++l) {
+    while ((t + 1) * B <= l) ++t;
+    const int32_t lo = p.offsets[l + t], hi = p.offsets[l + t + 1];
+    const bool malformed = (l == t * B && lo != 0) || hi < lo;
+    bad |= malformed ? 1 : 0;
+    const uint32_t L = malformed ? 0u : (uint32_t)(hi - lo);
+    uint32_t n = (L + C - 1u) / C;
+    n = n < 1u ? 1u : n;
+    items += n;
+    cost += (int64_t)L * f.row[t] + f.out[t] + (int64_t)n * p.K;
+    nlong += n > (uint32_t)kDirectMaxItems ? 1 : 0;
+  }
+  return bad | (nlong << 1);
+}
+
+template <int V>
+__global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x;
+  const int64_t blk = blockIdx.x, nb = p.nblk;
+  int64_t* const flags = d.block_sum + 4 * nb + 3;
+
+  const uint64_t tag = (uint64_t)p.plan_id << 32;
+  // this tile's sums (block 0: also the field info), published
+  int64_t mine[3];
+  plan_reduce_block<V>(pa, blk, nb, mine);
+  if (tid == 0) {
+    uint64_t* w = reinterpret_cast<uint64_t*>(flags) + blk * kTileWords;
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      __hip_atomic_store(w + 2 * q, tag | ((uint64_t)mine[q] & 0xffffffffu), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(w + 2 * q + 1, tag | ((uint64_t)mine[q] >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+  }
+
+  __shared__ FieldBytes s_f;
+  SlabRaw<scan_chunk<V>()> raw;
+  plan_scan_prologue<V>(pa, blk, s_f, raw);   // field bytes, and the first loads of the scan in flight
+  __syncthreads();
+
+  // every tile's sums: thread i takes tiles i, i + 256, ...
+  constexpr int kPer = kPlanDirectTiles / kScanThreads;
+  int64_t v[6] = {0, 0, 0, 0, 0, 0};   // prefix items, prefix cost, items, cost, malformed, long bags
+#pragma unroll
+  for (int m = 0; m < kPer; ++m) {
+    const int64_t j = tid + (int64_t)m * kScanThreads;
+    if (j >= nb) continue;
+    const uint64_t* w = reinterpret_cast<const uint64_t*>(flags) + j * kTileWords;
+    uint64_t word[kTileWords];
+    bool ready = false;
+    for (int spin = 0; !ready && spin < kPlanSpinLimit; ++spin) {
+      ready = true;
+#pragma unroll
+      for (int q = 0; q < kTileWords; ++q) {
+        word[q] = __hip_atomic_load(w + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        ready &= (word[q] & 0xffffffff00000000ull) == tag;
+      }
+      if (!ready) __builtin_amdgcn_s_sleep(2);
+    }
+    int64_t si, sc, se;
+    if (ready) {
+      si = (int64_t)((word[0] & 0xffffffffu) | (word[1] << 32));
+      sc = (int64_t)((word[2] & 0xffffffffu) | (word[3] << 32));
+      se = (int64_t)((word[4] & 0xffffffffu) | (word[5] << 32));
+    } else {
+      se = tile_sums_serial<V>(pa, s_f, j, si, sc);
+    }
+    v[0] += j < blk ? si : 0;
+    v[1] += j < blk ? sc : 0;
+    v[2] += si;
+    v[3] += sc;
+    v[4] += (se & 1) != 0 ? 1 : 0;
+    v[5] += se >> 1;
+  }
+  __shared__ int64_t s_red[kWavesPerBlock][6];
+  block_sums<6>(v, s_red);
+  plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], s_f, raw);
+}
+
+// Whether every block of a fused planning launch of nblk tiles is resident at
+// once (so that no flag waits for a block that cannot start).
+template <int V>
+bool plan_fused_fits(int64_t nblk) {
+  static int per_cu = -1, cus = 0;
+  if (per_cu < 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, plan_fused_kernel<V>, kScanThreads, 0) != hipSuccess)
+      n = 0;
+    per_cu = n;
+  }
+  return nblk <= (int64_t)per_cu * cus;
 }
 
 template <int V>
@@ -896,6 +1089,10 @@ hipError_t launch_plan_v(const PlanArgs& a, hipStream_t s) {
       hipLaunchKernelGGL(plan_single_kernel<V>, dim3(1), dim3(kScanThreads), 0, s, a);
       return hipGetLastError();
     }
+  }
+  if (blocks <= (unsigned)kPlanDirectTiles && plan_fused_fits<V>(blocks)) {
+    hipLaunchKernelGGL(plan_fused_kernel<V>, dim3(blocks), dim3(kScanThreads), 0, s, a);
+    return hipGetLastError();
   }
   hipLaunchKernelGGL(plan_reduce_kernel<V>, dim3(blocks), dim3(kScanThreads), 0, s, a);
   hipError_t e = hipGetLastError();

@@ -252,3 +252,20 @@ def test_superseded_plan_is_refused():
     assert st == dpi.DPI_ERR_INVALID_ARG and "later plan" in dpi.dpi_last_error()
     fl.lookup(second, ids, offs)
     assert dpi.dpi_plan_export(second)["header"][2] == 2
+
+
+@pytest.mark.parametrize("T,B", [(2, 100_000), (1, 9_000_000)])
+def test_bad_offsets_detected_in_multi_tile_batches(T, B):
+    """Malformed offsets seen by several threads of one tile, in batches planned
+    by one launch (fewer than 1024 tiles) and by three (more): the plan must
+    reject them.  (A tile's flag once summed the count of threads that saw a
+    malformed bag into its malformed bit, so two such threads cleared it.)"""
+    lengths = np.ones((T, B), np.int64)
+    offs_np = G.offsets_from_lengths(lengths).astype(np.int32)
+    offs_np[0, 1001] = offs_np[0, 1000] - 1     # decreasing: bags 999 and 1000 both malformed
+    offs_np[0, 1500] = offs_np[0, 1499] - 5
+    total = int(offs_np[:, -1].astype(np.int64).sum())
+    tabs = [torch.zeros((10, 16), device="cuda") for _ in range(T)]
+    fl = FusedLookup(tabs)
+    plan = fl.plan(torch.from_numpy(offs_np).cuda(), B, total, num_waves=4096)
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_OFFSETS
