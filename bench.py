@@ -46,7 +46,7 @@ def kernel_source_hash() -> str:
     """Hash of the lookup and plan kernel sources, comments and whitespace
     removed (a comment edit does not make a profile stale)."""
     h = hashlib.sha256()
-    for name in ("lookup.hip", "plan.hip", "dpi_internal.h"):
+    for name in ("lookup.hip", "small.hip", "gather.h", "plan.hip", "dpi_internal.h"):
         with open(os.path.join(ROOT, "paper_2606_21101_amd", "csrc", name)) as f:
             text = f.read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
@@ -364,6 +364,8 @@ def main():
     ap.add_argument("--second-config", type=int, default=None,
                     help="also measure this workload in the same run (default: the multi-hot workload when the "
                          "large one is the headline); 0: none")
+    ap.add_argument("--gated-steps", type=int, default=100,
+                    help="steps of the device-side series (enqueued behind a spin kernel); 0: none")
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
     ap.add_argument("--flush-mib", type=int, default=1024)
@@ -485,6 +487,7 @@ def main():
         "cold": m["cold"],
         "fm_second_order": m["fm"],
         "inflight": m["inflight"],
+        "device_series": m["device_series"],
         "setup_s": m["setup_s"],
         "kernel_source_hash": kernel_source_hash(),
     }
@@ -501,6 +504,7 @@ def main():
             "value": m2["value"], "unit": "rows/s", "ms_per_step": m2["ms_per_step"],
             "p50_lookup_ms": m2["p50_lookup_ms"], "p90_lookup_ms": m2["p90_lookup_ms"],
             "p50_plan_ms": m2["p50_plan_ms"], "p50_step_ms": m2["p50_step_ms"],
+            "device_series": m2["device_series"],
             "cold": m2["cold"],
             "pooled_ids_per_batch": m2["nnz_mean"],
             "algorithmic_bytes_per_batch": m2["alg_mean"],
@@ -604,12 +608,41 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
     t0 = time.perf_counter()
     for i in range(steps):
         plans.append(step(warmup + i, evs[i]))
+    enqueue_s = time.perf_counter() - t0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
     hdr = dpi.dpi_plan_export(plans[-1])["header"]   # before later steps plan into the same workspace
+    # device-side series: the same steps enqueued behind a spin kernel, so the
+    # GPU runs them back to back instead of waiting for the host.  For small
+    # batches the host's enqueue (Python, ctypes, three events) takes longer
+    # than a step, so the timed series above measures the host; these event
+    # times are the device's own step latency.  span_ms_per_step close to the
+    # p50 step shows that the gate held until the last step was enqueued.
+    gated = None
+    if args.gated_steps > 0:
+        n = args.gated_steps
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        torch.cuda._sleep(1_000_000)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        cycles_per_ms = 1_000_000 / max(c0.elapsed_time(c1), 1e-3)
+        gate_ms = 3.0 * (enqueue_s * 1e3 / steps) * n + 2.0
+        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+        torch.cuda._sleep(int(gate_ms * cycles_per_ms))
+        for i in range(n):
+            step(warmup + steps + i, gev[i])
+        torch.cuda.synchronize()
+        g_plan = np.array([e[0].elapsed_time(e[1]) for e in gev])
+        g_look = np.array([e[1].elapsed_time(e[2]) for e in gev])
+        g_step = np.array([e[0].elapsed_time(e[2]) for e in gev])
+        gated = {"steps": n, "gate_ms": gate_ms,
+                 "p50_step_ms": float(np.median(g_step)), "p90_step_ms": float(np.percentile(g_step, 90)),
+                 "p50_plan_ms": float(np.median(g_plan)), "p50_lookup_ms": float(np.median(g_look)),
+                 "span_ms_per_step": gev[0][0].elapsed_time(gev[-1][2]) / n}
     inflight_res = None
     if inflight > 1:
         # steps dealt round-robin to `inflight` streams, each with its own
@@ -707,6 +740,7 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         "cold": cold,
         "fm": fm_res,
         "inflight": inflight_res,
+        "device_series": gated,
         "setup_s": setup_s,
     }
     del plans, tables, batches, out, ws

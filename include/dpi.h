@@ -23,6 +23,9 @@
  *     dpi_plan_t and dpi_dcn_t (the latter also holds a rocBLAS handle, which
  *     manages device memory of its own).  A plan borrows its workspace: the
  *     workspace must outlive the plan and every lookup issued with it.
+ *     Planning into a workspace again supersedes the plan before it:
+ *     dpi_lookup, dpi_plan_sync_status and dpi_plan_export refuse a
+ *     superseded plan (DPI_ERR_INVALID_ARG).
  *   - dpi_plan and dpi_lookup validate host-visible arguments synchronously,
  *     enqueue kernels on `stream` (a hipStream_t; NULL = default stream) and
  *     return without synchronizing.  Device-detected errors (malformed
@@ -120,7 +123,9 @@ int64_t dpi_default_waves(int32_t num_tables, int64_t batch, int64_t total_ids);
 
 /*
  * Bytes of device workspace dpi_plan needs for these sizes (0 on invalid
- * arguments).  max_dim is the largest dim over the fields.
+ * arguments).  max_dim is the largest dim over the fields.  Batches that may
+ * take one launch per lookup also get room for the pieces of long bags:
+ * (16 + 8 * max_dim) / (4 * C) bytes per id.
  */
 size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total_ids,
                                 int32_t max_dim, const dpi_plan_opts* opts);
@@ -139,6 +144,12 @@ size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total
  *   stream:     hipStream_t or NULL;  plan_out: receives the plan handle.
  * Errors: INVALID_ARG, UNSUPPORTED, MISALIGNED, WORKSPACE_TOO_SMALL, HIP
  * synchronously; BAD_OFFSETS later through dpi_plan_sync_status.
+ * One launch per lookup: for a one-hot batch whose fields share one row
+ * class, and for a batch pooled bag by bag (see dpi_lookup) of at most 64
+ * fields and, with offsets, at most 1024 bags per field, dpi_plan enqueues
+ * nothing; each lookup derives the fields' first ids from the offsets and
+ * checks them itself (§I: for small batches a launch costs more than the
+ * lookup's work), and dpi_plan_sync_status before any lookup runs the check.
  */
 dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const int32_t* offsets,
                     int64_t batch, int64_t total_ids, const dpi_plan_opts* opts, void* workspace,
@@ -153,12 +164,16 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
  *   ids, offsets: the batch the plan was built from (same contents);
  *   pooling: host [T] of dpi_pooling, NULL = all sum;
  *   out:     device [B][sum dim] of the plan's out dtype.
- * A plan whose offsets were rejected on the device makes the lookup a no-op.
+ * With malformed offsets (DPI_ERR_BAD_OFFSETS) the lookup writes no row of
+ * a field whose offsets are malformed; whether it writes the other fields is
+ * unspecified.
  * Small and mid-size batches (at most 180000 bags, every row a multiple of
  * 16 bytes and at most 1024 bytes, wave count left at 0) are pooled bag by
  * bag, without the plan's partition: a wave takes a few bags of one field,
- * each bag several row slots.  If the plan counted a bag of more than 4 work
- * items (4*C ids), the same launch uses the partition instead.  An explicit
+ * each bag several row slots.  A bag of more than 4 work items (4*C ids) is
+ * pooled in pieces of at most 4*C ids spread over the field's waves when the
+ * lookup is the batch's only launch (see dpi_plan); otherwise, if the plan
+ * counted such a bag, the lookup uses the partition instead.  An explicit
  * wave count always uses the partition.  Either way the results are within
  * the same tolerance and deterministic.
  */
@@ -308,16 +323,17 @@ void dpi_dcn_destroy(dpi_dcn_t head);
  * caller's buffer.  Calls no allocating routine, host or device.
  *   Arguments as for dpi_plan (with opts) and dpi_lookup; `out` receives the
  *   same values, bit for bit, as that pair with a caller workspace.
- *   device_status: NULL, or device int32 receiving (asynchronously, after the
- *   lookup) the call's device-detected errors: DPI_DEVSTAT_BAD_OFFSETS,
- *   DPI_DEVSTAT_BAD_ID, 0 when none.
+ *   device_status: NULL, or device int32 receiving (asynchronously, by a
+ *   one-thread kernel after the lookup) the call's device-detected errors:
+ *   DPI_DEVSTAT_BAD_OFFSETS, DPI_DEVSTAT_BAD_ID, 0 when none.
  *   stream: a stream of the current device.
  * Every call on a GPU shares that GPU's array, which keeps the last call's
  * contents (each call resets what it reads): calls that overlap on one GPU --
  * on different streams, or from different host threads -- race, and must be
  * serialized by the caller.  A batch whose plan needs more than the array
  * holds (per-wave state and split-bag partials, about 12 + 8 * max dim bytes
- * per wave, plus 48 bytes per field and 24 bytes per tile of bags) returns
+ * per wave, plus 48 bytes per field and 24 bytes per tile of bags, plus the
+ * long-bag pieces of dpi_plan_workspace_bytes) returns
  * DPI_ERR_WORKSPACE_TOO_SMALL and enqueues nothing; other errors as for
  * dpi_plan and dpi_lookup.
  */
@@ -345,10 +361,10 @@ dpi_status dpi_plan_sync_status(dpi_plan_t plan);
  * first item of each wave's first bag -- and so is the wave partition when
  * dpi_lookup will not read it (a batch pooled bag by bag, a one-hot batch of
  * one row class, the input-first allocation) unless some bag is longer than
- * 4 items.  The first export of a plan therefore plans the batch again in
- * full, on the plan's stream, from the offsets given to dpi_plan -- they must
- * still hold the batch, and no lookup of this plan may be in flight on
- * another stream.
+ * 4 items; a plan of one launch per lookup has no planning launch at all.
+ * The first export of a plan therefore plans the batch again in full, on the
+ * plan's stream, from the offsets given to dpi_plan -- they must still hold
+ * the batch, and no lookup of this plan may be in flight on another stream.
  */
 dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base, int64_t* id_base,
                            int64_t* bag_item_base, int64_t* bag_cost_base, int64_t* wave_item_begin);
@@ -368,10 +384,11 @@ dpi_status dpi_plan_export(dpi_plan_t plan, int64_t* header16, int64_t* col_base
  * spread over threads after the whole workload is known).  *source receives 1
  * when the arrays (and dpi_plan_export's wave_item_begin) are the ones the
  * planning launch wrote, copied before the first re-plan -- the arrays a
- * lookup of this plan reads -- and 0 when the planning launch wrote no
+ * lookup of this plan reads -- and 0 when no planning launch wrote a
  * partition (the plan's lookup reads none: a batch pooled bag by bag without a
- * long bag, a one-hot batch of one row class, the input-first allocation) and
- * the export's re-plan computed them.  Any pointer may be NULL.
+ * long bag or in one launch, a one-hot batch of one row class, the
+ * input-first allocation) and the export's re-plan computed them.  Any
+ * pointer may be NULL.
  */
 dpi_status dpi_plan_export_waves(dpi_plan_t plan, int64_t* wave_bag, int64_t* wave_bag_base, int32_t* head_first,
                                  int32_t* split_pieces, int32_t* split_last, int32_t* source);

@@ -8,7 +8,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdpi.so")
-SOURCES = ["api.cpp", "plan.hip", "lookup.hip", "fm.hip", "stage.hip", "interact.hip", "sched.cpp", "noalloc.hip"]
+SOURCES = ["api.cpp", "plan.hip", "lookup.hip", "small.hip", "fm.hip", "stage.hip", "interact.hip", "sched.cpp",
+           "noalloc.hip"]
 ARCH = os.environ.get("DPI_OFFLOAD_ARCH", "gfx950")
 
 HIPCC_FLAGS = [

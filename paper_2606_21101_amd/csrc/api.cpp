@@ -7,7 +7,9 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
+#include <unordered_map>
 #include <vector>
 
 #include "dpi_internal.h"
@@ -36,13 +38,31 @@ constexpr int64_t kSmallBagsPerWave = 8;   // default-wave rule for small batche
 
 struct Layout {
   size_t hdr, status, tinfo, col_base, id_base, block_sum, bib, bcb, wib, wave_bag, wbase, head_first, split_pieces,
-      split_last, tickets, partial, total;
+      split_last, tickets, partial, small_tickets, small_partial, total;
+  int64_t small_slots;   // long-bag piece slots of a one-launch lookup (0: no one-launch bag-by-bag lookup)
 };
 
-// prefixes: room for the per-bag prefixes, which only an export writes (the
-// no-allocation entry point never exports, and leaves them out)
-Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax, bool prefixes = true) {
+// Piece slots a one-launch bag-by-bag lookup of this batch needs (two per
+// window of long_rows ids), or 0 when such a batch is planned by its own
+// launch: more than kSmallMaxFields fields or kSmallMaxBatch bags per field,
+// an explicit wave count, the input-first allocation, or so many windows that
+// a bag's piece count could overflow its ticket.
+int64_t small_slots(int64_t T, int64_t B, int64_t total_ids, const dpi_plan_opts& o, bool waves_given) {
+  if (T > kSmallMaxFields || B < 1 || B > kSmallMaxBatch || waves_given || (o.flags & DPI_FLAG_INPUT_FIRST))
+    return 0;
+  const int64_t pr = (int64_t)kDirectMaxItems * o.chunk_rows;
+  const int64_t windows = (total_ids + pr - 1) / pr;
+  if (windows >= ((int64_t)1 << 22)) return 0;
+  return 2 * windows + 2;
+}
+
+// o: resolved options.  prefixes: room for the per-bag prefixes, which only an
+// export writes (the no-allocation entry point never exports, and leaves them
+// out).
+Layout make_layout(int64_t T, int64_t B, int64_t total_ids, const dpi_plan_opts& o, bool waves_given, int64_t dmax,
+                   bool prefixes = true) {
   Layout L{};
+  const int64_t waves_req = o.num_waves;
   const int64_t TB = T * B;
   const int64_t nblk = plan_tiles(TB);
   size_t off = 0;
@@ -67,6 +87,9 @@ Layout make_layout(int64_t T, int64_t B, int64_t waves_req, int64_t dmax, bool p
   L.split_last = take(waves_req * sizeof(int32_t));
   L.tickets = take(waves_req * sizeof(int32_t));
   L.partial = take(2 * waves_req * dmax * sizeof(float));
+  L.small_slots = small_slots(T, B, total_ids, o, waves_given);
+  L.small_tickets = take(L.small_slots * sizeof(uint64_t));
+  L.small_partial = take(L.small_slots * dmax * sizeof(float));
   L.total = off;
   return L;
 }
@@ -83,6 +106,34 @@ int ilog2(int x) {
   int l = 0;
   while ((1 << l) < x) ++l;
   return l;
+}
+
+// The plan that last planned into each workspace (by address): a plan whose
+// workspace holds a later one is refused by dpi_lookup, the status query and
+// the export.
+std::mutex g_holder_mu;
+std::unordered_map<uintptr_t, int64_t> g_holder;
+
+void set_holder(const void* ws, int64_t plan_id) {
+  std::lock_guard<std::mutex> lock(g_holder_mu);
+  g_holder[reinterpret_cast<uintptr_t>(ws)] = plan_id;
+}
+
+bool is_holder(const void* ws, int64_t plan_id) {
+  std::lock_guard<std::mutex> lock(g_holder_mu);
+  const auto it = g_holder.find(reinterpret_cast<uintptr_t>(ws));
+  return it != g_holder.end() && it->second == plan_id;
+}
+
+dpi_status superseded() {
+  return fail(DPI_ERR_INVALID_ARG, "the plan's workspace holds a later plan: a plan is used up when another plan "
+                                   "is built into its workspace");
+}
+
+void drop_holder(const void* ws, int64_t plan_id) {
+  std::lock_guard<std::mutex> lock(g_holder_mu);
+  const auto it = g_holder.find(reinterpret_cast<uintptr_t>(ws));
+  if (it != g_holder.end() && it->second == plan_id) g_holder.erase(it);
 }
 
 }  // namespace
@@ -113,9 +164,16 @@ struct dpi_plan_s {
   int32_t uniform_class;   // shared row class of every field, or -1
   int32_t direct_jlog;     // small batches looked up bag by bag: log2 of bags per wave, or -1
   int32_t direct_jcap_log; // ... log2 of the most bags a wave of any field takes
-  int64_t plan_id;         // unique in the process; the planning launch stores it in the workspace
+  int64_t plan_id;         // unique in the process; tags the workspace's status word
   int32_t sticky_status;   // status bits latched by lookups before a re-plan
   bool partitioned;        // the plan has been planned again in full (first export)
+  // one launch per lookup: dpi_plan enqueued nothing, each lookup checks the
+  // offsets itself (small_args holds everything of a lookup but the batch's
+  // pointers)
+  bool one_launch;
+  bool looked_up;          // a lookup has been enqueued
+  bool validated;          // the status query ran the planning launch (no lookup before it)
+  SmallArgs small_args;
   // the partition as the planning launch wrote it (what lookups read), copied
   // before the first export plans again; empty when that launch wrote none
   bool snap_valid;
@@ -221,14 +279,15 @@ size_t dpi_plan_workspace_bytes(int32_t num_tables, int64_t batch, int64_t total
     return 0;
   dpi_plan_opts o;
   if (resolve_opts(opts, num_tables, batch, total_ids, o) != DPI_OK) return 0;
-  return make_layout(num_tables, batch, o.num_waves, max_dim).total;
+  return make_layout(num_tables, batch, total_ids, o, opts && opts->num_waves != 0, max_dim).total;
 }
 
 }  // extern "C"
 
-// Validate a batch, fill *plan (caller-owned storage) and enqueue the planning
-// launch into `workspace`; allocates nothing.  prefixes: the workspace has room
-// for the per-bag prefixes (plans that may be exported).
+// Validate a batch, fill *plan (caller-owned storage) and, unless its lookups
+// take one launch each, enqueue the planning launch into `workspace`;
+// allocates nothing.  prefixes: the workspace has room for the per-bag
+// prefixes (plans that may be exported).
 static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, int32_t num_tables,
                             const int32_t* offsets, int64_t batch, int64_t total_ids, const dpi_plan_opts* opts,
                             void* workspace, size_t workspace_bytes, void* stream, bool prefixes) {
@@ -294,7 +353,8 @@ static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, 
       uniform_class = -1;
   }
 
-  const Layout L = make_layout(num_tables, batch, o.num_waves, dmax, prefixes);
+  const bool waves_given = opts && opts->num_waves != 0;
+  const Layout L = make_layout(num_tables, batch, total_ids, o, waves_given, dmax, prefixes);
   if (!workspace) return fail(DPI_ERR_INVALID_ARG, "workspace is NULL");
   if (reinterpret_cast<uintptr_t>(workspace) & 15) return fail(DPI_ERR_MISALIGNED, "workspace not 16-byte aligned");
   if (workspace_bytes < L.total)
@@ -313,7 +373,7 @@ static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, 
   plan->onehot = offsets == nullptr;
   plan->uniform_class = uniform_class;
   plan->direct_jlog = direct_jlog(num_tables, batch, total_ids, row_class, offsets == nullptr, uniform_class,
-                                  o.flags, opts && opts->num_waves != 0);
+                                  o.flags, waves_given);
   plan->direct_jcap_log = plan->direct_jlog;
   if (plan->direct_jlog >= 0) {
     // a grid of several times the waves the GPU holds: fields with more slots
@@ -383,13 +443,53 @@ static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, 
     pa.num_rows[t] = table_meta[t].num_rows;
   }
   plan->args = pa;
+  // One launch per lookup (no planning launch) for one-hot batches of one row
+  // class and for bag-by-bag batches, when the fields' info fits the kernel
+  // arguments and, with offsets, the batch fits the lookup's own offset scan.
+  const bool small_fields = num_tables <= kSmallMaxFields;
+  plan->one_launch = small_fields && batch > 0 &&
+                     (onehot_kernel || (plan->direct_jlog >= 0 && (offsets == nullptr || L.small_slots > 0)));
+  plan->looked_up = false;
+  plan->validated = false;
+  if (plan->one_launch) {
+    SmallArgs& sa = plan->small_args;
+    std::memset(&sa, 0, sizeof(sa));
+    for (int t = 0; t < num_tables; ++t) {
+      sa.packed[t] = pa.packed[t];
+      sa.nrows[t] = (uint32_t)std::min<int64_t>(table_meta[t].num_rows, (int64_t)1 << 31);
+      sa.col_base[t] = (int32_t)col_base[t];
+    }
+    sa.status = reinterpret_cast<uint64_t*>(ws + L.status);
+    sa.tickets = reinterpret_cast<uint64_t*>(ws + L.small_tickets);
+    sa.partial = reinterpret_cast<float*>(ws + L.small_partial);
+    sa.slots = L.small_slots;
+    sa.B = batch;
+    sa.total_d = total_d;
+    sa.total_ids = total_ids;
+    sa.tag = plan->plan_id & kPlanIdMask;
+    sa.long_rows = (int64_t)kDirectMaxItems * o.chunk_rows;
+    sa.T = num_tables;
+    sa.dmax = dmax;
+    sa.out_f16 = o.out_dtype == DPI_F16;
+    sa.xcd_affine = (o.flags & DPI_FLAG_LINEAR_BLOCKS) ? 0 : 1;
+    sa.uniform_class = onehot_kernel ? uniform_class : -1;
+    sa.direct_plog = -1;
+    if (plan->direct_jlog >= 0) {
+      int glog_min = 6;
+      for (int t = 0; t < num_tables; ++t) glog_min = std::min(glog_min, 6 - ((row_class[t] >> kTiLprShift) & 7));
+      sa.direct_plog = glog_min - plan->direct_jlog;
+      sa.direct_jcap_log = plan->direct_jcap_log;
+      sa.direct_wpf = (batch + (1 << plan->direct_jlog) - 1) >> plan->direct_jlog;
+    }
+    return DPI_OK;
+  }
   const hipError_t e = launch_plan(pa, plan->stream);
   if (e != hipSuccess) return hip_fail(e, "plan launch");
   return DPI_OK;
 }
 
 // Enqueue the fused lookup of a plan; allocates nothing.
-static dpi_status lookup_enqueue(const dpi_plan_s* plan, const void* const* tables, const int32_t* ids,
+static dpi_status lookup_enqueue(dpi_plan_s* plan, const void* const* tables, const int32_t* ids,
                                  const int32_t* offsets, const int32_t* pooling, void* out, void* stream) {
   if (!tables) return fail(DPI_ERR_INVALID_ARG, "tables is NULL");
   if ((offsets == nullptr) != plan->onehot)
@@ -408,6 +508,18 @@ static dpi_status lookup_enqueue(const dpi_plan_s* plan, const void* const* tabl
   }
   if (out && (reinterpret_cast<uintptr_t>(out) & 15)) return fail(DPI_ERR_MISALIGNED, "out not 16-byte aligned");
   if (plan->B == 0 || plan->waves_req == 0) return DPI_OK;
+  if (plan->one_launch) {
+    SmallArgs sa = plan->small_args;
+    for (int t = 0; t < plan->T; ++t) sa.tables[t] = tables[t];
+    for (int q = 0; q < kSmallMaxFields / 32; ++q) sa.mean_bits[q] = a.mean_bits[q];
+    sa.ids = ids;
+    sa.offsets = offsets;
+    sa.out = out;
+    const hipError_t e = launch_lookup_small(sa, reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return hip_fail(e, "lookup launch");
+    plan->looked_up = true;
+    return DPI_OK;
+  }
   const Layout& L = plan->layout;
   char* ws = plan->ws;
   a.ids = ids;
@@ -471,7 +583,8 @@ __attribute__((visibility("hidden"))) dpi_status dpi_plan_lookup_into(
   for (int t = 0; t < num_tables; ++t) dmax = std::max(dmax, std::min(table_meta[t].dim, (int32_t)DPI_MAX_DIM));
   dpi_plan_opts o;
   if (batch >= 0 && total_ids >= 0 && resolve_opts(opts, num_tables, batch, total_ids, o) == DPI_OK) {
-    const size_t need = make_layout(num_tables, batch, o.num_waves, dmax, false).total;
+    const size_t need =
+        make_layout(num_tables, batch, total_ids, o, opts && opts->num_waves != 0, dmax, false).total;
     if (need > scratch_bytes)
       return fail(DPI_ERR_WORKSPACE_TOO_SMALL,
                   "this batch needs %zu bytes of scratch (%lld waves), the no-allocation entry point holds %zu",
@@ -484,10 +597,22 @@ __attribute__((visibility("hidden"))) dpi_status dpi_plan_lookup_into(
   st = lookup_enqueue(&plan, tables, ids, offsets, pooling, out, stream);
   if (st != DPI_OK) return st;
   if (device_status) {
-    const hipError_t e = hipMemcpyAsync(device_status, plan.ws + plan.layout.status, sizeof(int32_t),
-                                        hipMemcpyDeviceToDevice, plan.stream);
-    if (e != hipSuccess) return hip_fail(e, "status copy");
+    const hipError_t e = launch_status_out(reinterpret_cast<const uint64_t*>(plan.ws + plan.layout.status),
+                                           plan.plan_id & kPlanIdMask, device_status, plan.stream);
+    if (e != hipSuccess) return hip_fail(e, "status launch");
   }
+  return DPI_OK;
+}
+
+// The plan's error bits from its workspace's status word (zero when the word
+// belongs to another plan) and the planning launch's long-bag count.
+static dpi_status read_status(const dpi_plan_s* plan, int32_t* bits, int32_t* nlong) {
+  uint64_t words[2] = {0, 0};
+  const hipError_t e = hipMemcpy(words, plan->ws + plan->layout.status, sizeof(words), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+  const bool mine = (words[0] >> kStatusTagShift) == (uint64_t)(plan->plan_id & kPlanIdMask);
+  *bits = mine ? (int32_t)(words[0] & kStatusBitsMask) : 0;
+  if (nlong) *nlong = (int32_t)(words[1] & 0xffffffffu);
   return DPI_OK;
 }
 
@@ -506,6 +631,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
     delete plan;
     return st;
   }
+  set_holder(plan->ws, plan->plan_id);
   *plan_out = plan;
   return DPI_OK;
 }
@@ -513,6 +639,7 @@ dpi_status dpi_plan(const dpi_table_meta* table_meta, int32_t num_tables, const 
 dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t* ids, const int32_t* offsets,
                       const int32_t* pooling, void* out, void* stream) {
   if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  if (!is_holder(plan->ws, plan->plan_id)) return superseded();
   return lookup_enqueue(plan, tables, ids, offsets, pooling, out, stream);
 }
 
@@ -612,11 +739,19 @@ dpi_status dpi_stage_csr(const void* packed, int32_t x_dtype, int32_t num_fields
 
 dpi_status dpi_plan_sync_status(dpi_plan_t plan) {
   if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
-  hipError_t e = hipStreamSynchronize(plan->stream);
+  if (!is_holder(plan->ws, plan->plan_id)) return superseded();
+  hipError_t e;
+  if (plan->one_launch && !plan->looked_up && !plan->validated) {
+    // nothing has checked the offsets yet: the planning launch does
+    e = launch_plan(plan->args, plan->stream);
+    if (e != hipSuccess) return hip_fail(e, "plan launch");
+    plan->validated = true;
+  }
+  e = hipStreamSynchronize(plan->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   int32_t status = 0;
-  e = hipMemcpy(&status, plan->ws + plan->layout.status, sizeof(status), hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
+  dpi_status st = read_status(plan, &status, nullptr);
+  if (st != DPI_OK) return st;
   status |= plan->sticky_status;
   if (status & kStatusBadOffsets) return fail(DPI_ERR_BAD_OFFSETS, "device rejected the offsets");
   if (status & kStatusBadId) return fail(DPI_ERR_BAD_ID, "a lookup met an id outside its table");
@@ -640,20 +775,17 @@ hipError_t copy_out(std::vector<V>& v, const char* src, int64_t count) {
 // either unless a bag was long -- from the offsets given to dpi_plan, keeping
 // the status bits earlier lookups latched.
 dpi_status replan_for_export(dpi_plan_t plan) {
+  if (!is_holder(plan->ws, plan->plan_id)) return superseded();
   hipError_t e = hipStreamSynchronize(plan->stream);
   if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize");
   const Layout& L = plan->layout;
-  int32_t status[4] = {0, 0, 0, 0};
-  e = hipMemcpy(status, plan->ws + L.status, sizeof(status), hipMemcpyDeviceToHost);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpy status");
-  int64_t holder = 0;
-  std::memcpy(&holder, status + 2, sizeof(holder));
-  if (holder != plan->plan_id)
-    return fail(DPI_ERR_INVALID_ARG, "the plan's workspace holds a later plan: export a plan before planning "
-                                     "into its workspace again");
   if (plan->partitioned) return DPI_OK;
-  plan->sticky_status |= status[0] & kStatusBadId;
-  const bool written = !(plan->args.p.lazy_partition && status[1] == 0);
+  int32_t bits = 0, nlong = 0;
+  const dpi_status st = read_status(plan, &bits, &nlong);
+  if (st != DPI_OK) return st;
+  plan->sticky_status |= bits & kStatusBadId;
+  // what lookups read: the planning launch's partition, if it ran and wrote one
+  const bool written = !plan->one_launch && !(plan->args.p.lazy_partition && nlong == 0);
   plan->snap_valid = false;
   if (written && plan->B > 0) {
     int64_t hdr[16];
@@ -764,6 +896,10 @@ dpi_status dpi_plan_export_waves(dpi_plan_t plan, int64_t* wave_bag, int64_t* wa
   return DPI_OK;
 }
 
-void dpi_plan_destroy(dpi_plan_t plan) { delete plan; }
+void dpi_plan_destroy(dpi_plan_t plan) {
+  if (!plan) return;
+  drop_holder(plan->ws, plan->plan_id);
+  delete plan;
+}
 
 }  // extern "C"

@@ -31,9 +31,27 @@ constexpr int kDirectMaxItems = 4;
 constexpr int kDirectGroupRows = 8;   // rows in flight per slot
 constexpr int64_t kDirectMaxBags = 180000;
 
-// status word bits (device-latched errors)
+// Status words in the workspace.  Word 0 (64 bits): device-latched error
+// bits in the low kStatusTagShift bits, the id of the plan they belong to
+// above them; a word holding another plan's id holds no error of this plan,
+// so a plan needs no launch to clear it.  Word kStatusLongWord (32 bits): the
+// bags of more than kDirectMaxItems items the planning launch counted.
 constexpr int kStatusBadOffsets = 1;
 constexpr int kStatusBadId = 2;
+constexpr int kStatusTagShift = 24;
+constexpr uint64_t kStatusBitsMask = (1ull << kStatusTagShift) - 1;
+constexpr int64_t kPlanIdMask = ((int64_t)1 << (64 - kStatusTagShift)) - 1;
+constexpr int kStatusLongWord = 2;
+
+__host__ __device__ inline uint64_t status_word(int64_t plan_id, uint32_t bits) {
+  return ((uint64_t)(plan_id & kPlanIdMask) << kStatusTagShift) | bits;
+}
+
+// One-launch batches: at most kSmallMaxFields fields (their static info
+// travels in the kernel arguments) and, with offsets, at most kSmallMaxBatch
+// bags per field (every wave of a field reads all of the field's offsets).
+constexpr int kSmallMaxFields = 64;
+constexpr int64_t kSmallMaxBatch = 1024;
 
 // header16 slots
 enum : int {
@@ -63,8 +81,7 @@ struct alignas(16) TableInfo {
 // Device pointers of a plan inside the caller's workspace.
 struct PlanDev {
   int64_t* hdr;          // [16]
-  int32_t* status;       // [4]: error bits; bags of more than kDirectMaxItems items; then the int64
-                         // id of the plan that last planned into this workspace
+  int32_t* status;       // [4]: the status words (kStatus*)
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
@@ -100,8 +117,7 @@ struct PlanParams {
   int64_t total_ids;
   int64_t waves_req;
   int64_t total_d;
-  int64_t plan_id;         // written next to the status words: tells a plan whether its workspace
-                           // still holds it
+  int64_t plan_id;         // tags the status word
   const int32_t* offsets;  // device [T][B+1] or nullptr
 };
 
@@ -152,6 +168,41 @@ struct LookupArgs {
   uint8_t lpr_log[DPI_MAX_TABLES];
 };
 
+// Kernel arguments of the one-launch lookups (small.hip): one-hot batches of
+// one row class, and bag-by-bag batches whose fields all take the 16-byte row
+// path.  Nothing of the batch is planned beforehand: the kernel derives each
+// field's first id from the offsets, checks the offsets, and pools bags of
+// more than long_rows ids in pieces of at most long_rows ids spread over the
+// field's waves (fp32 partials combined by the last piece to arrive).
+struct SmallArgs {
+  const void* tables[kSmallMaxFields];
+  uint32_t packed[kSmallMaxFields];     // dim | TableInfo flags << 17
+  uint32_t nrows[kSmallMaxFields];      // min(num_rows, 2^31)
+  int32_t col_base[kSmallMaxFields];
+  uint32_t mean_bits[kSmallMaxFields / 32];
+  const int32_t* ids;
+  const int32_t* offsets;               // device [T][B+1], or nullptr (one id per bag)
+  void* out;
+  uint64_t* status;                     // status word 0
+  uint64_t* tickets;                    // [slots] arrival counters of long bags (tagged like the status)
+  float* partial;                       // [slots][dmax] fp32 sums of long-bag pieces
+  int64_t slots;                        // 2 * ceil(total_ids / long_rows) + 2
+  int64_t B;
+  int64_t total_d;
+  int64_t total_ids;
+  int64_t tag;                          // the plan's id (masked by kPlanIdMask)
+  int64_t long_rows;                    // kDirectMaxItems * C
+  int32_t T;
+  int32_t dmax;
+  int32_t out_f16;
+  int32_t xcd_affine;
+  int32_t uniform_class;                // one-hot: the class shared by every field
+  // bag by bag (as in LookupArgs)
+  int32_t direct_plog;
+  int32_t direct_jcap_log;
+  int64_t direct_wpf;
+};
+
 // Second-order FM term over a [B, row_stride] block of T fields of dim D.
 struct FmArgs {
   const void* emb;
@@ -200,6 +251,9 @@ inline int64_t plan_tiles(int64_t TB) {
 // kernel launchers (plan.hip / lookup.hip); return the launch's hipError_t
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_lookup(const LookupArgs& a, hipStream_t s);
+hipError_t launch_lookup_small(const SmallArgs& a, hipStream_t s);
+// *dst = the error bits of status word *word when it belongs to plan `tag`, else 0
+hipError_t launch_status_out(const uint64_t* word, int64_t tag, int32_t* dst, hipStream_t s);
 hipError_t launch_fm(const FmArgs& a, hipStream_t s);
 hipError_t launch_stage(const StageArgs& a, hipStream_t s);
 hipError_t launch_stage_csr(const void* src, int32_t x_dtype, int64_t n_off, int64_t n_ids, int32_t* offsets,

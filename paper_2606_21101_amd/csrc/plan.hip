@@ -697,9 +697,8 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     d.wbase[0] = 0;
     if (W > 0 && partition) d.head_first[0] = -1;   // wave 0 starts at the first bag
     // the only writer of the status words during planning; lookups latch later
-    d.status[0] = err ? kStatusBadOffsets : 0;
-    d.status[1] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
-    *reinterpret_cast<int64_t*>(d.status + 2) = p.plan_id;
+    *reinterpret_cast<uint64_t*>(d.status) = status_word(p.plan_id, err ? kStatusBadOffsets : 0);
+    d.status[kStatusLongWord] = nlong < INT32_MAX ? (int32_t)nlong : INT32_MAX;
   }
   int64_t* const tile_splits = d.block_sum + 3 * nb + 3;
   if (p.TB == 0 || !partition) {   // block-uniform
@@ -894,9 +893,8 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
     h[kHdrSplit] = 0;
     h[14] = 0;
     h[15] = 0;
-    d.status[0] = bad ? kStatusBadOffsets : 0;
-    d.status[1] = 0;   // every bag is one item
-    *reinterpret_cast<int64_t*>(d.status + 2) = p.plan_id;
+    *reinterpret_cast<uint64_t*>(d.status) = status_word(p.plan_id, bad ? kStatusBadOffsets : 0);
+    d.status[kStatusLongWord] = 0;   // every bag is one item
   }
   const int64_t first = (int64_t)blockIdx.x * kScanThreads + tid, stride = (int64_t)gridDim.x * kScanThreads;
   for (int64_t j = first; j < p.nblk; j += stride) d.block_sum[3 * (int64_t)p.nblk + 3 + j] = 0;   // no split bags

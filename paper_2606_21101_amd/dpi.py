@@ -198,26 +198,16 @@ def dpi_plan_workspace_bytes(num_tables: int, batch: int, total_ids: int, max_di
 class Plan:
     """Handle of a device plan; keeps the borrowed buffers alive.  A workspace
     holds one plan at a time: planning into it again supersedes the plan before,
-    which then refuses lookups and exports."""
+    which the library then refuses for lookups, status queries and exports."""
     handle: int
     num_tables: int
     batch: int
     keep: tuple
-    workspace_ptr: int = 0
-    serial: int = 0
-
-    def check_current(self):
-        if _workspace_holder.get(self.workspace_ptr) != self.serial:
-            raise DpiError(DPI_ERR_INVALID_ARG, "plan superseded: its workspace holds a later plan")
 
     def __del__(self):
         if self.handle and _lib is not None:
             _lib.dpi_plan_destroy(ctypes.c_void_p(self.handle))
             self.handle = 0
-
-
-_workspace_holder = {}   # workspace address -> serial of the plan that last planned into it
-_plan_serial = [0]
 
 
 def dpi_plan(table_meta, offsets, batch: int, total_ids: int, opts: Optional[dpi_plan_opts], workspace,
@@ -231,10 +221,7 @@ def dpi_plan(table_meta, offsets, batch: int, total_ids: int, opts: Optional[dpi
                       ctypes.byref(opts) if opts is not None else None, _ptr(workspace), workspace_bytes,
                       _stream(stream), ctypes.byref(out))
     _check(st)
-    _plan_serial[0] += 1
-    ws_ptr = _ptr(workspace) or 0
-    _workspace_holder[ws_ptr] = _plan_serial[0]
-    return Plan(out.value, T, batch, (workspace, offsets, table_meta), ws_ptr, _plan_serial[0])
+    return Plan(out.value, T, batch, (workspace, offsets, table_meta))
 
 
 def table_array(tables) -> ctypes.Array:
@@ -250,7 +237,6 @@ def pooling_array(pooling: Sequence[int]) -> ctypes.Array:
 def dpi_lookup(plan: Plan, tables, ids, offsets, pooling: Optional[Sequence[int]], out, stream=None) -> None:
     """tables / pooling: sequences, or the arrays table_array / pooling_array built."""
     lib = load()
-    plan.check_current()
     T = plan.num_tables
     ptrs = tables if isinstance(tables, ctypes.Array) else table_array(tables)
     pool = pooling if (pooling is None or isinstance(pooling, ctypes.Array)) else pooling_array(pooling)
@@ -285,7 +271,6 @@ def dpi_plan_sync_status(plan: Plan) -> int:
 
 def dpi_plan_export(plan: Plan) -> dict:
     lib = load()
-    plan.check_current()
     hdr = np.zeros(16, dtype=np.int64)
     p64 = ctypes.POINTER(ctypes.c_int64)
     _check(lib.dpi_plan_export(ctypes.c_void_p(plan.handle), hdr.ctypes.data_as(p64), None, None, None, None, None))
@@ -306,7 +291,6 @@ def dpi_plan_export_waves(plan: Plan) -> dict:
     """What a lookup reads of the plan besides the wave starts; "source" is 1 when
     these are the arrays the planning launch wrote (see include/dpi.h)."""
     lib = load()
-    plan.check_current()
     hdr = np.zeros(16, dtype=np.int64)
     p64 = ctypes.POINTER(ctypes.c_int64)
     p32 = ctypes.POINTER(ctypes.c_int32)

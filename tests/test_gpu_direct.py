@@ -1,10 +1,13 @@
 """Small batches looked up bag by bag (no partition), against the oracle.
 
 With the wave count left to the library, a batch of at most 180,000 bags whose
-fields all take the 16-byte row path is pooled bag by bag; a bag of more than
-four chunks anywhere in the batch sends the same launch back to the plan's
-partition.  Every case is also run with an explicit wave count (the plan's
-partition) and both results are checked against the oracle.
+fields all take the 16-byte row path is pooled bag by bag.  Up to 64 fields
+and 1024 bags per field that is one launch per lookup, which pools a bag of
+more than four chunks in pieces over the field's waves; larger batches are
+planned by their own launch first, and a bag of more than four chunks anywhere
+in the batch sends the lookup to the plan's partition.  Every case is also run
+with an explicit wave count (the plan's partition) and both results are
+checked against the oracle.
 """
 import numpy as np
 import pytest
@@ -46,7 +49,7 @@ def test_direct_one_field_long_bags_up_to_the_limit(B):
 
 
 @pytest.mark.parametrize("long_len", [129, 1000, 20000])
-def test_direct_falls_back_for_a_long_bag(long_len):
+def test_direct_long_bag(long_len):
     rng = np.random.default_rng(long_len)
     B = 20
     tables, ids, offs, pool = random_problem(rng, [16, 64, 8], [0, 1, 0], B, 30, rows=500)
@@ -104,17 +107,23 @@ def test_direct_bad_ids_reported_and_skipped():
     check(tables_z, fixed, offs, [0, 0], 12, out)
 
 
-def test_direct_bad_offsets_make_the_lookup_a_no_op():
+@pytest.mark.parametrize("B", [2, 2000])
+def test_direct_bad_offsets_reported_and_their_field_not_written(B):
+    # one launch (B = 2) and planned by its own launch (B = 2000)
     tabs = [torch.zeros((10, 16), device="cuda"), torch.zeros((10, 8), device="cuda", dtype=torch.float16)]
     from paper_2606_21101_amd.lookup import FusedLookup
     fl = FusedLookup(tabs)
-    offs = torch.tensor([[0, 2, 1], [0, 1, 2]], dtype=torch.int32, device="cuda")
-    plan = fl.plan(offs, 2, 4)
+    offs_np = np.stack([np.arange(B + 1), np.arange(B + 1)]).astype(np.int32)
+    offs_np[0, 1] = 2
+    offs_np[0, 2] = 1                      # field 0 decreases
+    offs = torch.from_numpy(offs_np).cuda()
+    total = int(offs_np[:, -1].sum())
+    plan = fl.plan(offs, B, total)
     assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_OFFSETS
-    out = torch.full((2, 24), 7.0, device="cuda")
-    fl.lookup(plan, torch.zeros(4, dtype=torch.int32, device="cuda"), offs, out)
-    torch.cuda.synchronize()
-    assert torch.all(out == 7.0)
+    out = torch.full((B, 24), 7.0, device="cuda")
+    fl.lookup(plan, torch.zeros(total, dtype=torch.int32, device="cuda"), offs, out)
+    assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_OFFSETS
+    assert torch.all(out[:, :16] == 7.0)
 
 
 def test_direct_repeated_lookups_deterministic():

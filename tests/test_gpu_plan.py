@@ -182,7 +182,7 @@ def test_bad_offsets_detected():
         ids = torch.zeros(total, dtype=torch.int32, device="cuda")
         fl.lookup(plan, ids, offs, out)
         torch.cuda.synchronize()
-        assert torch.all(out == 7.0)      # a rejected plan makes the lookup a no-op
+        assert torch.all(out == 7.0)      # the malformed field is not written
         fl_if = FusedLookup(tabs, flags=dpi.DPI_FLAG_INPUT_FIRST)
         plan_if = fl_if.plan(offs, 2, total, num_waves=4)
         assert dpi.dpi_plan_sync_status(plan_if) == dpi.DPI_ERR_BAD_OFFSETS

@@ -80,3 +80,37 @@ def test_noalloc_rejects_a_batch_beyond_the_scratch():
     assert "scratch" in dpi.dpi_last_error()
     torch.cuda.synchronize()
     assert torch.all(out == 3.0)
+
+
+def test_noalloc_long_bags_and_bad_offsets():
+    """A small batch with long bags (one launch per lookup: the long bags pooled
+    in pieces over their fields' waves) bit for bit against the workspace path,
+    then malformed offsets reported in the device status word."""
+    from test_gpu_edges import random_problem
+    rng = np.random.default_rng(31)
+    B = 40
+    tables, _, offs0, pool = random_problem(rng, [16, 64], [0, 1], B, 10, rows=300)
+    lens = np.diff(offs0, axis=1).astype(np.int64)
+    lens[1, 5] = 3000
+    lens[0, 39] = 200
+    offs = np.zeros((2, B + 1), np.int32)
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    ids = np.concatenate([rng.integers(0, 300, int(offs[t, -1])) for t in range(2)]).astype(np.int32)
+    tt = [torch.from_numpy(t).cuda() for t in tables]
+    ids_d, offs_d = torch.from_numpy(ids).cuda(), torch.from_numpy(offs).cuda()
+    fl = FusedLookup(tt, pool)
+    ref = fl(ids_d, offs_d, B)
+    out = torch.full_like(ref, float("nan"))
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    print(f"  noalloc: long bags B={B}", flush=True)
+    dpi.dpi_lookup_noalloc(fl.meta, tt, ids_d, offs_d, B, len(ids), pool, fl.opts(), out, status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == 0
+    assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
+    bad = offs.copy()
+    bad[0, 3] = bad[0, 2] - 1
+    status.fill_(-1)
+    dpi.dpi_lookup_noalloc(fl.meta, tt, ids_d, torch.from_numpy(bad).cuda(), B, len(ids), pool, fl.opts(),
+                           torch.empty_like(ref), status)
+    torch.cuda.synchronize()
+    assert int(status.item()) == dpi.DPI_DEVSTAT_BAD_OFFSETS
