@@ -326,7 +326,7 @@ def sched_sweep(args, dev) -> dict:
         marks = torch.zeros((args.steps + args.warmup, 2), dtype=torch.int64, device=dev)
         row = {"batch": B}
         for mode, name in names.items():
-            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps + args.warmup)]
+            evs = timing_events(args.steps + args.warmup, 2, after)
             for i in range(args.steps + args.warmup):
                 evs[i][0].record(after)
                 head.forward(x0, oc, om, mode, se, si, after, marks[i])
@@ -364,8 +364,9 @@ def main():
     ap.add_argument("--second-config", type=int, default=None,
                     help="also measure this workload in the same run (default: the multi-hot workload when the "
                          "large one is the headline); 0: none")
-    ap.add_argument("--gated-steps", type=int, default=100,
-                    help="steps of the device-side series (enqueued behind a spin kernel); 0: none")
+    ap.add_argument("--graph-steps", type=int, default=16,
+                    help="steps captured in one HIP graph for the device-side series; 0: none")
+    ap.add_argument("--graph-replays", type=int, default=50)
     ap.add_argument("--cold-steps", type=int, default=10,
                     help="extra steps, each after overwriting a buffer larger than the caches (0: none)")
     ap.add_argument("--flush-mib", type=int, default=1024)
@@ -475,6 +476,7 @@ def main():
         "p50_plan_ms": m["p50_plan_ms"],
         "p50_step_ms": m["p50_step_ms"],
         "wall_ms_per_step": m["wall_ms_per_step"],
+        "max_gap_ms": m["max_gap_ms"],
         "pooled_ids_per_batch": m["nnz_mean"],
         "algorithmic_bytes_per_batch": m["alg_mean"],
         "gathered_bytes_per_batch": m["gathered_mean"],
@@ -530,6 +532,19 @@ def roofline(alg_bytes: float, mean_ms: float, traffic) -> dict:
             "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, "mean_lookup_ms": mean_ms}
 
 
+def timing_events(n: int, k: int, stream):
+    """n lists of k timing events, each recorded once already: torch creates an
+    event's device object on its first record, which costs tens of
+    microseconds of host time, far more than a small batch's step."""
+    import torch
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(k)] for _ in range(n)]
+    for row in evs:
+        for e in row:
+            e.record(stream)
+    torch.cuda.synchronize()
+    return evs
+
+
 def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight: int = 1) -> dict:
     """Tables and R rotating batches of one workload resident on the device, then
     untimed clock-ramp steps, warm-up steps, the timed warm series (HIP events on
@@ -579,16 +594,17 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
     table_ptrs = dpi.table_array(tables)
     pool_arr = None if pool is None else dpi.pooling_array(pool)
 
-    def step(i, ev=None):
+    def step(i, ev=None, s=None):
+        s = stream if s is None else s
         bt = batches[i % len(batches)]
         if ev is not None:
-            ev[0].record(stream)
-        plan = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, opts, ws, ws_bytes, stream=stream)
+            ev[0].record(s)
+        plan = dpi.dpi_plan(fl.meta, bt.offsets, cfg.batch, bt.total_ids, opts, ws, ws_bytes, stream=s)
         if ev is not None:
-            ev[1].record(stream)
-        dpi.dpi_lookup(plan, table_ptrs, bt.ids, bt.offsets, pool_arr, out, stream=stream)
+            ev[1].record(s)
+        dpi.dpi_lookup(plan, table_ptrs, bt.ids, bt.offsets, pool_arr, out, stream=s)
         if ev is not None:
-            ev[2].record(stream)
+            ev[2].record(s)
         return plan
 
     # untimed steps until the clocks have ramped (short steps would otherwise be
@@ -604,45 +620,49 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         step(i)
     torch.cuda.synchronize()
     plans = []
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
+    evs = timing_events(steps, 3, stream)
     t0 = time.perf_counter()
     for i in range(steps):
         plans.append(step(warmup + i, evs[i]))
-    enqueue_s = time.perf_counter() - t0
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
     hdr = dpi.dpi_plan_export(plans[-1])["header"]   # before later steps plan into the same workspace
-    # device-side series: the same steps enqueued behind a spin kernel, so the
-    # GPU runs them back to back instead of waiting for the host.  For small
-    # batches the host's enqueue (Python, ctypes, three events) takes longer
-    # than a step, so the timed series above measures the host; these event
-    # times are the device's own step latency.  span_ms_per_step close to the
-    # p50 step shows that the gate held until the last step was enqueued.
-    gated = None
-    if args.gated_steps > 0:
-        n = args.gated_steps
-        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        c0.record(stream)
-        torch.cuda._sleep(1_000_000)
-        c1.record(stream)
+    # device-side series: K consecutive steps captured in one HIP graph and
+    # replayed, so the GPU runs them back to back instead of waiting for the
+    # host.  For small batches the host's enqueue (Python, ctypes, events)
+    # takes longer than a step, so the timed series above measures the host;
+    # a replay's time over K is the device's own time per step (launch gaps
+    # between the step's kernels included).  The replayed output is checked
+    # against the same step run eagerly.
+    graph_res = None
+    if args.graph_steps > 0:
+        K, R = args.graph_steps, args.graph_replays
+        gs = torch.cuda.Stream()
+        gs.wait_stream(stream)
+        g = torch.cuda.CUDAGraph()
+        gplans = []
+        with torch.cuda.graph(g, stream=gs):
+            for i in range(K):
+                gplans.append(step(i, s=gs))
         torch.cuda.synchronize()
-        cycles_per_ms = 1_000_000 / max(c0.elapsed_time(c1), 1e-3)
-        gate_ms = 3.0 * (enqueue_s * 1e3 / steps) * n + 2.0
-        gev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
-        torch.cuda._sleep(int(gate_ms * cycles_per_ms))
-        for i in range(n):
-            step(warmup + steps + i, gev[i])
+        rev = timing_events(R, 2, stream)
+        for r in range(R):
+            rev[r][0].record(stream)
+            g.replay()
+            rev[r][1].record(stream)
         torch.cuda.synchronize()
-        g_plan = np.array([e[0].elapsed_time(e[1]) for e in gev])
-        g_look = np.array([e[1].elapsed_time(e[2]) for e in gev])
-        g_step = np.array([e[0].elapsed_time(e[2]) for e in gev])
-        gated = {"steps": n, "gate_ms": gate_ms,
-                 "p50_step_ms": float(np.median(g_step)), "p90_step_ms": float(np.percentile(g_step, 90)),
-                 "p50_plan_ms": float(np.median(g_plan)), "p50_lookup_ms": float(np.median(g_look)),
-                 "span_ms_per_step": gev[0][0].elapsed_time(gev[-1][2]) / n}
+        replayed = out.clone()
+        step(K - 1)
+        torch.cuda.synchronize()
+        if not torch.equal(replayed.view(torch.uint8), out.view(torch.uint8)):
+            raise SystemExit("graph replay output differs from the eager step")
+        per_step = np.array([e[0].elapsed_time(e[1]) for e in rev]) / K
+        graph_res = {"steps_per_graph": K, "replays": R, "p50_step_ms": float(np.median(per_step)),
+                     "min_step_ms": float(per_step.min()), "mean_step_ms": float(per_step.mean())}
+        del g, gplans
     inflight_res = None
     if inflight > 1:
         # steps dealt round-robin to `inflight` streams, each with its own
@@ -662,7 +682,7 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         for i in range(warmup):
             step_on(i, i % n)
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        (e0, e1), = timing_events(1, 2, stream)
         e0.record(stream)
         for st in streams:
             st.wait_stream(stream)
@@ -687,7 +707,7 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         D = dims.pop()
         y = torch.empty(cfg.batch, dtype=torch.float32, device=dev)
         odt = dpi.DPI_F16 if out_dt == torch.float16 else dpi.DPI_F32
-        fev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps + warmup)]
+        fev = timing_events(steps + warmup, 2, stream)
         for i in range(steps + warmup):
             fev[i][0].record(stream)
             dpi.dpi_fm_second_order(out, odt, cfg.batch, cfg.num_tables, D, total_d, y, stream=stream)
@@ -704,7 +724,7 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         # cold series: the L2s and the 256 MB Infinity Cache are overwritten
         # before each step, outside the timed events
         flush = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
-        cev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.cold_steps)]
+        cev = timing_events(args.cold_steps, 3, stream)
         for i in range(args.cold_steps):
             flush.fill_(i & 0xFF)
             step(warmup + steps + i, cev[i])
@@ -732,6 +752,7 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         "p50_plan_ms": float(np.median(plan_ms)),
         "p50_step_ms": float(np.median(plan_ms + look_ms)),
         "wall_ms_per_step": wall * 1e3 / steps,
+        "max_gap_ms": float(max([evs[i][2].elapsed_time(evs[i + 1][0]) for i in range(steps - 1)], default=0.0)),
         "nnz_mean": float(np.mean(nnz_list)),
         "alg_mean": float(steps_alg.mean()),
         "gathered_mean": float(steps_gath.mean()),
@@ -740,7 +761,7 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
         "cold": cold,
         "fm": fm_res,
         "inflight": inflight_res,
-        "device_series": gated,
+        "device_series": graph_res,
         "setup_s": setup_s,
     }
     del plans, tables, batches, out, ws

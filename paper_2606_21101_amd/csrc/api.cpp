@@ -560,7 +560,8 @@ static dpi_status lookup_enqueue(dpi_plan_s* plan, const void* const* tables, co
     a.direct_plog = glog_min - plan->direct_jlog;
     a.direct_jcap_log = plan->direct_jcap_log;
     a.direct_wpf = (plan->B + (1 << plan->direct_jlog) - 1) >> plan->direct_jlog;
-    for (int t = 0; t < plan->T; ++t) a.lpr_log[t] = (uint8_t)((plan->row_class[t] >> kTiLprShift) & 7);
+    for (int t = 0; t < plan->T; ++t)
+      a.lpr_log[t >> 2] |= (uint32_t)((plan->row_class[t] >> kTiLprShift) & 7) << (8 * (t & 3));
   }
   const hipError_t e = launch_lookup(a, reinterpret_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "lookup launch");

@@ -165,7 +165,7 @@ struct LookupArgs {
   int32_t direct_plog;
   int32_t direct_jcap_log;
   int64_t direct_wpf;
-  uint8_t lpr_log[DPI_MAX_TABLES];
+  uint32_t lpr_log[DPI_MAX_TABLES / 4];   // byte t & 3 of word t >> 2 (a dword: one scalar load)
 };
 
 // Kernel arguments of the one-launch lookups (small.hip): one-hot batches of

@@ -638,26 +638,25 @@ void lookup_direct_kernel(const LookupArgs args) {
   const int lane = threadIdx.x & (kWaveSize - 1);
   const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   // the plan's verdicts, the field's info and the wave's bag offsets are all
-  // requested before the first of them is needed (one round trip, not three)
+  // requested before the first of them is needed (one round trip, not three):
+  // the slot count comes from a kernel-argument dword (a scalar load), and
+  // every lane loads offsets from a clamped, valid index, keeping only its
+  // own (a load under a branch is waited for before the branch joins)
   const int32_t st_err = a->status[0], st_long = a->status[kStatusLongWord];
   const int64_t wpf = a->direct_wpf;
   const int64_t t = w < wpf * a->T ? uni(w / wpf) : 0;
-  // this field's bags per wave (its slot count from the kernel arguments)
-  const int jlog = min(6 - (int)a->lpr_log[t] - a->direct_plog, a->direct_jcap_log);
+  const int lpr_log = (int)((a->lpr_log[t >> 2] >> (8 * (t & 3))) & 7);
+  const int jlog = min(6 - lpr_log - a->direct_plog, a->direct_jcap_log);
   const int64_t b0 = (w - t * wpf) << jlog;
   const bool mine = w < wpf * a->T && b0 < a->B;
-  DirectOffsets o{0, 0};
-  if (mine && lane < (1 << jlog)) {
-    const int64_t bl = min(b0 + lane, a->B - 1);   // bags past the batch end are inactive
-    if (a->offsets) {
-      const int32_t* src = a->offsets + t * (a->B + 1) + bl;
-      o.lo = src[0];
-      o.hi = src[1];
-    } else {
-      o.lo = (int32_t)bl;
-      o.hi = (int32_t)bl + 1;
-    }
+  const int64_t bl = min(b0 + lane, a->B - 1);   // bags past the batch end are inactive
+  DirectOffsets o{(int32_t)bl, (int32_t)bl + 1};
+  if (a->offsets) {
+    const int32_t* src = a->offsets + t * (a->B + 1) + bl;
+    o.lo = src[0];
+    o.hi = src[1];
   }
+  if (!(mine && lane < (1 << jlog))) o = DirectOffsets{0, 0};
   const TableInfo ti = table_info(a, t);
   if (st_err & kStatusBadOffsets) return;   // the plan rejected the offsets
   if (st_long != 0) {                       // a long bag: the plan's partition

@@ -25,6 +25,7 @@
 // word holding another id counts as clear, so no launch resets them, and the
 // last arrival of a bag clears its ticket for the next lookup of the plan.
 #include "gather.h"
+#include "wave_scan.h"
 
 namespace dpi {
 namespace {
@@ -81,22 +82,6 @@ __device__ int64_t ticket_arrive(uint64_t* tk, int64_t tag) {
                                              __HIP_MEMORY_SCOPE_AGENT))
       return (int64_t)(n + 1);
   }
-}
-
-__device__ __forceinline__ int64_t wave_sum(int64_t v) {
-#pragma unroll
-  for (int m = 1; m < kWaveSize; m <<= 1) v += __shfl_xor(v, m, kWaveSize);
-  return v;
-}
-
-__device__ __forceinline__ int64_t wave_exclusive(int64_t v, int lane) {
-  int64_t x = v;
-#pragma unroll
-  for (int m = 1; m < kWaveSize; m <<= 1) {
-    const int64_t y = __shfl_up(x, m, kWaveSize);
-    if (lane >= m) x += y;
-  }
-  return x - v;
 }
 
 // Pieces of a long bag occupying flat ids [gs, ge): the windows of pr ids it
@@ -156,7 +141,7 @@ __device__ __attribute__((noinline)) int long_piece(KS a, const TableInfo& ti, i
     const int32_t* row = a->offsets + t * (a->B + 1) + first;
     int32_t u[kScanMax + 1];
 #pragma unroll
-    for (int j = 0; j <= kScanMax; ++j) u[j] = j <= nb ? row[j] : 0;
+    for (int j = 0; j <= kScanMax; ++j) u[j] = row[min((int64_t)j, nb)];
     int64_t r = q - pre;
     bool found = false;
 #pragma unroll
@@ -227,7 +212,8 @@ void lookup_small_direct_kernel(const SmallArgs args) {
   const int64_t wpf = a->direct_wpf;
   const int32_t T = a->T;
   if (w >= wpf * T) return;
-  const int64_t t = uni(w / wpf);
+  // grids hold fewer than 2^31 waves: a 32-bit division
+  const int64_t t = uni((int32_t)((uint32_t)w / (uint32_t)wpf));
   const int64_t i = w - t * wpf;   // the wave's rank among the field's waves
   const int lpr_log = (int)((a->packed[t] >> (17 + kTiLprShift)) & 7);
   const int jlog = min(6 - lpr_log - a->direct_plog, a->direct_jcap_log);
@@ -249,44 +235,59 @@ void lookup_small_direct_kernel(const SmallArgs args) {
     }
   } else {
     // the wave's bag offsets, every field's id count and all of this field's
-    // offsets (lane l: bags [l * bpl, l * bpl + bpl)), requested together
+    // offsets (lane l: bags [l * bpl, l * bpl + bpl)), requested together:
+    // every lane loads from a clamped, valid index and the values it does not
+    // need are dropped afterwards (a load under a branch makes the compiler
+    // wait for it before the branch joins, one round trip per branch)
     const int32_t* const row = offs + t * (B + 1);
-    if (mine && lane < (1 << jlog)) {
-      const int64_t bl = min(b0 + lane, B - 1);
-      o.lo = row[bl];
-      o.hi = row[bl + 1];
-    }
-    const int64_t nnz_l = lane < T ? (int64_t)offs[(int64_t)lane * (B + 1) + B] : 0;
+    const int64_t bl = min(b0 + lane, B - 1);
+    const int32_t lo = row[bl], hi = row[bl + 1];
+    const int32_t nz = offs[(int64_t)min(lane, T - 1) * (B + 1) + B];
     const int64_t bpl = (B + kWaveSize - 1) / kWaveSize;
     const int64_t first = lane * bpl;
     int32_t v[kScanMax + 1];
 #pragma unroll
-    for (int j = 0; j <= kScanMax; ++j) v[j] = (j <= bpl && first + j <= B) ? row[first + j] : 0;
-    // the field's first id and id count; the counts must add up to total_ids
-    const int64_t total = wave_sum(nnz_l);
-    const int64_t id_base = wave_sum(lane < t ? nnz_l : 0);
-    const int64_t nnz = __shfl(nnz_l, (int)t, kWaveSize);
-    if (__any(nnz_l < 0) || total != a->total_ids) {
-      if (w == 0 && lane == 0) latch(a, kStatusBadOffsets);
-      return;
+    for (int j = 0; j <= kScanMax; ++j) v[j] = row[min(first + j, B)];
+    if (mine && lane < (1 << jlog)) {
+      o.lo = lo;
+      o.hi = hi;
     }
+    const int64_t nnz_l = lane < T ? (int64_t)nz : 0;
+    // the field's first id and id count (one DPP scan of the counts); the
+    // counts must add up to total_ids.  The checks are branch-free up to the
+    // first exit, so that no load above is moved below a branch.
+    const int64_t incl = wave_incl_scan(nnz_l, lane);
+    const int64_t total = lane_value(incl, kWaveSize - 1);
+    const int64_t nnz = lane_value(nnz_l, (int)t);
+    const int64_t id_base = lane_value(incl, (int)t) - nnz;
     const int64_t pr = a->long_rows;
     const int64_t nb = max((int64_t)0, min(bpl, B - first));   // the lane's bags
-    int badf = lane == 0 && v[0] != 0;
-    int64_t cnt = 0;
+    int badf = (lane == 0 && v[0] != 0) | (o.hi < o.lo);
+    int haslong = 0;
 #pragma unroll
-    for (int j = 0; j < kScanMax; ++j) {
-      if (j < nb) {
-        badf |= v[j + 1] < v[j];
-        if ((int64_t)v[j + 1] - v[j] > pr) cnt += piece_count(id_base + v[j], id_base + v[j + 1], pr);
-      }
+    for (int j = 0; j < kScanMax; ++j) {   // v[j], v[j + 1]: the lane's own offsets for j < nb
+      const int in = j < nb;
+      badf |= in & (v[j + 1] < v[j]);
+      haslong |= in & ((int64_t)v[j + 1] - v[j] > pr);
     }
-    if (__any(badf)) {
-      if (i == 0 && lane == 0) latch(a, kStatusBadOffsets);
+    // one exit for both verdicts (no short circuit): a bad count or total is
+    // latched by the grid's first wave, a bad field by the field's first
+    const int gbad = __any(nnz_l < 0) | (int)(total != a->total_ids);
+    const int fbad = __any(badf);
+    if (gbad | fbad) {
+      if ((gbad ? w : i) == 0 && lane == 0) latch(a, kStatusBadOffsets);
       return;
     }
-    const int64_t pre = wave_exclusive(cnt, lane);
-    const int64_t pieces = uni(__shfl(pre + cnt, kWaveSize - 1, kWaveSize));
+    // pieces of the lane's long bags (rare: a 64-bit division each)
+    int64_t cnt = 0;
+    if (__any(haslong)) {
+#pragma unroll
+      for (int j = 0; j < kScanMax; ++j) {
+        if (j < nb && (int64_t)v[j + 1] - v[j] > pr) cnt += piece_count(id_base + v[j], id_base + v[j + 1], pr);
+      }
+    }
+    const int64_t pre = wave_incl_scan(cnt, lane) - cnt;
+    const int64_t pieces = lane_value(pre + cnt, kWaveSize - 1);
     const TableInfo ti = small_info(a, t, id_base, nnz);
     if (mine) bad = direct_wave<TOUT>(a, ti, t, b0, jlog, o, pr, lane);
     for (int64_t q = i; q < pieces; q += wpf) bad |= long_piece<TOUT>(a, ti, t, q, pre, cnt, first, nb, lane);
