@@ -199,10 +199,13 @@ def stage_sweep(args, dev) -> dict:
     from paper_2606_21101_amd import dpi
     from synth import configs, generate as G
 
+    from paper_2606_21101_amd.lookup import FusedLookup
+
     base = configs.get(5)
     T = base.onehot_fields
     reps, warm = 200, 20
     rows = []
+    tables = [G.make_table(base, t, dev) for t in range(base.num_tables)]
     for B in base.batches:
         cfg = base.with_batch(B)
         batch = G.make_batch(cfg, device="cpu")
@@ -284,6 +287,46 @@ def stage_sweep(args, dev) -> dict:
             res[name + "_us"] = float(np.median(ts) * 1e6)
         res["csr_fields"] = T_all
         res["csr_speedup"] = res["csr_per_field_us"] / res["csr_consolidated_us"]
+
+        # the whole step from the host CSR to the pooled block: dpi_stage_csr,
+        # then dpi_plan and dpi_lookup; against dpi_plan and dpi_lookup_csr
+        # (one copy and one kernel when the lookup is the batch's only launch)
+        fl = FusedLookup(tables, None, torch.float32, num_rows=G.table_sizes(cfg))
+        out = torch.empty((B, fl.total_dim), dtype=torch.float32, device=dev)
+        n_ids = len(ids64)
+
+        def step_staged():
+            dpi.dpi_stage_csr(packed, dpi.DPI_X_I64, T_all, B, n_ids, st2, o32, i32)
+            p = fl.plan(o32, B, n_ids)
+            fl.lookup(p, i32, o32, out)
+            torch.cuda.synchronize()
+            return out.clone()
+
+        def step_fused():
+            p = fl.plan(o32, B, n_ids)
+            dpi.dpi_lookup_csr(p, packed, dpi.DPI_X_I64, st2, fl._table_ptrs, None, o32, i32, out)
+            torch.cuda.synchronize()
+            return out.clone()
+
+        fused_ok = True
+        try:
+            a_out = step_staged()
+            b_out = step_fused()
+        except dpi.DpiError:
+            fused_ok = False          # a batch planned by its own launch: no fused path
+        if fused_ok:
+            if not torch.equal(a_out.view(torch.int32), b_out.view(torch.int32)):
+                raise SystemExit("dpi_lookup_csr output differs from staging then lookup")
+            for name, fn in (("step_staged", step_staged), ("step_fused", step_fused)):
+                for _ in range(warm):
+                    fn()
+                ts = []
+                for _ in range(reps):
+                    t0 = time.perf_counter()
+                    fn()
+                    ts.append(time.perf_counter() - t0)
+                res[name + "_us"] = float(np.median(ts) * 1e6)
+            res["step_fused_speedup"] = res["step_staged_us"] / res["step_fused_us"]
         rows.append(res)
     return {"metric": "input staging latency", "unit": "us", "reps": reps, "higher_is_better": False,
             "data": "synthetic (heterogeneous workload: its one-hot fields as a float matrix, all fields as "

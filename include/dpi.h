@@ -245,6 +245,33 @@ dpi_status dpi_stage_csr(const void* packed, int32_t x_dtype, int32_t num_fields
                          void* stream);
 
 /*
+ * Input consolidation folded into the lookup (§V breakdown): for a plan whose
+ * lookups take one launch (bag by bag, see dpi_plan and dpi_lookup), one
+ * asynchronous copy moves the packed host CSR that dpi_stage_csr takes
+ * (every field's offsets [T][B+1], then the fields' ids, as x_dtype) into
+ * `staging`, and the lookup kernel reads it there: each offset and id is
+ * converted as dpi_stage_csr converts it (not an integer in [0, 2^31): -1)
+ * when the kernel reads it, written to `offsets` / `ids` (the int32 arrays
+ * dpi_stage_csr would have produced), and pooled into `out` -- one copy and
+ * one kernel for the whole step, the same `out` bits as dpi_stage_csr then
+ * dpi_lookup.
+ *   plan:    built by dpi_plan with `offsets` as its offsets pointer (dpi_plan
+ *            reads nothing of them for such a plan, so they may still be
+ *            unwritten); batch sizes from the plan;
+ *   packed:  host, (T*(B+1) + total_ids) elements, ideally pinned, valid until
+ *            the copy has run;  staging: device, 16-byte aligned, that many
+ *            elements;  offsets, ids: device int32 outputs;
+ *   tables, pooling, out: as for dpi_lookup.
+ * With malformed offsets the converted arrays and `out` are unspecified (the
+ * status reports DPI_ERR_BAD_OFFSETS).  Query the status after the lookup.
+ * Errors: UNSUPPORTED (a plan that is not one launch per lookup: stage with
+ * dpi_stage_csr, then dpi_lookup), INVALID_ARG, MISALIGNED, HIP.
+ */
+dpi_status dpi_lookup_csr(dpi_plan_t plan, const void* packed, int32_t x_dtype, void* staging, size_t staging_bytes,
+                          const void* const* tables, const int32_t* pooling, int32_t* offsets, int32_t* ids, void* out,
+                          void* stream);
+
+/*
  * Breadth-first two-stream scheduling of the interaction modules (§IV-E,
  * Algorithm 2).  A model's explicit interaction module (e.g. a cross network)
  * and implicit one (an MLP) are independent, so each gets a stream; the host

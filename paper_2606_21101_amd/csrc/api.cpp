@@ -174,6 +174,7 @@ struct dpi_plan_s {
   bool looked_up;          // a lookup has been enqueued
   bool validated;          // the status query ran the planning launch (no lookup before it)
   SmallArgs small_args;
+  const int32_t* offsets_arg;   // the offsets pointer given to dpi_plan
   // the partition as the planning launch wrote it (what lookups read), copied
   // before the first export plans again; empty when that launch wrote none
   bool snap_valid;
@@ -371,6 +372,7 @@ static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, 
   plan->dmax = dmax;
   plan->total_d = total_d;
   plan->onehot = offsets == nullptr;
+  plan->offsets_arg = offsets;
   plan->uniform_class = uniform_class;
   plan->direct_jlog = direct_jlog(num_tables, batch, total_ids, row_class, offsets == nullptr, uniform_class,
                                   o.flags, waves_given);
@@ -488,9 +490,19 @@ static dpi_status plan_init(dpi_plan_s* plan, const dpi_table_meta* table_meta, 
   return DPI_OK;
 }
 
-// Enqueue the fused lookup of a plan; allocates nothing.
+// A staged packed CSR a one-launch lookup reads instead of int32 offsets and
+// ids (dpi_lookup_csr).
+struct StagedInput {
+  const void* data;
+  int32_t x_dtype;
+};
+
+// Enqueue the fused lookup of a plan; allocates nothing.  staged: read the
+// batch from a staged packed CSR and write the converted int32 arrays to
+// offsets / ids (one-launch plans only).
 static dpi_status lookup_enqueue(dpi_plan_s* plan, const void* const* tables, const int32_t* ids,
-                                 const int32_t* offsets, const int32_t* pooling, void* out, void* stream) {
+                                 const int32_t* offsets, const int32_t* pooling, void* out, void* stream,
+                                 const StagedInput* staged = nullptr) {
   if (!tables) return fail(DPI_ERR_INVALID_ARG, "tables is NULL");
   if ((offsets == nullptr) != plan->onehot)
     return fail(DPI_ERR_INVALID_ARG, "offsets must be NULL exactly when the plan was built without offsets");
@@ -515,6 +527,12 @@ static dpi_status lookup_enqueue(dpi_plan_s* plan, const void* const* tables, co
     sa.ids = ids;
     sa.offsets = offsets;
     sa.out = out;
+    if (staged) {
+      sa.staged = staged->data;
+      sa.staged_dtype = staged->x_dtype;
+      sa.offsets_out = const_cast<int32_t*>(offsets);
+      sa.ids_out = const_cast<int32_t*>(ids);
+    }
     const hipError_t e = launch_lookup_small(sa, reinterpret_cast<hipStream_t>(stream));
     if (e != hipSuccess) return hip_fail(e, "lookup launch");
     plan->looked_up = true;
@@ -642,6 +660,39 @@ dpi_status dpi_lookup(dpi_plan_t plan, const void* const* tables, const int32_t*
   if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
   if (!is_holder(plan->ws, plan->plan_id)) return superseded();
   return lookup_enqueue(plan, tables, ids, offsets, pooling, out, stream);
+}
+
+dpi_status dpi_lookup_csr(dpi_plan_t plan, const void* packed, int32_t x_dtype, void* staging, size_t staging_bytes,
+                          const void* const* tables, const int32_t* pooling, int32_t* offsets, int32_t* ids, void* out,
+                          void* stream) {
+  if (!plan) return fail(DPI_ERR_INVALID_ARG, "plan is NULL");
+  if (!is_holder(plan->ws, plan->plan_id)) return superseded();
+  if (!plan->one_launch || plan->onehot)
+    return fail(DPI_ERR_UNSUPPORTED, "dpi_lookup_csr needs a plan whose lookups take one launch (bag by bag, at "
+                                     "most 64 fields and 1024 bags per field): stage with dpi_stage_csr, then "
+                                     "call dpi_lookup");
+  if (!offsets || offsets != plan->offsets_arg)
+    return fail(DPI_ERR_INVALID_ARG, "offsets must be the pointer the plan was built with");
+  int esize = 0;
+  switch (x_dtype) {
+    case DPI_X_F32: esize = 4; break;
+    case DPI_X_I64: esize = 8; break;
+    case DPI_X_I32: esize = 4; break;
+    default: return fail(DPI_ERR_INVALID_ARG, "bad x_dtype");
+  }
+  const int64_t n = (int64_t)plan->T * (plan->B + 1) + plan->total_ids;
+  const size_t bytes = (size_t)n * (size_t)esize;
+  if (!packed || !staging) return fail(DPI_ERR_INVALID_ARG, "packed or staging is NULL");
+  if (staging_bytes < bytes) return fail(DPI_ERR_INVALID_ARG, "staging %zu bytes, need %zu", staging_bytes, bytes);
+  if (reinterpret_cast<uintptr_t>(staging) & 15) return fail(DPI_ERR_MISALIGNED, "staging not 16-byte aligned");
+  if (reinterpret_cast<uintptr_t>(packed) % esize) return fail(DPI_ERR_MISALIGNED, "packed not element-aligned");
+  if ((reinterpret_cast<uintptr_t>(offsets) | reinterpret_cast<uintptr_t>(ids)) & 3)
+    return fail(DPI_ERR_MISALIGNED, "offsets or ids not 4-byte aligned");
+  const hipError_t e = hipMemcpyAsync(staging, packed, bytes, hipMemcpyHostToDevice,
+                                      reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync");
+  const StagedInput st{staging, x_dtype};
+  return lookup_enqueue(plan, tables, ids, offsets, pooling, out, stream, &st);
 }
 
 dpi_status dpi_fm_second_order(const void* emb, int32_t emb_dtype, int64_t batch, int32_t num_fields,

@@ -183,6 +183,12 @@ struct SmallArgs {
   const int32_t* ids;
   const int32_t* offsets;               // device [T][B+1], or nullptr (one id per bag)
   void* out;
+  // a staged packed CSR read instead of offsets / ids (nullptr: none): its
+  // dpi_x_dtype, and where the converted int32 offsets and ids go
+  const void* staged;
+  int32_t staged_dtype;
+  int32_t* offsets_out;
+  int32_t* ids_out;
   uint64_t* status;                     // status word 0
   uint64_t* tickets;                    // [slots] arrival counters of long bags (tagged like the status)
   float* partial;                       // [slots][dmax] fp32 sums of long-bag pieces

@@ -212,26 +212,69 @@ __device__ __forceinline__ int64_t xcd_affine_block(int64_t g, int64_t n) {
   MACRO(0, 1) MACRO(1, 2) MACRO(2, 4) MACRO(3, 8) MACRO(4, 16) MACRO(5, 32) MACRO(6, 64)
 
 // ---------------------------------------------------------------------------
+// Where a kernel reads the batch's offsets and ids.  NativeIds: the int32
+// arrays dpi_plan and dpi_lookup take.  StagedIds<TX>: a staged copy of a
+// data loader's packed CSR (every field's offsets, then the fields' ids, as
+// float, int64 or int32), converted as it is read exactly as dpi_stage_csr
+// converts it, and written out as the int32 arrays it would have produced
+// (put_offset / put_id, called by the kernel once per element after its
+// pooling: on gfx9 loads and stores share one counter, and a store still in
+// flight makes every later wait for a load a wait for everything).
+// ---------------------------------------------------------------------------
+// a value that is not an integer in [0, 2^31) becomes -1
+__device__ __forceinline__ int32_t to_id(float v) {
+  return (v >= 0.f && v < 2147483648.f && v == truncf(v)) ? (int32_t)v : -1;
+}
+__device__ __forceinline__ int32_t to_id(int64_t v) { return (v >= 0 && v < ((int64_t)1 << 31)) ? (int32_t)v : -1; }
+__device__ __forceinline__ int32_t to_id(int32_t v) { return v >= 0 ? v : -1; }
+
+struct NativeIds {
+  const int32_t* __restrict__ off;
+  const int32_t* __restrict__ ids;
+  __device__ __forceinline__ int32_t offset(int64_t i) const { return off[i]; }
+  __device__ __forceinline__ int32_t id(int64_t i) const { return ids[i]; }
+  __device__ __forceinline__ void put_offset(int64_t, int32_t) const {}
+  __device__ __forceinline__ void put_id(int64_t, int32_t) const {}
+  static constexpr bool kWrites = false;
+};
+
+template <typename TX>
+struct StagedIds {
+  const TX* __restrict__ off;     // [T][B+1]
+  const TX* __restrict__ ids;     // [total_ids], right after the offsets
+  int32_t* __restrict__ off_out;
+  int32_t* __restrict__ ids_out;
+  __device__ __forceinline__ int32_t offset(int64_t i) const { return to_id(off[i]); }
+  __device__ __forceinline__ int32_t id(int64_t i) const { return to_id(ids[i]); }
+  __device__ __forceinline__ void put_offset(int64_t i, int32_t v) const { off_out[i] = v; }
+  __device__ __forceinline__ void put_id(int64_t i, int32_t v) const { ids_out[i] = v; }
+  static constexpr bool kWrites = true;
+};
+
+// ---------------------------------------------------------------------------
 // Fast path: row bytes a multiple of 16 and at most 1024; LPR lanes per row.
 // ---------------------------------------------------------------------------
 
-// Rows [r0, r1) of field t pooled by all slots of the wave; on return every
-// slot holds the total for its lane's columns.
-template <typename TIN, int LPR, bool BUF, typename KX>
-__device__ __forceinline__ void pool_rows_coop(KX a, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1,
-                                               int lane, float* acc, int& bad) {
+// Rows [r0, r1) of field t pooled by all slots of the wave, its ids read
+// from `src`; on return every slot holds the total for its lane's columns.
+template <typename TIN, int LPR, bool BUF, typename KX, typename S>
+__device__ __forceinline__ void pool_rows_src(KX a, const S& src, const TableInfo& ti, int64_t t, int64_t r0,
+                                              int64_t r1, int lane, float* acc, int& bad) {
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
   const int g = lane / LPR, k = lane % LPR;
   const RowReader<BUF> rows(a->tables[t], ti, k);
-  const int32_t* __restrict__ ids = a->ids + ti.id_base;
+  const int64_t ib = ti.id_base;
   const uint32_t nrows = id_limit(ti);
   const bool col = k * EPL < ti.dim;
 #pragma unroll
   for (int i = 0; i < EPL; ++i) acc[i] = 0.f;
   int32_t idn[kUnroll];
 #pragma unroll
-  for (int u = 0; u < kUnroll; ++u) idn[u] = (r0 + g + u * G < r1) ? ids[r0 + g + u * G] : -1;
+  for (int u = 0; u < kUnroll; ++u) {
+    const int64_t q = r0 + g + u * G;
+    idn[u] = q < r1 ? src.id(ib + q) : -1;
+  }
   for (int64_t r = r0 + g; r < r1; r += (int64_t)G * kUnroll) {
     raw16_t raw[kUnroll];
 #pragma unroll
@@ -244,7 +287,10 @@ __device__ __forceinline__ void pool_rows_coop(KX a, const TableInfo& ti, int64_
     }
     const int64_t rn = r + (int64_t)G * kUnroll;
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) idn[u] = (rn + u * G < r1) ? ids[rn + u * G] : -1;
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t q = rn + u * G;
+      idn[u] = q < r1 ? src.id(ib + q) : -1;
+    }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
   }
@@ -253,6 +299,13 @@ __device__ __forceinline__ void pool_rows_coop(KX a, const TableInfo& ti, int64_
 #pragma unroll
     for (int i = 0; i < EPL; ++i) acc[i] += __shfl_xor(acc[i], m, kWaveSize);
   }
+}
+
+// The same with the ids of the kernel arguments.
+template <typename TIN, int LPR, bool BUF, typename KX>
+__device__ __forceinline__ void pool_rows_coop(KX a, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1,
+                                               int lane, float* acc, int& bad) {
+  pool_rows_src<TIN, LPR, BUF>(a, NativeIds{a->offsets, a->ids}, ti, t, r0, r1, lane, acc, bad);
 }
 
 // ---------------------------------------------------------------------------
@@ -270,8 +323,8 @@ struct DirectOffsets {
   int32_t lo, hi;
 };
 
-template <typename TIN, typename TOUT, int LPR, bool BUF, typename KX>
-__device__ __forceinline__ int direct_bags(KX a, const TableInfo& ti, int64_t t, int64_t b0, int jlog,
+template <typename TIN, typename TOUT, int LPR, bool BUF, typename KX, typename S>
+__device__ __forceinline__ int direct_bags(KX a, const S& src, const TableInfo& ti, int64_t t, int64_t b0, int jlog,
                                            DirectOffsets o, int64_t long_rows, int lane) {
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
@@ -291,7 +344,7 @@ __device__ __forceinline__ int direct_bags(KX a, const TableInfo& ti, int64_t t,
   const bool skip = e - s > long_rows;
   if (skip) e = s;
   const RowReader<BUF> rows(a->tables[t], ti, k);
-  const int32_t* __restrict__ ids = a->ids + ti.id_base;
+  const int64_t ib = ti.id_base;
   const uint32_t nrows = id_limit(ti);
   const bool col = k * EPL < ti.dim;
   float acc[EPL];
@@ -303,7 +356,7 @@ __device__ __forceinline__ int direct_bags(KX a, const TableInfo& ti, int64_t t,
 #pragma unroll
   for (int u = 0; u < kUnroll; ++u) {
     const int64_t r = s + p + (int64_t)u * P;
-    idn[u] = r < e ? ids[r] : -1;
+    idn[u] = r < e ? src.id(ib + r) : -1;
   }
   for (int64_t r = s + p; r < e; r += stride) {
     raw16_t raw[kUnroll];
@@ -319,7 +372,7 @@ __device__ __forceinline__ int direct_bags(KX a, const TableInfo& ti, int64_t t,
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t q = rn + (int64_t)u * P;
-      idn[u] = q < e ? ids[q] : -1;
+      idn[u] = q < e ? src.id(ib + q) : -1;
     }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) accumulate<TIN, EPL>(acc, raw[u]);
@@ -340,18 +393,18 @@ __device__ __forceinline__ int direct_bags(KX a, const TableInfo& ti, int64_t t,
   return bad;
 }
 
-template <typename TOUT, typename KX>
-__device__ __forceinline__ int direct_wave(KX a, const TableInfo& ti, int64_t t, int64_t b0, int jlog,
+template <typename TOUT, typename KX, typename S>
+__device__ __forceinline__ int direct_wave(KX a, const S& src, const TableInfo& ti, int64_t t, int64_t b0, int jlog,
                                            DirectOffsets o, int64_t long_rows, int lane) {
   const bool buf = use_buffer(ti), f16 = (ti.flags & kTiF16) != 0;
   switch ((ti.flags >> kTiLprShift) & 7) {
 #define DPI_CASE(L, LPR)                                                                                   \
   case L:                                                                                                  \
     if (f16)                                                                                               \
-      return buf ? direct_bags<_Float16, TOUT, LPR, true>(a, ti, t, b0, jlog, o, long_rows, lane)          \
-                 : direct_bags<_Float16, TOUT, LPR, false>(a, ti, t, b0, jlog, o, long_rows, lane);        \
-    return buf ? direct_bags<float, TOUT, LPR, true>(a, ti, t, b0, jlog, o, long_rows, lane)               \
-               : direct_bags<float, TOUT, LPR, false>(a, ti, t, b0, jlog, o, long_rows, lane);
+      return buf ? direct_bags<_Float16, TOUT, LPR, true>(a, src, ti, t, b0, jlog, o, long_rows, lane)     \
+                 : direct_bags<_Float16, TOUT, LPR, false>(a, src, ti, t, b0, jlog, o, long_rows, lane);   \
+    return buf ? direct_bags<float, TOUT, LPR, true>(a, src, ti, t, b0, jlog, o, long_rows, lane)          \
+               : direct_bags<float, TOUT, LPR, false>(a, src, ti, t, b0, jlog, o, long_rows, lane);
     DPI_FOR_LPR(DPI_CASE)
 #undef DPI_CASE
     default:

@@ -664,7 +664,7 @@ void lookup_direct_kernel(const LookupArgs args) {
     return;
   }
   if (!mine) return;
-  const int bad = direct_wave<TOUT>(a, ti, t, b0, jlog, o, INT64_MAX, lane);
+  const int bad = direct_wave<TOUT>(a, NativeIds{a->offsets, a->ids}, ti, t, b0, jlog, o, INT64_MAX, lane);
   if (__any(bad) && lane == 0)
     __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

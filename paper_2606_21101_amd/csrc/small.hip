@@ -92,13 +92,13 @@ __device__ __forceinline__ int64_t piece_count(int64_t gs, int64_t ge, int64_t p
 
 // Rows [r0, r1) of field t (positions in the field's id list) pooled by the
 // whole wave; the lanes of slot 0 write the fp32 sums of their columns to dst.
-template <typename TIN, int LPR, bool BUF>
-__device__ __forceinline__ int piece_fast(KS a, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1, float* dst,
-                                          int lane) {
+template <typename TIN, int LPR, bool BUF, typename S>
+__device__ __forceinline__ int piece_fast(KS a, const S& src, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1,
+                                          float* dst, int lane) {
   constexpr int EPL = In<TIN>::EPL;
   float acc[EPL];
   int bad = 0;
-  pool_rows_coop<TIN, LPR, BUF>(a, ti, t, r0, r1, lane, acc, bad);
+  pool_rows_src<TIN, LPR, BUF>(a, src, ti, t, r0, r1, lane, acc, bad);
   const int g = lane / LPR, k = lane % LPR;
   if (g == 0 && k * EPL < ti.dim) {
 #pragma unroll
@@ -107,17 +107,18 @@ __device__ __forceinline__ int piece_fast(KS a, const TableInfo& ti, int64_t t, 
   return bad;
 }
 
-__device__ __forceinline__ int piece_wave(KS a, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1, float* dst,
-                                          int lane) {
+template <typename S>
+__device__ __forceinline__ int piece_wave(KS a, const S& src, const TableInfo& ti, int64_t t, int64_t r0, int64_t r1,
+                                          float* dst, int lane) {
   const bool buf = use_buffer(ti), f16 = (ti.flags & kTiF16) != 0;
   switch ((ti.flags >> kTiLprShift) & 7) {
 #define DPI_CASE(L, LPR)                                                                     \
   case L:                                                                                    \
     if (f16)                                                                                 \
-      return buf ? piece_fast<_Float16, LPR, true>(a, ti, t, r0, r1, dst, lane)              \
-                 : piece_fast<_Float16, LPR, false>(a, ti, t, r0, r1, dst, lane);            \
-    return buf ? piece_fast<float, LPR, true>(a, ti, t, r0, r1, dst, lane)                   \
-               : piece_fast<float, LPR, false>(a, ti, t, r0, r1, dst, lane);
+      return buf ? piece_fast<_Float16, LPR, true>(a, src, ti, t, r0, r1, dst, lane)         \
+                 : piece_fast<_Float16, LPR, false>(a, src, ti, t, r0, r1, dst, lane);       \
+    return buf ? piece_fast<float, LPR, true>(a, src, ti, t, r0, r1, dst, lane)              \
+               : piece_fast<float, LPR, false>(a, src, ti, t, r0, r1, dst, lane);
     DPI_FOR_LPR(DPI_CASE)
 #undef DPI_CASE
     default:
@@ -128,9 +129,9 @@ __device__ __forceinline__ int piece_wave(KS a, const TableInfo& ti, int64_t t, 
 // Piece q of field t's long bags.  Lane l's bags [first, first + nb) hold
 // pieces [pre, pre + cnt) of the field (in bag order, each bag's pieces in
 // window order).  Out of line: the rare path keeps its registers to itself.
-template <typename TOUT>
-__device__ __attribute__((noinline)) int long_piece(KS a, const TableInfo& ti, int64_t t, int64_t q, int64_t pre,
-                                                    int64_t cnt, int64_t first, int64_t nb, int lane) {
+template <typename TOUT, typename S>
+__device__ __attribute__((noinline)) int long_piece(KS a, const S& src, const TableInfo& ti, int64_t t, int64_t q,
+                                                    int64_t pre, int64_t cnt, int64_t first, int64_t nb, int lane) {
   const int64_t pr = a->long_rows;
   const uint64_t m = __ballot(cnt > 0 && pre <= q && q < pre + cnt);
   if (m == 0) return 0;   // q < the field's piece count, so some lane holds it
@@ -138,10 +139,10 @@ __device__ __attribute__((noinline)) int long_piece(KS a, const TableInfo& ti, i
   int64_t bag = 0, rank = 0, lo = 0, hi = 0;
   if (lane == owner) {
     // the owner's offsets again (one round trip), then a walk in registers
-    const int32_t* row = a->offsets + t * (a->B + 1) + first;
+    const int64_t row = t * (a->B + 1) + first;
     int32_t u[kScanMax + 1];
 #pragma unroll
-    for (int j = 0; j <= kScanMax; ++j) u[j] = row[min((int64_t)j, nb)];
+    for (int j = 0; j <= kScanMax; ++j) u[j] = src.offset(row + min((int64_t)j, nb));
     int64_t r = q - pre;
     bool found = false;
 #pragma unroll
@@ -178,7 +179,7 @@ __device__ __attribute__((noinline)) int long_piece(KS a, const TableInfo& ti, i
   if (2 * (wf + n - 1) >= a->slots) return 0;   // not for offsets that passed the checks
   const int64_t r0 = (gs > win * pr ? gs : win * pr) - ti.id_base;
   const int64_t r1 = (ge < (win + 1) * pr ? ge : (win + 1) * pr) - ti.id_base;
-  const int bad = piece_wave(a, ti, t, r0, r1, a->partial + slot * a->dmax, lane);
+  const int bad = piece_wave(a, src, ti, t, r0, r1, a->partial + slot * a->dmax, lane);
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   int64_t arrived = 0;
   if (lane == 0) arrived = ticket_arrive(a->tickets + head, a->tag);
@@ -201,12 +202,35 @@ __device__ __attribute__((noinline)) int long_piece(KS a, const TableInfo& ti, i
   return bad;
 }
 
-// four waves per SIMD, as the two-launch bag-by-bag kernel
-template <typename TOUT>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4)))
-void lookup_small_direct_kernel(const SmallArgs args) {
-  (void)args;
-  const KS a = (KS)__builtin_amdgcn_kernarg_segment_ptr();
+// Field t's converted offsets [row, row + B] (a staged input; B <=
+// kSmallMaxBatch): every load first, then every store (one round trip).
+template <typename S>
+__device__ __forceinline__ void write_offsets(const S& src, int64_t row, int64_t B, int lane) {
+  int32_t v[kScanMax + 1];
+#pragma unroll
+  for (int j = 0; j <= kScanMax; ++j) v[j] = src.offset(row + min((int64_t)lane + j * kWaveSize, B));
+#pragma unroll
+  for (int j = 0; j <= kScanMax; ++j)
+    if (lane + j * kWaveSize <= B) src.put_offset(row + lane + j * kWaveSize, v[j]);
+}
+
+// Converted ids [r_lo, r_hi) of the flat id list, 8 per lane per round trip.
+template <typename S>
+__device__ __forceinline__ void write_ids(const S& src, int64_t r_lo, int64_t r_hi, int lane) {
+  constexpr int kPer = 8;
+  for (int64_t r0 = r_lo; r0 < r_hi; r0 += (int64_t)kPer * kWaveSize) {
+    int32_t v[kPer];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) v[u] = src.id(min(r0 + lane + u * kWaveSize, r_hi - 1));
+#pragma unroll
+    for (int u = 0; u < kPer; ++u)
+      if (r0 + lane + u * kWaveSize < r_hi) src.put_id(r0 + lane + u * kWaveSize, v[u]);
+  }
+}
+
+// The bag-by-bag lookup, the offsets and ids read from `src`.
+template <typename TOUT, typename S>
+__device__ __forceinline__ void small_direct(KS a, const S& src, bool has_offsets) {
   const int lane = threadIdx.x & (kWaveSize - 1);
   const int64_t w = (int64_t)blockIdx.x * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   const int64_t wpf = a->direct_wpf;
@@ -220,10 +244,9 @@ void lookup_small_direct_kernel(const SmallArgs args) {
   const int64_t B = a->B;
   const int64_t b0 = i << jlog;
   const bool mine = b0 < B;
-  const int32_t* const offs = a->offsets;
   int bad = 0;
   DirectOffsets o{0, 0};
-  if (!offs) {
+  if (!has_offsets) {
     if (mine && lane < (1 << jlog)) {
       const int64_t bl = min(b0 + lane, B - 1);   // bags past the batch end are inactive
       o.lo = (int32_t)bl;
@@ -231,7 +254,7 @@ void lookup_small_direct_kernel(const SmallArgs args) {
     }
     if (mine) {
       const TableInfo ti = small_info(a, t, t * B, B);
-      bad = direct_wave<TOUT>(a, ti, t, b0, jlog, o, INT64_MAX, lane);
+      bad = direct_wave<TOUT>(a, src, ti, t, b0, jlog, o, INT64_MAX, lane);
     }
   } else {
     // the wave's bag offsets, every field's id count and all of this field's
@@ -239,15 +262,15 @@ void lookup_small_direct_kernel(const SmallArgs args) {
     // every lane loads from a clamped, valid index and the values it does not
     // need are dropped afterwards (a load under a branch makes the compiler
     // wait for it before the branch joins, one round trip per branch)
-    const int32_t* const row = offs + t * (B + 1);
+    const int64_t row = t * (B + 1);
     const int64_t bl = min(b0 + lane, B - 1);
-    const int32_t lo = row[bl], hi = row[bl + 1];
-    const int32_t nz = offs[(int64_t)min(lane, T - 1) * (B + 1) + B];
+    const int32_t lo = src.offset(row + bl), hi = src.offset(row + bl + 1);
+    const int32_t nz = src.offset((int64_t)min(lane, T - 1) * (B + 1) + B);
     const int64_t bpl = (B + kWaveSize - 1) / kWaveSize;
     const int64_t first = lane * bpl;
     int32_t v[kScanMax + 1];
 #pragma unroll
-    for (int j = 0; j <= kScanMax; ++j) v[j] = row[min(first + j, B)];
+    for (int j = 0; j <= kScanMax; ++j) v[j] = src.offset(row + min(first + j, B));
     if (mine && lane < (1 << jlog)) {
       o.lo = lo;
       o.hi = hi;
@@ -275,6 +298,7 @@ void lookup_small_direct_kernel(const SmallArgs args) {
     const int gbad = __any(nnz_l < 0) | (int)(total != a->total_ids);
     const int fbad = __any(badf);
     if (gbad | fbad) {
+      if (S::kWrites && i == 0) write_offsets(src, row, B, lane);
       if ((gbad ? w : i) == 0 && lane == 0) latch(a, kStatusBadOffsets);
       return;
     }
@@ -289,10 +313,43 @@ void lookup_small_direct_kernel(const SmallArgs args) {
     const int64_t pre = wave_incl_scan(cnt, lane) - cnt;
     const int64_t pieces = lane_value(pre + cnt, kWaveSize - 1);
     const TableInfo ti = small_info(a, t, id_base, nnz);
-    if (mine) bad = direct_wave<TOUT>(a, ti, t, b0, jlog, o, pr, lane);
-    for (int64_t q = i; q < pieces; q += wpf) bad |= long_piece<TOUT>(a, ti, t, q, pre, cnt, first, nb, lane);
+    if (mine) bad = direct_wave<TOUT>(a, src, ti, t, b0, jlog, o, pr, lane);
+    for (int64_t q = i; q < pieces; q += wpf)
+      bad |= long_piece<TOUT>(a, src, ti, t, q, pre, cnt, first, nb, lane);
+    if (S::kWrites) {
+      // the converted arrays, after the pooling: the field's offsets by its
+      // first wave, the ids of the wave's own bags (long ones included) by
+      // the wave
+      if (i == 0) write_offsets(src, row, B, lane);
+      if (mine) {
+        const int64_t nbags = min((int64_t)1 << jlog, B - b0);
+        const int64_t r_lo = min(max((int64_t)__shfl(o.lo, 0, kWaveSize), (int64_t)0), nnz);
+        const int64_t r_hi = min(max((int64_t)__shfl(o.hi, (int)nbags - 1, kWaveSize), r_lo), nnz);
+        write_ids(src, id_base + r_lo, id_base + r_hi, lane);
+      }
+    }
   }
   if (__any(bad) && lane == 0) latch(a, kStatusBadId);
+}
+
+// four waves per SIMD, as the two-launch bag-by-bag kernel
+template <typename TOUT>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void lookup_small_direct_kernel(const SmallArgs args) {
+  (void)args;
+  const KS a = (KS)__builtin_amdgcn_kernarg_segment_ptr();
+  small_direct<TOUT>(a, NativeIds{a->offsets, a->ids}, a->offsets != nullptr);
+}
+
+// The same from a staged packed CSR of element type TX (dpi_lookup_csr): the
+// input conversion of dpi_stage_csr happens as the lookup reads its input.
+template <typename TOUT, typename TX>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(4)))
+void lookup_small_staged_kernel(const SmallArgs args) {
+  (void)args;
+  const KS a = (KS)__builtin_amdgcn_kernarg_segment_ptr();
+  const TX* raw = reinterpret_cast<const TX*>(a->staged);
+  small_direct<TOUT>(a, StagedIds<TX>{raw, raw + (int64_t)a->T * (a->B + 1), a->offsets_out, a->ids_out}, true);
 }
 
 // one-hot batches of one row class
@@ -353,10 +410,26 @@ hipError_t launch_lookup_small(const SmallArgs& a, hipStream_t s) {
   const int64_t waves = a.direct_wpf * a.T;
   const int64_t blocks = (waves + kWavesPerBlock - 1) / kWavesPerBlock;
   if (blocks <= 0) return hipSuccess;
+  const dim3 grid((unsigned)blocks), block(kBlockThreads);
+  if (a.staged) {
+#define DPI_STAGED(TX)                                                                                 \
+  if (a.out_f16)                                                                                       \
+    hipLaunchKernelGGL((lookup_small_staged_kernel<_Float16, TX>), grid, block, 0, s, a);              \
+  else                                                                                                 \
+    hipLaunchKernelGGL((lookup_small_staged_kernel<float, TX>), grid, block, 0, s, a);
+    switch (a.staged_dtype) {
+      case DPI_X_F32: DPI_STAGED(float) break;
+      case DPI_X_I64: DPI_STAGED(int64_t) break;
+      case DPI_X_I32: DPI_STAGED(int32_t) break;
+      default: return hipErrorInvalidValue;
+    }
+#undef DPI_STAGED
+    return hipGetLastError();
+  }
   if (a.out_f16)
-    hipLaunchKernelGGL(lookup_small_direct_kernel<_Float16>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+    hipLaunchKernelGGL(lookup_small_direct_kernel<_Float16>, grid, block, 0, s, a);
   else
-    hipLaunchKernelGGL(lookup_small_direct_kernel<float>, dim3((unsigned)blocks), dim3(kBlockThreads), 0, s, a);
+    hipLaunchKernelGGL(lookup_small_direct_kernel<float>, grid, block, 0, s, a);
   return hipGetLastError();
 }
 

@@ -9,19 +9,12 @@
 // lookup (the transpose of Algorithm 1's sample-major id matrix).
 // 64 x 64 tiles through LDS: reads along a sample's fields and writes along a
 // field's samples are both contiguous.
-#include "dpi_internal.h"
+#include "gather.h"   // to_id: the conversion the one-launch lookup applies to a staged CSR too
 
 namespace dpi {
 namespace {
 
 constexpr int kTile = 64;
-
-__device__ __forceinline__ int32_t to_id(float v) {
-  // an integer-valued float in [0, 2^31)
-  return (v >= 0.f && v < 2147483648.f && v == truncf(v)) ? (int32_t)v : -1;
-}
-__device__ __forceinline__ int32_t to_id(int64_t v) { return (v >= 0 && v < ((int64_t)1 << 31)) ? (int32_t)v : -1; }
-__device__ __forceinline__ int32_t to_id(int32_t v) { return v >= 0 ? v : -1; }
 
 template <typename TX>
 __global__ __launch_bounds__(kTile * 4) void stage_onehot_kernel(const StageArgs args) {

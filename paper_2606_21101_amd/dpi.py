@@ -114,6 +114,8 @@ def load() -> ctypes.CDLL:
     lib.dpi_stage_onehot.argtypes = [vp, i32, i64, i32, i64, vp, sz, vp, vp]
     lib.dpi_stage_csr.restype = ctypes.c_int
     lib.dpi_stage_csr.argtypes = [vp, i32, i32, i64, i64, vp, sz, vp, vp, vp]
+    lib.dpi_lookup_csr.restype = ctypes.c_int
+    lib.dpi_lookup_csr.argtypes = [vp, vp, i32, vp, sz, ctypes.POINTER(vp), ctypes.POINTER(i32), vp, vp, vp, vp]
     lib.dpi_breadth_first_order.restype = ctypes.c_int
     lib.dpi_breadth_first_order.argtypes = [i32, i32, ctypes.POINTER(i32)]
     lib.dpi_launch_two_streams.restype = ctypes.c_int
@@ -391,6 +393,23 @@ def dpi_stage_csr(packed, x_dtype: int, num_fields: int, batch: int, total_ids: 
         staging_bytes = int(staging.numel() * staging.element_size())
     _check(load().dpi_stage_csr(_ptr(packed), x_dtype, num_fields, batch, total_ids, _ptr(staging), staging_bytes,
                                 _ptr(offsets), _ptr(ids), _stream(stream)))
+
+
+def dpi_lookup_csr(plan: Plan, packed, x_dtype: int, staging, tables, pooling: Optional[Sequence[int]], offsets, ids,
+                   out, staging_bytes: Optional[int] = None, stream=None) -> None:
+    """One copy of the packed host CSR into `staging` and one lookup kernel that
+    converts it as it reads it (writing the int32 offsets and ids) and pools; for
+    plans whose lookups take one launch (see include/dpi.h)."""
+    lib = load()
+    T = plan.num_tables
+    if staging_bytes is None:
+        staging_bytes = int(staging.numel() * staging.element_size())
+    ptrs = tables if isinstance(tables, ctypes.Array) else table_array(tables)
+    pool = pooling if (pooling is None or isinstance(pooling, ctypes.Array)) else pooling_array(pooling)
+    if len(ptrs) != T or (pool is not None and len(pool) != T):
+        raise DpiError(DPI_ERR_INVALID_ARG, "tables / pooling must have one entry per field")
+    _check(lib.dpi_lookup_csr(ctypes.c_void_p(plan.handle), _ptr(packed), x_dtype, _ptr(staging), staging_bytes, ptrs,
+                              pool, _ptr(offsets), _ptr(ids), _ptr(out), _stream(stream)))
 
 
 def dpi_plan_destroy(plan: Plan) -> None:

@@ -32,6 +32,11 @@ def test_version_and_strings():
     assert "unknown" in dpi.dpi_status_str(99)
 
 
+def _gpu_present():
+    import torch
+    return torch.cuda.device_count() > 0
+
+
 def _meta(dims=(16, 16), dtypes=(0, 0), rows=(10, 10)):
     return dpi.make_meta(rows, dims, dtypes)
 
@@ -178,3 +183,59 @@ def test_binding_constants_mirror_the_header():
         assert getattr(dpi, name) == int(value), name
     for name, bit in shifts.items():
         assert getattr(dpi, name) == 1 << int(bit), name
+
+
+def test_one_launch_plans_enqueue_nothing():
+    """Bag-by-bag and one-hot batches of at most 64 fields (and 1024 bags per
+    field with offsets) plan on the host alone: dpi_plan succeeds with no
+    device present, while a plan that needs its planning launch reports the
+    HIP error of that launch."""
+    if _gpu_present():
+        pytest.skip("needs a host without a GPU")
+    lib = dpi.load()
+    m = _meta()
+    for offsets, B, total, opts in ((0x10000, 4, 8, dpi.make_opts()), (None, 4, 8, dpi.make_opts()),
+                                    (0x10000, 1024, 3000, dpi.make_opts()), (None, 5000, 10000, dpi.make_opts())):
+        out = ctypes.c_void_p()
+        assert lib.dpi_plan(m, 2, offsets, B, total, ctypes.byref(opts), 0x20000, 1 << 30, None,
+                            ctypes.byref(out)) == dpi.DPI_OK, dpi.dpi_last_error()
+        lib.dpi_plan_destroy(out)
+    for offsets, B, total, opts in ((0x10000, 4, 8, dpi.make_opts(num_waves=64)),     # explicit wave count
+                                    (0x10000, 1025, 3000, dpi.make_opts())):           # more than 1024 bags
+        out = ctypes.c_void_p()
+        assert lib.dpi_plan(m, 2, offsets, B, total, ctypes.byref(opts), 0x20000, 1 << 30, None,
+                            ctypes.byref(out)) == dpi.DPI_ERR_HIP
+    wide = _meta(dims=[16] * 65, dtypes=[0] * 65, rows=[10] * 65)
+    out = ctypes.c_void_p()
+    assert lib.dpi_plan(wide, 65, 0x10000, 4, 8, ctypes.byref(dpi.make_opts()), 0x20000, 1 << 30, None,
+                        ctypes.byref(out)) == dpi.DPI_ERR_HIP                          # 65 fields
+
+
+def test_lookup_csr_host_validation():
+    lib = dpi.load()
+    vp = 0x10000
+    tabs = (ctypes.c_void_p * 2)(0x30000, 0x30000)
+    assert lib.dpi_lookup_csr(None, vp, dpi.DPI_X_I64, 0x40000, 1 << 20, tabs, None, vp, vp, 0x50000,
+                              None) == dpi.DPI_ERR_INVALID_ARG
+    if _gpu_present():
+        return
+    out = ctypes.c_void_p()
+    assert lib.dpi_plan(_meta(), 2, vp, 4, 8, ctypes.byref(dpi.make_opts()), 0x20000, 1 << 30, None,
+                        ctypes.byref(out)) == dpi.DPI_OK
+    args = dict(packed=vp, x=dpi.DPI_X_I64, staging=0x40000, sbytes=1 << 20, offsets=vp)
+
+    def call(**kw):
+        a = {**args, **kw}
+        return lib.dpi_lookup_csr(out, a["packed"], a["x"], a["staging"], a["sbytes"], tabs, None, a["offsets"], vp,
+                                  0x50000, None)
+    assert call(offsets=vp + 4) == dpi.DPI_ERR_INVALID_ARG       # not the plan's offsets
+    assert call(x=7) == dpi.DPI_ERR_INVALID_ARG
+    assert call(sbytes=8 * 17) == dpi.DPI_ERR_INVALID_ARG        # 2 * 5 offsets + 8 ids = 18 elements
+    assert call(staging=0x40008) == dpi.DPI_ERR_MISALIGNED
+    assert call(packed=vp + 4) == dpi.DPI_ERR_MISALIGNED
+    later = ctypes.c_void_p()
+    assert lib.dpi_plan(_meta(), 2, vp, 4, 8, ctypes.byref(dpi.make_opts()), 0x20000, 1 << 30, None,
+                        ctypes.byref(later)) == dpi.DPI_OK
+    assert call() == dpi.DPI_ERR_INVALID_ARG and "later plan" in dpi.dpi_last_error()
+    lib.dpi_plan_destroy(out)
+    lib.dpi_plan_destroy(later)

@@ -115,3 +115,81 @@ def test_stage_csr_then_lookup_equals_direct():
     a = fl(torch.from_numpy(got_i).cuda(), torch.from_numpy(got_o).cuda(), B)
     b = fl(torch.from_numpy(ids.astype(np.int32)).cuda(), torch.from_numpy(offs.astype(np.int32)).cuda(), B)
     assert torch.equal(a, b)
+
+
+# --- the staged CSR read by the lookup itself (dpi_lookup_csr) --------------
+
+def csr_problem(rng, B, dims, dtypes, rows=400, long_bag=0):
+    T = len(dims)
+    tables = [torch.from_numpy((rng.standard_normal((rows, d)) * 0.01).astype(np.float16 if dt else np.float32))
+              .cuda() for d, dt in zip(dims, dtypes)]
+    lens = rng.integers(0, 25, size=(T, B))
+    if long_bag:
+        lens[T // 2, B // 2] = long_bag
+    offs = np.zeros((T, B + 1), np.int64)
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    n_ids = int(offs[:, -1].sum())
+    ids = rng.integers(0, rows, size=n_ids)
+    return tables, offs, ids, n_ids
+
+
+def lookup_csr(tables, pool, packed_np, x_dtype, B, n_ids, out_dtype=torch.float32):
+    """dpi_plan over not-yet-written offsets, then dpi_lookup_csr: returns the
+    output, the converted offsets and ids, and the status."""
+    T = len(tables)
+    host = torch.empty(len(packed_np), dtype=XT[x_dtype][1], pin_memory=True)
+    host.copy_(torch.from_numpy(packed_np))
+    staging = torch.empty(max(16, len(packed_np) * host.element_size()), dtype=torch.uint8, device="cuda")
+    offs = torch.full((T, B + 1), 777, dtype=torch.int32, device="cuda")
+    ids = torch.full((max(1, n_ids),), 777, dtype=torch.int32, device="cuda")
+    fl = FusedLookup(tables, pool, out_dtype)
+    plan = fl.plan(offs, B, n_ids)
+    out = torch.full((B, fl.total_dim), float("nan"), dtype=out_dtype, device="cuda")
+    dpi.dpi_lookup_csr(plan, host, x_dtype, staging, fl._table_ptrs, fl._pool, offs, ids, out)
+    st = dpi.dpi_plan_sync_status(plan)
+    return out, offs.cpu().numpy(), ids[:n_ids].cpu().numpy(), st
+
+
+@pytest.mark.parametrize("x_dtype", [dpi.DPI_X_F32, dpi.DPI_X_I64, dpi.DPI_X_I32])
+@pytest.mark.parametrize("B,long_bag", [(1, 0), (16, 0), (128, 0), (512, 0), (37, 700), (1024, 3000)])
+def test_lookup_csr_equals_stage_then_lookup(x_dtype, B, long_bag):
+    """One copy and one kernel: the converted offsets and ids bit for bit as
+    the oracle converts them, and the output bit for bit as dpi_stage_csr then
+    dpi_lookup gives it (the same kernel arithmetic), long bags included."""
+    rng = np.random.default_rng(B * 10 + x_dtype + long_bag)
+    dims, dtypes = [8, 16, 32, 64, 16, 8], [0, 0, 0, 0, 1, 1]
+    tables, offs, ids, n_ids = csr_problem(rng, B, dims, dtypes, long_bag=long_bag)
+    packed = np.concatenate([offs.reshape(-1), ids]).astype(XT[x_dtype][0])
+    pool = [0, 1, 0, 1, 0, 1]
+    print(f"  lookup_csr x_dtype={x_dtype} B={B} long={long_bag}", flush=True)
+    out, got_o, got_i, st = lookup_csr(tables, pool, packed, x_dtype, B, n_ids)
+    assert st == dpi.DPI_OK
+    want_o, want_i = oracle.stage_csr(packed, len(dims), B, n_ids)
+    assert np.array_equal(got_o, want_o) and np.array_equal(got_i, want_i)
+    so, si = stage_csr(packed, x_dtype, len(dims), B, n_ids)
+    ref = FusedLookup(tables, pool)(torch.from_numpy(si).cuda(), torch.from_numpy(so).cuda(), B)
+    assert torch.equal(out.view(torch.int32), ref.view(torch.int32))
+
+
+def test_lookup_csr_reports_bad_ids_and_offsets():
+    rng = np.random.default_rng(5)
+    B = 40
+    tables, offs, ids, n_ids = csr_problem(rng, B, [16, 32], [0, 1])
+    packed = np.concatenate([offs.reshape(-1), ids]).astype(np.float64)
+    packed[2 * (B + 1) + 3] = 2.5                      # an id that is not an integer
+    out, _, got_i, st = lookup_csr(tables, None, packed.astype(np.float32), dpi.DPI_X_F32, B, n_ids)
+    assert st == dpi.DPI_ERR_BAD_ID and got_i[3] == -1
+    bad = np.concatenate([offs.reshape(-1), ids]).astype(np.int64)
+    bad[5] = -3                                        # an offset that becomes -1
+    _, got_o, _, st = lookup_csr(tables, None, bad, dpi.DPI_X_I64, B, n_ids)
+    assert st == dpi.DPI_ERR_BAD_OFFSETS and got_o[0, 5] == -1
+
+
+def test_lookup_csr_needs_a_one_launch_plan():
+    rng = np.random.default_rng(6)
+    B = 2000                                           # more than 1024 bags per field: planned by its own launch
+    tables, offs, ids, n_ids = csr_problem(rng, B, [16], [0])
+    packed = np.concatenate([offs.reshape(-1), ids]).astype(np.int64)
+    with pytest.raises(dpi.DpiError) as e:
+        lookup_csr(tables, None, packed, dpi.DPI_X_I64, B, n_ids)
+    assert e.value.status == dpi.DPI_ERR_UNSUPPORTED
