@@ -32,12 +32,13 @@ def test_bag_length_laws():
 
 def test_values_distribution_and_rounding():
     cfg = configs.get(3)
-    t = G.make_table(cfg, 0)                 # 1011 x 64 fp16
+    assert int(G.table_sizes(cfg)[2]) == 1088
+    t = G.make_table(cfg, 2)                 # 1088 x 64 fp16
     x = t.double()
     assert abs(x.mean().item()) < 5e-4
     assert abs(x.std().item() - 0.01) < 0.0002
     c32 = configs.Config(**{**cfg.__dict__, "dtype": configs.F32})
-    t32 = G.make_table(c32, 0)
+    t32 = G.make_table(c32, 2)
     assert torch.equal(t32.half(), t)
 
 
