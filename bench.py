@@ -18,6 +18,7 @@ the current kernel source, else reported as null.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -664,11 +665,16 @@ def measure(cfg, args, dev, steps: int, warmup: int, fm: bool = False, inflight:
     torch.cuda.synchronize()
     plans = []
     evs = timing_events(steps, 3, stream)
+    # no garbage collection inside the timed loop (a collection pass stalls the
+    # host for milliseconds, and small steps wait on the host)
+    gc.collect()
+    gc.disable()
     t0 = time.perf_counter()
     for i in range(steps):
         plans.append(step(warmup + i, evs[i]))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    gc.enable()
     status = dpi.dpi_plan_sync_status(plans[-1])
     if status != dpi.DPI_OK:
         raise SystemExit(f"device reported {dpi.dpi_status_str(status)}")
