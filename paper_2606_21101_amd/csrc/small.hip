@@ -270,7 +270,10 @@ __device__ __forceinline__ void small_direct(KS a, const S& src, bool has_offset
     const int64_t first = lane * bpl;
     int32_t v[kScanMax + 1];
 #pragma unroll
-    for (int j = 0; j <= kScanMax; ++j) v[j] = src.offset(row + min(first + j, B));
+    for (int j = 0; j <= kScanMax; ++j) {
+      v[j] = 0;
+      if (j <= bpl) v[j] = src.offset(row + min(first + j, B));   // bpl is the same for the whole wave
+    }
     if (mine && lane < (1 << jlog)) {
       o.lo = lo;
       o.hi = hi;
