@@ -209,3 +209,33 @@ def test_field_count_limit_both_sides(T):
     out1, st1, _, _ = run_case(tables, oh, None, pool, 9)
     assert st1 == dpi.DPI_OK
     check(tables, oh, None, pool, 9, out1, exact=True)
+
+
+@pytest.mark.parametrize("B", [1, 1000])
+def test_empty_batches_and_empty_fields(B):
+    """Every bag empty (no ids at all), then one field without ids among
+    others: zeros where there is nothing to pool, status clean."""
+    rng = np.random.default_rng(B + 3)
+    tables, _, _, pool = random_problem(rng, [16, 64, 8], [0, 1, 0], B, 4, rows=50)
+    lens = np.zeros((3, B), np.int64)
+    offs, ids = with_lengths(rng, tables, lens)
+    out, st, _, _ = run_case(tables, ids, offs, pool, B)
+    assert st == dpi.DPI_OK
+    assert torch.all(out == 0)
+    lens = rng.integers(0, 6, size=(3, B))
+    lens[1] = 0
+    offs, ids = with_lengths(rng, tables, lens)
+    out, st, _, _ = run_case(tables, ids, offs, pool, B)
+    assert st == dpi.DPI_OK
+    check(tables, ids, offs, pool, B, out)
+
+
+def test_sixty_four_fields_one_sample():
+    """The widest one-launch batch at B = 1: 64 fields of every row class."""
+    rng = np.random.default_rng(64)
+    dims = [4 * (1 << (t % 7)) for t in range(64)]          # 16 .. 1024-byte fp32 rows
+    dtypes = [0] * 64
+    tables, ids, offs, pool = random_problem(rng, dims, dtypes, 1, 30, rows=20)
+    out, st, _, _ = run_case(tables, ids, offs, pool, 1)
+    assert st == dpi.DPI_OK
+    check(tables, ids, offs, pool, 1, out)
