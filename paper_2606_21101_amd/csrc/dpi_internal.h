@@ -112,6 +112,7 @@ struct PlanParams {
   int32_t lazy_partition;  // skip the bag prefixes and the wave partition when no bag is longer than
                            // kDirectMaxItems items (the lookup kernel does not read them)
   int32_t prefixes;        // write the per-bag prefixes bib / bcb (read only by an export)
+  int32_t reduce_blocks;   // one-launch planner: blocks that sum tiles (0: every block its own tile)
   int64_t B;
   int64_t TB;
   int64_t total_ids;

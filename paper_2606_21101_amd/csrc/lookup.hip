@@ -515,25 +515,25 @@ struct Mixed {
   }
 };
 
-// Bags [lA, lB) (global bag numbers, field-major), split at field ends.
+// Bags [lA, lB) (global bag numbers, field-major; lA in field t), split at
+// field ends.
 template <typename P>
-__device__ __forceinline__ int pool_bag_range(KA a, int64_t lA, int64_t lB, int lane) {
+__device__ __forceinline__ int pool_bag_range(KA a, int64_t t, int64_t lA, int64_t lB, int lane) {
   int bad = 0;
   while (lA < lB) {
-    const int64_t t = __builtin_amdgcn_readfirstlane((int)(lA / a->B));
     const int64_t seg_end = min(lB, (t + 1) * a->B);
     bad |= P::segment(a, t, lA - t * a->B, seg_end - t * a->B, lane);
     lA = seg_end;
+    ++t;
   }
   return bad;
 }
 
-// Rows [row_lo, row_hi) of a bag shared with other waves: partial, then the
-// arrival protocol.
+// Rows [row_lo, row_hi) of a bag (of field t) shared with other waves:
+// partial, then the arrival protocol.
 template <typename P>
-__device__ __forceinline__ int pool_partial(KA a, int64_t bag, int64_t row_lo, int64_t row_hi, int64_t slot,
-                                            int64_t w_first, int lane) {
-  const int64_t t = __builtin_amdgcn_readfirstlane((int)(bag / a->B));
+__device__ __forceinline__ int pool_partial(KA a, int64_t t, int64_t bag, int64_t row_lo, int64_t row_hi,
+                                            int64_t slot, int64_t w_first, int lane) {
   const int bad = P::partial(a, t, bag - t * a->B, row_lo, row_hi, slot, lane);
   P::finish(a, w_first, bag, lane);
   return bad;
@@ -565,20 +565,26 @@ __device__ __forceinline__ void wave_body(KA a) {
   const int64_t lb = tail ? lz : lz - 1;
   const int64_t lb_base = lz_base;   // read only with tail
   const bool head = la_base < i0;
+  // the fields of the wave's first and last bags, both divisions here (the
+  // divisor's reciprocal is then dead before the pooling loops, where it
+  // would cost a register or a spill)
+  const int64_t ta = __builtin_amdgcn_readfirstlane((int)(la / a->B));
+  const int64_t tb = __builtin_amdgcn_readfirstlane((int)(lb / a->B));
   int bad = 0;
   if (la == lb && (head || tail)) {
     const int64_t slot = head ? 2 * w : 2 * w + 1;
     const int64_t w_first = head ? (int64_t)a->head_first[w] : w;
-    bad |= pool_partial<P>(a, la, (i0 - la_base) * C, (i1 - la_base) * C, slot, w_first, lane);
+    bad |= pool_partial<P>(a, ta, la, (i0 - la_base) * C, (i1 - la_base) * C, slot, w_first, lane);
   } else {
-    int64_t lA = la, lB = lb + 1;
+    int64_t lA = la, lB = lb + 1, tA = ta;
     if (head) {
-      bad |= pool_partial<P>(a, la, (i0 - la_base) * C, INT64_MAX / 2, 2 * w, a->head_first[w], lane);
+      bad |= pool_partial<P>(a, ta, la, (i0 - la_base) * C, INT64_MAX / 2, 2 * w, a->head_first[w], lane);
       lA = la + 1;
+      tA += lA == (ta + 1) * a->B ? 1 : 0;
     }
     if (tail) lB = lb;
-    bad |= pool_bag_range<P>(a, lA, lB, lane);
-    if (tail) bad |= pool_partial<P>(a, lb, 0, (i1 - lb_base) * C, 2 * w + 1, w, lane);
+    bad |= pool_bag_range<P>(a, tA, lA, lB, lane);
+    if (tail) bad |= pool_partial<P>(a, tb, lb, 0, (i1 - lb_base) * C, 2 * w + 1, w, lane);
   }
   if (__any(bad) && lane == 0)
     __hip_atomic_fetch_or(a->status, kStatusBadId, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

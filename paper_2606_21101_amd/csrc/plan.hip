@@ -15,8 +15,10 @@
 //                  prefixes of items and cost, and every wave boundary that
 //                  falls in a bag's cost interval.
 // A batch of one tile runs both steps in a single block (one launch); a batch
-// of at most kPlanDirectTiles tiles, all resident at once, runs both in one
-// launch whose blocks exchange their tile sums (plan_fused); a one-hot batch
+// of at most kPlanDirectTiles tiles runs both in one launch whose blocks
+// exchange their tile sums (plan_fused: a block per tile when every tile's
+// block fits on the device at once, else a resident grid whose blocks take
+// several tiles each); a one-hot batch
 // (no offsets) takes plan_onehot, which writes the closed forms of the same
 // arrays in one fully parallel launch.
 //
@@ -297,8 +299,10 @@ __device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk) {
 }
 
 // sums (optional): receives the tile's items, cost and malformed | long << 1
-// on every thread.
-template <int V>
+// on every thread.  UNROLL: groups of slabs unrolled (all of them by default,
+// so that the compiler can issue every group's loads together; fewer keep the
+// registers for a caller that scans afterwards in the same kernel).
+template <int V, int UNROLL = (V < kPlanChunk ? 1 : V / kPlanChunk)>
 __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks, int64_t* sums = nullptr) {
   PPR p = pa->p;
   PDR d = pa->d;
@@ -314,7 +318,7 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
     SlabRaw<CH> raw;
     slab_load<CH>(pa, tile0 + tid, raw);   // in flight across the barrier
     __syncthreads();
-#pragma unroll
+#pragma unroll UNROLL
     for (int c0 = 0; c0 < V; c0 += CH) {
       SlabBags<CH> s;
       slab_cost<CH>(pa, s_f, raw, s);
@@ -887,11 +891,12 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
 }
 
 // ---------------------------------------------------------------------------
-// One launch for batches of several tiles (at most kPlanDirectTiles, every
-// block resident): each block sums its tile and publishes the sums, then
+// One launch for batches of several tiles (at most kPlanDirectTiles; every
+// block resident, a block per tile or several tiles per block): each block
+// sums its tiles and publishes the sums, then
 // gathers every tile's sums -- the partition needs the batch's total cost,
 // so a block waits for the tiles after it as well as those before -- and
-// scans and partitions its tile.  A published sum travels as two 64-bit
+// scans and partitions its tiles.  A published sum travels as two 64-bit
 // words, each holding the low 32 bits of the plan's id above 32 bits of the
 // value, stored and loaded with device-scope atomics: a word is valid exactly
 // when its id matches, so no fence (no write-back or invalidation of the
@@ -941,38 +946,30 @@ __device__ int64_t tile_sums_serial(PA pa, const FieldBytes& f, int64_t j, int64
   return bad | (nlong << 1);
 }
 
-template <int V>
-__global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs args) {
-  (void)args;
-  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
-  PPR p = pa->p;
-  PDR d = pa->d;
-  const int tid = threadIdx.x;
-  const int64_t blk = blockIdx.x, nb = p.nblk;
-  int64_t* const flags = d.block_sum + 4 * nb + 3;
-
-  const uint64_t tag = (uint64_t)p.plan_id << 32;
-  // this tile's sums (block 0: also the field info), published
-  int64_t mine[3];
-  plan_reduce_block<V>(pa, blk, nb, mine);
-  if (tid == 0) {
-    uint64_t* w = reinterpret_cast<uint64_t*>(flags) + blk * kTileWords;
+// Publishes tile blk's sums (items, cost, malformed | long << 1) as tagged
+// words; one thread.
+__device__ __forceinline__ void publish_tile_sums(int64_t* flags, int64_t blk, uint64_t tag,
+                                                  const int64_t (&mine)[3]) {
+  uint64_t* w = reinterpret_cast<uint64_t*>(flags) + blk * kTileWords;
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-      __hip_atomic_store(w + 2 * q, tag | ((uint64_t)mine[q] & 0xffffffffu), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(w + 2 * q + 1, tag | ((uint64_t)mine[q] >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+  for (int q = 0; q < 3; ++q) {
+    __hip_atomic_store(w + 2 * q, tag | ((uint64_t)mine[q] & 0xffffffffu), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(w + 2 * q + 1, tag | ((uint64_t)mine[q] >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
+}
 
-  __shared__ FieldBytes s_f;
-  SlabRaw<scan_chunk<V>()> raw;
-  plan_scan_prologue<V>(pa, blk, s_f, raw);   // field bytes, and the first loads of the scan in flight
-  __syncthreads();
-
-  // every tile's sums: thread i takes tiles i, i + 256, ...
+// Every tile's published sums, gathered for tile blk (thread i takes tiles i,
+// i + 256, ...): v = prefix items, prefix cost, items, cost, malformed tiles,
+// long bags, block-reduced on every thread.
+template <int V>
+__device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t tag, const int64_t* flags,
+                                                 const FieldBytes& s_f, int64_t (&v)[6]) {
+  const int tid = threadIdx.x;
+  const int64_t nb = pa->p.nblk;
   constexpr int kPer = kPlanDirectTiles / kScanThreads;
-  int64_t v[6] = {0, 0, 0, 0, 0, 0};   // prefix items, prefix cost, items, cost, malformed, long bags
+#pragma unroll
+  for (int q = 0; q < 6; ++q) v[q] = 0;
 #pragma unroll
   for (int m = 0; m < kPer; ++m) {
     const int64_t j = tid + (int64_t)m * kScanThreads;
@@ -1006,23 +1003,64 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
   }
   __shared__ int64_t s_red[kWavesPerBlock][6];
   block_sums<6>(v, s_red);
+}
+
+// A block per tile.  SPREAD = false: every block resident at once, each
+// sums its own tile.  SPREAD = true: more tiles than resident blocks; blocks
+// b < p.reduce_blocks (the first to start, all resident together) sum tiles
+// b, b + reduce_blocks, ... and publish all of them before any block waits,
+// and the later blocks, which start as the first ones finish, only gather
+// and scan.
+template <int V, bool SPREAD>
+__global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs args) {
+  (void)args;
+  const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
+  PPR p = pa->p;
+  PDR d = pa->d;
+  const int tid = threadIdx.x;
+  const int64_t blk = blockIdx.x, nb = p.nblk;
+  int64_t* const flags = d.block_sum + 4 * nb + 3;
+  const uint64_t tag = (uint64_t)p.plan_id << 32;
+
+  // tile sums (tile 0: also the field info), published
+  if constexpr (!SPREAD) {
+    int64_t mine[3];
+    plan_reduce_block<V>(pa, blk, nb, mine);
+    if (tid == 0) publish_tile_sums(flags, blk, tag, mine);
+  } else {
+    const int64_t G = p.reduce_blocks;
+#pragma unroll 1
+    for (int64_t j = blk; blk < G && j < nb; j += G) {
+      int64_t mine[3];
+      plan_reduce_block<V, 1>(pa, j, nb, mine);
+      if (tid == 0) publish_tile_sums(flags, j, tag, mine);
+      __syncthreads();   // the next tile's sums reuse the block's LDS
+    }
+  }
+
+  __shared__ FieldBytes s_f;
+  SlabRaw<scan_chunk<V>()> raw;
+  plan_scan_prologue<V>(pa, blk, s_f, raw);   // field bytes, and the first loads of the scan in flight
+  __syncthreads();
+  int64_t v[6];
+  gather_tile_sums<V>(pa, blk, tag, flags, s_f, v);
   plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], s_f, raw);
 }
 
-// Whether every block of a fused planning launch of nblk tiles is resident at
-// once (so that no flag waits for a block that cannot start).
-template <int V>
-bool plan_fused_fits(int64_t nblk) {
-  static int per_cu = -1, cus = 0;
-  if (per_cu < 0) {
-    int dev = 0, n = 0;
+// Blocks of plan_fused_kernel<V, SPREAD> resident at once on the device (0
+// if the runtime cannot say).
+template <int V, bool SPREAD>
+int64_t plan_fused_capacity() {
+  static int64_t cap = -1;
+  if (cap < 0) {
+    int dev = 0, n = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, plan_fused_kernel<V>, kScanThreads, 0) != hipSuccess)
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, plan_fused_kernel<V, SPREAD>, kScanThreads, 0) != hipSuccess)
       n = 0;
-    per_cu = n;
+    cap = (int64_t)n * cus;
   }
-  return nblk <= (int64_t)per_cu * cus;
+  return cap;
 }
 
 template <int V>
@@ -1034,9 +1072,20 @@ hipError_t launch_plan_v(const PlanArgs& a, hipStream_t s) {
       return hipGetLastError();
     }
   }
-  if (blocks <= (unsigned)kPlanDirectTiles && plan_fused_fits<V>(blocks)) {
-    hipLaunchKernelGGL(plan_fused_kernel<V>, dim3(blocks), dim3(kScanThreads), 0, s, a);
-    return hipGetLastError();
+  if (blocks <= (unsigned)kPlanDirectTiles) {
+    // one launch: every tile's block resident, or the first resident blocks
+    // summing the tiles of those that start later
+    if ((int64_t)blocks <= plan_fused_capacity<V, false>()) {
+      hipLaunchKernelGGL((plan_fused_kernel<V, false>), dim3(blocks), dim3(kScanThreads), 0, s, a);
+      return hipGetLastError();
+    }
+    const int64_t cap = plan_fused_capacity<V, true>();
+    if (cap > 0) {
+      PlanArgs b = a;
+      b.p.reduce_blocks = (int32_t)cap;
+      hipLaunchKernelGGL((plan_fused_kernel<V, true>), dim3(blocks), dim3(kScanThreads), 0, s, b);
+      return hipGetLastError();
+    }
   }
   hipLaunchKernelGGL(plan_reduce_kernel<V>, dim3(blocks), dim3(kScanThreads), 0, s, a);
   hipError_t e = hipGetLastError();

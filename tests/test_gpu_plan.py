@@ -147,6 +147,18 @@ def test_plan_parity_many_tiles_multihot():
     run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False)
 
 
+@pytest.mark.parametrize("T,B", [(1, 1_600_000), (2, 3_000_000)])
+def test_plan_parity_tiles_beyond_residency(T, B):
+    """Batches of more tiles than fit on the device at once but at most 1024
+    (about 390 tiles of 4096 bags, about 730 of 8192): the one-launch
+    planner's first blocks sum the tiles of the blocks that start later.  Bags
+    of 0..5 ids, split bags under a tight wave count, then the default one."""
+    rng = np.random.default_rng(12)
+    lengths = rng.integers(0, 6, size=(T, B))
+    run_plan([16, 64][:T], [0, 1][:T], 1, [1000] * T, lengths, False, W=50_001, C=2)
+    run_plan([16, 64][:T], [0, 1][:T], 1, [1000] * T, lengths, False)
+
+
 @pytest.mark.parametrize("W", [1, 7, 26 * 4096, 1_000_000, 0])
 def test_plan_onehot_closed_form_wave_counts(W):
     """The closed-form one-hot plan against the oracle at wave counts from one
@@ -254,16 +266,21 @@ def test_superseded_plan_is_refused():
     assert dpi.dpi_plan_export(second)["header"][2] == 2
 
 
-@pytest.mark.parametrize("T,B", [(2, 100_000), (1, 9_000_000)])
-def test_bad_offsets_detected_in_multi_tile_batches(T, B):
+@pytest.mark.parametrize("T,B,late", [(2, 100_000, False), (1, 9_000_000, False), (1, 6_000_000, False),
+                                      (1, 6_000_000, True)])
+def test_bad_offsets_detected_in_multi_tile_batches(T, B, late):
     """Malformed offsets seen by several threads of one tile, in batches planned
-    by one launch (fewer than 1024 tiles) and by three (more): the plan must
-    reject them.  (A tile's flag once summed the count of threads that saw a
-    malformed bag into its malformed bit, so two such threads cleared it.)"""
+    by one launch (fewer than 1024 tiles; 6 M bags are more tiles than fit on
+    the device at once) and by three (more): the plan must reject them.  (A
+    tile's flag once summed the count of threads that saw a malformed bag into
+    its malformed bit, so two such threads cleared it.)  late: the malformed
+    bags sit in a tile past the first blocks' own, summed by a block that
+    sums several tiles."""
     lengths = np.ones((T, B), np.int64)
     offs_np = G.offsets_from_lengths(lengths).astype(np.int32)
-    offs_np[0, 1001] = offs_np[0, 1000] - 1     # decreasing: bags 999 and 1000 both malformed
-    offs_np[0, 1500] = offs_np[0, 1499] - 5
+    at = B - 1000 if late else 1000
+    offs_np[0, at + 1] = offs_np[0, at] - 1     # decreasing: bags at - 1 and at both malformed
+    offs_np[0, at + 500] = offs_np[0, at + 499] - 5
     total = int(offs_np[:, -1].astype(np.int64).sum())
     tabs = [torch.zeros((10, 16), device="cuda") for _ in range(T)]
     fl = FusedLookup(tabs)
