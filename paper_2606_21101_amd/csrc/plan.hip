@@ -78,6 +78,54 @@ __device__ __forceinline__ int64_t floor_div128(u128 num, int64_t den, double g)
   return q;
 }
 
+// The same quotients in 64-bit arithmetic, for callers whose products and
+// corrected quotients times den stay below 2^63.
+__device__ __forceinline__ uint64_t mul64(int64_t a, int64_t b) { return (uint64_t)a * (uint64_t)b; }
+
+__device__ __forceinline__ int64_t ceil_div64(uint64_t num, int64_t den, double inv_den) {
+  int64_t q = (int64_t)((double)num * inv_den);
+  if (q < 0) q = 0;
+  while (q > 0 && mul64(q - 1, den) >= num) --q;
+  while (mul64(q, den) < num) ++q;
+  return q;
+}
+
+__device__ __forceinline__ int64_t floor_div64(uint64_t num, int64_t den, double g) {
+  int64_t q = (int64_t)g;
+  if (q < 0) q = 0;
+  while (q > 0 && mul64(q, den) > num) --q;
+  while (mul64(q + 1, den) <= num) ++q;
+  return q;
+}
+
+// Exact quotients for the wave-boundary arithmetic: 128-bit, or 64-bit when
+// S*W < 2^62 (then every product below stays under 2^63: E <= S, w <= W, a
+// corrected quotient exceeds the true one by less than one, and an item
+// costs at most S).
+template <bool F64> struct Quot;
+template <> struct Quot<false> {
+  static __device__ __forceinline__ int64_t floor_mul_div(int64_t a, int64_t b, int64_t den, double g) {
+    return floor_div128(mul128(a, b), den, g);
+  }
+  static __device__ __forceinline__ int64_t ceil_mul_div(int64_t a, int64_t b, int64_t den, double inv) {
+    return ceil_div128(mul128(a, b), den, inv);
+  }
+  static __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t den, double inv) {
+    return ceil_div128((u128)(uint64_t)num, den, inv);
+  }
+};
+template <> struct Quot<true> {
+  static __device__ __forceinline__ int64_t floor_mul_div(int64_t a, int64_t b, int64_t den, double g) {
+    return floor_div64(mul64(a, b), den, g);
+  }
+  static __device__ __forceinline__ int64_t ceil_mul_div(int64_t a, int64_t b, int64_t den, double inv) {
+    return ceil_div64(mul64(a, b), den, inv);
+  }
+  static __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t den, double inv) {
+    return ceil_div64((uint64_t)num, den, inv);
+  }
+};
+
 // field of bag l: floor(l / B), exact (the quotient is below DPI_MAX_TABLES)
 __device__ __forceinline__ int32_t field_of(int64_t l, int64_t B, double inv_b) {
   int32_t t = (int32_t)((double)l * inv_b);
@@ -249,6 +297,34 @@ __device__ __forceinline__ void slab_cost(PA pa, const FieldBytes& f, const Slab
   }
 }
 
+// The same for a tile whose cost sum fits 32 bits (so does every bag's cost,
+// formed here modulo 2^32).
+template <int CH>
+struct SlabBags32 {
+  int32_t t[CH];
+  uint32_t n[CH];
+  uint32_t c[CH];
+};
+
+template <int CH>
+__device__ __forceinline__ void slab_cost32(PA pa, const FieldBytes& f, const SlabRaw<CH>& r, SlabBags32<CH>& s) {
+  PPR p = pa->p;
+  const uint32_t C = (uint32_t)p.C, K = (uint32_t)p.K;
+  const int32_t sh = p.c_shift;
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    const bool bad = (r.first[k] & (r.lo[k] != 0)) | (r.hi[k] < r.lo[k]);
+    const uint32_t L = bad ? 0u : (uint32_t)(r.hi[k] - r.lo[k]);
+    const uint32_t up = L + C - 1u;
+    uint32_t n = sh >= 0 ? up >> sh : up / C;
+    n = n < 1u ? 1u : n;
+    const int t = r.t[k];
+    s.t[k] = t;
+    s.n[k] = r.ok[k] ? n : 0u;
+    s.c[k] = r.ok[k] ? L * (uint32_t)f.row[t] + (uint32_t)f.out[t] + n * K : 0u;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Launch 1: tile sums, validation, field info.
 // ---------------------------------------------------------------------------
@@ -308,7 +384,7 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
   PDR d = pa->d;
   const int tid = threadIdx.x;
   constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
-  bool bad = plan_setup_block(pa, blk);
+  bool bad = false;
 
   int64_t v[4] = {0, 0, 0, 0};   // items, cost, malformed offsets, long bags
   if (p.TB > 0) {
@@ -316,7 +392,8 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
     stage_fields(pa, s_f);
     const int64_t tile0 = blk * (int64_t)kScanThreads * V;
     SlabRaw<CH> raw;
-    slab_load<CH>(pa, tile0 + tid, raw);   // in flight across the barrier
+    slab_load<CH>(pa, tile0 + tid, raw);   // in flight across the setup and the barrier
+    bad = plan_setup_block(pa, blk);        // (tile 0: the field info, its loads behind the slabs')
     __syncthreads();
 #pragma unroll UNROLL
     for (int c0 = 0; c0 < V; c0 += CH) {
@@ -331,6 +408,8 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
       }
       bad |= s.bad;
     }
+  } else {
+    bad = plan_setup_block(pa, blk);
   }
   v[2] = bad ? 1 : 0;
   __shared__ int64_t s_red[kWavesPerBlock][4];
@@ -411,6 +490,7 @@ struct Targets {
   double scale;     // W / S
   double inv_w;     // 1 / W
   bool exact;       // no snapping of starts to bag ends
+  bool fits64;      // S * W < 2^62: the boundary quotients in 64-bit arithmetic
 };
 
 // A bag whose cost interval may hold a wave target (after the filter in the
@@ -441,21 +521,23 @@ struct BoundaryOut {
 // head link of wave w, and the split entries of wave w - 1 (the wave ending
 // at it), whose arrival counter it also clears.
 // Returns whether the bag is split between waves.
+template <bool F64>
 __device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targets& g, const FieldBytes& f,
                                                const Cand& cd) {
+  typedef Quot<F64> Q;
   const int64_t W = g.W, S = g.S, E_lo = cd.E_lo, E_hi = cd.E_hi, n = cd.n;
-  const int64_t f_lo = floor_div128(mul128(E_lo, W), S, floor((double)E_lo * g.scale));
-  int64_t f_hi = floor_div128(mul128(E_hi, W), S, floor((double)E_hi * g.scale));
+  const int64_t f_lo = Q::floor_mul_div(E_lo, W, S, floor((double)E_lo * g.scale));
+  int64_t f_hi = Q::floor_mul_div(E_hi, W, S, floor((double)E_hi * g.scale));
   if (f_hi > W) f_hi = W;
   const int64_t out_bytes = f.out[cd.t];
   const int64_t per_item = o.C * f.row[cd.t] + o.K;
   const double inv_item = 1.0 / (double)per_item;
   int64_t w_first = -1, begin_prev = -1, pieces = 1, w_last = -1;
   for (int64_t w = f_lo + 1; w <= f_hi; ++w) {
-    const int64_t c = ceil_div128(mul128(w, S), W, g.inv_w);   // ceil(w*S/W), in (E_lo, E_hi]
+    const int64_t c = Q::ceil_mul_div(w, S, W, g.inv_w);   // ceil(w*S/W), in (E_lo, E_hi]
     // smallest j in [1, n] whose cost prefix reaches c
     const int64_t num = c - E_lo - out_bytes;
-    int64_t j = num <= 0 ? 1 : ceil_div128((u128)(uint64_t)num, per_item, inv_item);
+    int64_t j = num <= 0 ? 1 : Q::ceil_div(num, per_item, inv_item);
     if (j < 1) j = 1;
     if (j > n - 1) j = n;
     bool inside = j < n;
@@ -497,7 +579,8 @@ __device__ __forceinline__ void resolve_candidates(BoundaryOut& o, const Targets
   // the list was written by other lanes of this wave: keep the reads after the writes
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   __builtin_amdgcn_wave_barrier();
-  const bool split = lane < count && bag_boundaries(o, g, f, list[lane]);
+  const bool split = lane < count && (g.fits64 ? bag_boundaries<true>(o, g, f, list[lane])
+                                               : bag_boundaries<false>(o, g, f, list[lane]));
   const uint64_t m = __ballot(split);
   if (m != 0 && lane == 0) atomicAdd(&o.splits, (unsigned long long)__popcll(m));
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
@@ -520,8 +603,8 @@ __device__ __forceinline__ void plan_scan_prologue(PA pa, int64_t blk, FieldByte
 
 template <int V>
 __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i, int64_t pre_c, int64_t N,
-                                               int64_t S, bool err, int64_t nlong, FieldBytes& s_f,
-                                               SlabRaw<scan_chunk<V>()>& raw);
+                                               int64_t S, bool err, int64_t nlong, int64_t own_i, int64_t own_c,
+                                               FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw);
 
 // SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
 // its sums come straight from the block instead of from plan_reduce, and
@@ -537,8 +620,8 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
   const int64_t* bs = d.block_sum;
   constexpr int CH = scan_chunk<V>();
 
-  // this tile's exclusive prefix and the totals
-  int64_t pre_i, pre_c, N, S;
+  // this tile's exclusive prefix, its own sums and the totals
+  int64_t pre_i, pre_c, N, S, own_i, own_c;
   int64_t nlong = 1;   // bags of more than kDirectMaxItems items (not counted beyond kPlanDirectTiles tiles)
   bool err;
   if constexpr (SINGLE) {
@@ -564,6 +647,8 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     S = v[1];
     err = v[2] != 0;
     nlong = v[3];
+    own_i = N;
+    own_c = S;
   } else if (nb <= kPlanDirectTiles) {
     // from the tile sums: every entry loaded at once, then block sums
     int64_t v[6] = {0, 0, 0, 0, 0, 0};   // prefix items, prefix cost, items, cost, malformed, long bags
@@ -588,6 +673,8 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     S = v[3];
     err = v[4] != 0;
     nlong = v[5];
+    own_i = bs[blk];
+    own_c = bs[nb + blk];
   } else {
     // plan_tiles left exclusive prefixes in place and the totals after them
     pre_i = bs[blk];
@@ -595,8 +682,10 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     N = bs[3 * nb];
     S = bs[3 * nb + 1];
     err = bs[3 * nb + 2] != 0;
+    own_i = (blk + 1 < nb ? bs[blk + 1] : N) - pre_i;
+    own_c = (blk + 1 < nb ? bs[nb + blk + 1] : S) - pre_c;
   }
-  plan_scan_core<V>(pa, blk, pre_i, pre_c, N, S, err, nlong, s_f, raw);
+  plan_scan_core<V>(pa, blk, pre_i, pre_c, N, S, err, nlong, own_i, own_c, s_f, raw);
 }
 
 // The scan and partition of tile blk, its exclusive prefix (pre_i items,
@@ -605,8 +694,8 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
 // header and the status words.
 template <int V>
 __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i, int64_t pre_c, int64_t N,
-                                               int64_t S, bool err, int64_t nlong, FieldBytes& s_f,
-                                               SlabRaw<scan_chunk<V>()>& raw) {
+                                               int64_t S, bool err, int64_t nlong, int64_t own_i, int64_t own_c,
+                                               FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -665,6 +754,7 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     g.scale = W > 0 ? (double)W / (double)S : 0.0;
     g.inv_w = W > 0 ? 1.0 / (double)W : 0.0;
     g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
+    g.fits64 = mul128(S, W) < ((u128)1 << 62);
     o.wib = d.wib;
     o.wave_bag = d.wave_bag;
     o.wbase = d.wbase;
@@ -678,79 +768,126 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
   }
   __syncthreads();   // publishes the field bytes, g and o
   const double scale = g.scale;
-  // per slab and wave: the wave's item and cost totals
-  __shared__ int64_t s_wt[V][2][kWavesPerBlock];
   __shared__ Cand s_cand[kWavesPerBlock][kWaveSize];
   int ncand = 0;   // collected candidates of this wave (wave-uniform)
-  int64_t run_i = pre_i, run_c = pre_c;
+  // Collects bag `bag` (items [ibase, ibase + n), cost interval (E_lo, E_hi])
+  // when the filter passed for some lane; resolves a full list first.
+  auto collect = [&](bool cand, int64_t bag, int64_t ibase, int64_t E_lo, int64_t E_hi, int32_t t, int32_t n) {
+    const uint64_t m = __ballot(cand);
+    if (m == 0) return;
+    const int cnt = __popcll(m);
+    if (ncand + cnt > kWaveSize) {
+      resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
+      ncand = 0;
+    }
+    if (cand) {
+      const int pos = ncand + __popcll(m & ((1ull << lane) - 1ull));
+      Cand& e = s_cand[wv][pos];
+      e.bag = bag;
+      e.ibase = ibase;
+      e.E_lo = E_lo;
+      e.E_hi = E_hi;
+      e.t = t;
+      e.n = n;
+    }
+    ncand += cnt;
+  };
+  // filter in double: both products are within (x + 1) * 2^-50 of E*W/S,
+  // so equal floors of the widened interval prove it holds no target
+  auto may_hold_target = [](double x_lo, double x_hi) {
+    const double margin = (x_hi + 1.0) * 0x1p-45;
+    return floor(x_hi + margin) != floor(x_lo - margin);
+  };
+  if (own_i >= 0 && own_i <= (int64_t)UINT32_MAX && own_c >= 0 && own_c <= (int64_t)UINT32_MAX) {
+    // Narrow tile (block-uniform): every sum inside the tile fits 32 bits, so
+    // the costs, scans, wave totals and running sums are 32-bit and a bag's
+    // 64-bit prefixes are the tile prefix plus its local ones.  The filter
+    // forms E*W/S as fma(local, W/S, pre_c*W/S): three roundings of relative
+    // size 2^-53, inside the same bound.
+    __shared__ __align__(16) uint32_t s_w32[V][2][kWavesPerBlock];
+    const double base = (double)pre_c * scale;
+    uint32_t run_i = 0, run_c = 0;
 #pragma unroll 1
-  for (int c0 = 0; c0 < V; c0 += CH) {
-    SlabBags<CH> s;
-    slab_cost<CH>(pa, s_f, raw, s);
-    if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw);   // next group
-    int64_t xi[CH], xc[CH];
+    for (int c0 = 0; c0 < V; c0 += CH) {
+      SlabBags32<CH> s;
+      slab_cost32<CH>(pa, s_f, raw, s);
+      if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw);   // next group
+      uint32_t xi[CH], xc[CH];
 #pragma unroll
-    for (int k = 0; k < CH; ++k) {
-      // wave totals below 2^32 (every cost below 2^25) take the 32-bit scan
-      if (__all(s.c[k] < ((int64_t)1 << 25))) {
-        xi[k] = wave_incl_scan32((uint32_t)s.n[k], lane);
-        xc[k] = wave_incl_scan32((uint32_t)s.c[k], lane);
-      } else {
-        xi[k] = wave_incl_scan(s.n[k], lane);
-        xc[k] = wave_incl_scan(s.c[k], lane);
+      for (int k = 0; k < CH; ++k) {
+        xi[k] = wave_incl_scan32(s.n[k], lane);
+        xc[k] = wave_incl_scan32(s.c[k], lane);
+        if (lane == 63) {
+          s_w32[c0 + k][0][wv] = xi[k];
+          s_w32[c0 + k][1][wv] = xc[k];
+        }
       }
-      if (lane == 63) {
-        s_wt[c0 + k][0][wv] = xi[k];
-        s_wt[c0 + k][1][wv] = xc[k];
+      __syncthreads();   // every slab of the group has its own LDS slots: one barrier per group
+#pragma unroll
+      for (int k = 0; k < CH; ++k) {
+        const uint4 wi = *reinterpret_cast<const uint4*>(s_w32[c0 + k][0]);
+        const uint4 wc = *reinterpret_cast<const uint4*>(s_w32[c0 + k][1]);
+        const uint32_t bi = (wv > 0 ? wi.x : 0u) + (wv > 1 ? wi.y : 0u) + (wv > 2 ? wi.z : 0u);
+        const uint32_t bc = (wv > 0 ? wc.x : 0u) + (wv > 1 ? wc.y : 0u) + (wv > 2 ? wc.z : 0u);
+        const uint32_t li = run_i + bi + xi[k] - s.n[k];   // local exclusive prefixes
+        const uint32_t lc = run_c + bc + xc[k] - s.c[k];
+        run_i += wi.x + wi.y + wi.z + wi.w;
+        run_c += wc.x + wc.y + wc.z + wc.w;
+        const int64_t bag = tile0 + (int64_t)(c0 + k) * kScanThreads + tid;
+        const bool valid = bag < p.TB;
+        if (valid && p.prefixes) {
+          d.bib[bag] = pre_i + li;
+          d.bcb[bag] = pre_c + lc;
+        }
+        if (W == 0) continue;
+        const double x_lo = fma((double)lc, scale, base), x_hi = fma((double)(lc + s.c[k]), scale, base);
+        const bool cand = valid && may_hold_target(x_lo, x_hi);
+        collect(cand, bag, pre_i + li, pre_c + lc, pre_c + lc + s.c[k], s.t[k], (int32_t)s.n[k]);
       }
     }
-    __syncthreads();   // every slab of the group has its own LDS slots: one barrier per group
-#pragma unroll
-    for (int k = 0; k < CH; ++k) {
+  } else {
+    // Wide tile (a tile cost of 2^32 bytes or more: rows of hundreds of
+    // kilobytes): 64-bit sums, one slab at a time with its own loads, two
+    // barriers per slab -- slower, and light on registers, so that this rare
+    // path does not cost the narrow one occupancy.
+    __shared__ int64_t s_wt[2][kWavesPerBlock];
+    int64_t run_i = pre_i, run_c = pre_c;
+#pragma unroll 1
+    for (int k = 0; k < V; ++k) {
+      const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
+      SlabRaw<1> r1;
+      slab_load<1>(pa, bag, r1);
+      SlabBags<1> s1;
+      slab_cost<1>(pa, s_f, r1, s1);
+      const int64_t xi = wave_incl_scan(s1.n[0], lane), xc = wave_incl_scan(s1.c[0], lane);
+      __syncthreads();   // the previous slab's totals are read
+      if (lane == 63) {
+        s_wt[0][wv] = xi;
+        s_wt[1][wv] = xc;
+      }
+      __syncthreads();
       int64_t bi = 0, bc = 0, ai = 0, ac = 0;
 #pragma unroll
       for (int v = 0; v < kWavesPerBlock; ++v) {
-        const int64_t a = s_wt[c0 + k][0][v], b = s_wt[c0 + k][1][v];
+        const int64_t a = s_wt[0][v], b = s_wt[1][v];
         ai += a;
         ac += b;
         bi += v < wv ? a : 0;
         bc += v < wv ? b : 0;
       }
-      const int64_t ibase = run_i + bi + xi[k] - s.n[k];
-      const int64_t E_lo = run_c + bc + xc[k] - s.c[k];
-      const int64_t E_hi = E_lo + s.c[k];
+      const int64_t ibase = run_i + bi + xi - s1.n[0];
+      const int64_t E_lo = run_c + bc + xc - s1.c[0];
+      const int64_t E_hi = E_lo + s1.c[0];
       run_i += ai;
       run_c += ac;
-      const int64_t bag = tile0 + (int64_t)(c0 + k) * kScanThreads + tid;
       const bool valid = bag < p.TB;
       if (valid && p.prefixes) {
         d.bib[bag] = ibase;
         d.bcb[bag] = E_lo;
       }
       if (W == 0) continue;
-      // filter in double: both products are within (x + 1) * 2^-50 of E*W/S,
-      // so equal floors of the widened interval prove it holds no target
-      const double x_lo = (double)E_lo * scale, x_hi = (double)E_hi * scale;
-      const double margin = (x_hi + 1.0) * 0x1p-45;
-      const bool cand = valid && floor(x_hi + margin) != floor(x_lo - margin);
-      const uint64_t m = __ballot(cand);
-      if (m == 0) continue;
-      const int cnt = __popcll(m);
-      if (ncand + cnt > kWaveSize) {
-        resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
-        ncand = 0;
-      }
-      if (cand) {
-        const int pos = ncand + __popcll(m & ((1ull << lane) - 1ull));
-        Cand& e = s_cand[wv][pos];
-        e.bag = bag;
-        e.ibase = ibase;
-        e.E_lo = E_lo;
-        e.E_hi = E_hi;
-        e.t = s.t[k];
-        e.n = s.n[k];
-      }
-      ncand += cnt;
+      const bool cand = valid && may_hold_target((double)E_lo * scale, (double)E_hi * scale);
+      collect(cand, bag, ibase, E_lo, E_hi, s1.t[0], s1.n[0]);
     }
   }
   if (ncand > 0) resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
@@ -961,38 +1098,73 @@ __device__ __forceinline__ void publish_tile_sums(int64_t* flags, int64_t blk, u
 
 // Every tile's published sums, gathered for tile blk (thread i takes tiles i,
 // i + 256, ...): v = prefix items, prefix cost, items, cost, malformed tiles,
-// long bags, block-reduced on every thread.
+// long bags, block-reduced on every thread; own = tile blk's items and cost.
+// A thread requests all of its tiles' words at once, three 16-byte loads per
+// tile at agent scope (sc1: served past the XCD's L2, as an agent-scope
+// atomic load is; every 8-byte word carries its own tag, so a pair need not
+// be read atomically), so the usual case -- every tile published -- costs one
+// round trip, and each further polling round one more for all of the
+// thread's tiles still missing.
 template <int V>
 __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t tag, const int64_t* flags,
-                                                 const FieldBytes& s_f, int64_t (&v)[6]) {
+                                                 const FieldBytes& s_f, int64_t (&v)[6], int64_t (&own)[2]) {
+  typedef int i32x4 __attribute__((ext_vector_type(4)));
+  constexpr int kSc1 = 1 << 4;   // buffer cache policy: agent scope
   const int tid = threadIdx.x;
   const int64_t nb = pa->p.nblk;
   constexpr int kPer = kPlanDirectTiles / kScanThreads;
+  __shared__ int64_t s_own[2];
+  const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int64_t*>(flags), (short)0, (int)(nb * kTileWords * 8), 0x00020000);
+  i32x4 raw_w[kPer][kTileWords / 2];
+  bool ready[kPer];
+  auto load_tile = [&](int m) {
+    const int64_t j = min(tid + (int64_t)m * kScanThreads, nb - 1);
+#pragma unroll
+    for (int q = 0; q < kTileWords / 2; ++q)
+      raw_w[m][q] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)(j * kTileWords * 8 + 16 * q), 0, kSc1);
+  };
+  auto tagged = [&](int m) {
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < kTileWords / 2; ++q) ok &= (uint32_t)raw_w[m][q].y == (uint32_t)(tag >> 32) &&
+                                                   (uint32_t)raw_w[m][q].w == (uint32_t)(tag >> 32);
+    return ok;
+  };
+#pragma unroll
+  for (int m = 0; m < kPer; ++m)
+    if ((int64_t)m * kScanThreads < nb) load_tile(m);   // block-uniform
+#pragma unroll
+  for (int m = 0; m < kPer; ++m) ready[m] = tid + (int64_t)m * kScanThreads >= nb || tagged(m);
+  // tiles not yet published: every missing tile of the thread polled again
+  // per round, one round trip each round
+  for (int spin = 0; spin < kPlanSpinLimit; ++spin) {
+    bool all = true;
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) all &= ready[m];
+    if (all) break;
+    __builtin_amdgcn_s_sleep(1);
+#pragma unroll
+    for (int m = 0; m < kPer; ++m)
+      if (!ready[m]) load_tile(m);
+#pragma unroll
+    for (int m = 0; m < kPer; ++m) ready[m] = ready[m] || tagged(m);
+  }
 #pragma unroll
   for (int q = 0; q < 6; ++q) v[q] = 0;
 #pragma unroll
   for (int m = 0; m < kPer; ++m) {
+    if ((int64_t)m * kScanThreads >= nb) break;
     const int64_t j = tid + (int64_t)m * kScanThreads;
     if (j >= nb) continue;
-    const uint64_t* w = reinterpret_cast<const uint64_t*>(flags) + j * kTileWords;
-    uint64_t word[kTileWords];
-    bool ready = false;
-    for (int spin = 0; !ready && spin < kPlanSpinLimit; ++spin) {
-      ready = true;
-#pragma unroll
-      for (int q = 0; q < kTileWords; ++q) {
-        word[q] = __hip_atomic_load(w + q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        ready &= (word[q] & 0xffffffff00000000ull) == tag;
-      }
-      if (!ready) __builtin_amdgcn_s_sleep(2);
-    }
     int64_t si, sc, se;
-    if (ready) {
-      si = (int64_t)((word[0] & 0xffffffffu) | (word[1] << 32));
-      sc = (int64_t)((word[2] & 0xffffffffu) | (word[3] << 32));
-      se = (int64_t)((word[4] & 0xffffffffu) | (word[5] << 32));
+    if (ready[m]) {
+      const i32x4 r0 = raw_w[m][0], r1 = raw_w[m][1], r2 = raw_w[m][2];
+      si = (int64_t)((uint64_t)(uint32_t)r0.x | (uint64_t)(uint32_t)r0.z << 32);
+      sc = (int64_t)((uint64_t)(uint32_t)r1.x | (uint64_t)(uint32_t)r1.z << 32);
+      se = (int64_t)((uint64_t)(uint32_t)r2.x | (uint64_t)(uint32_t)r2.z << 32);
     } else {
-      se = tile_sums_serial<V>(pa, s_f, j, si, sc);
+      se = tile_sums_serial<V>(pa, s_f, j, si, sc);   // not published in time: summed here
     }
     v[0] += j < blk ? si : 0;
     v[1] += j < blk ? sc : 0;
@@ -1000,9 +1172,15 @@ __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t ta
     v[3] += sc;
     v[4] += (se & 1) != 0 ? 1 : 0;
     v[5] += se >> 1;
+    if (j == blk) {
+      s_own[0] = si;
+      s_own[1] = sc;
+    }
   }
   __shared__ int64_t s_red[kWavesPerBlock][6];
-  block_sums<6>(v, s_red);
+  block_sums<6>(v, s_red);   // its barrier also publishes s_own
+  own[0] = s_own[0];
+  own[1] = s_own[1];
 }
 
 // A block per tile.  SPREAD = false: every block resident at once, each
@@ -1042,9 +1220,9 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
   SlabRaw<scan_chunk<V>()> raw;
   plan_scan_prologue<V>(pa, blk, s_f, raw);   // field bytes, and the first loads of the scan in flight
   __syncthreads();
-  int64_t v[6];
-  gather_tile_sums<V>(pa, blk, tag, flags, s_f, v);
-  plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], s_f, raw);
+  int64_t v[6], own[2];
+  gather_tile_sums<V>(pa, blk, tag, flags, s_f, v, own);
+  plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], own[0], own[1], s_f, raw);
 }
 
 // Blocks of plan_fused_kernel<V, SPREAD> resident at once on the device (0

@@ -8,56 +8,46 @@
 namespace dpi {
 namespace {
 
-template <int CTRL>
-__device__ __forceinline__ int64_t dpp_move(int64_t x) {
-  const int lo = __builtin_amdgcn_mov_dpp((int)(uint32_t)(uint64_t)x, CTRL, 0xf, 0xf, false);
-  const int hi = __builtin_amdgcn_mov_dpp((int)(uint32_t)((uint64_t)x >> 32), CTRL, 0xf, 0xf, false);
-  return (int64_t)(((uint64_t)(uint32_t)hi << 32) | (uint64_t)(uint32_t)lo);
+// DPP move in which lanes whose source lies outside the pattern, and lanes of
+// rows outside ROWS (a row mask), receive 0: each scan step is then one
+// unconditional add.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_or_zero(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROWS, 0xf, true);
 }
 
-// Inclusive scan over the 64 lanes: shifts within rows of 16 lanes, then the
-// row-15 and lane-31 broadcasts.  Lanes whose DPP source does not exist never
-// add what they received.
-__device__ __forceinline__ int64_t wave_incl_scan(int64_t x, int lane) {
-  const int r = lane & 15;
-  int64_t y;
-  y = dpp_move<0x111>(x);   // row_shr:1
-  x = r >= 1 ? x + y : x;
-  y = dpp_move<0x112>(x);   // row_shr:2
-  x = r >= 2 ? x + y : x;
-  y = dpp_move<0x114>(x);   // row_shr:4
-  x = r >= 4 ? x + y : x;
-  y = dpp_move<0x118>(x);   // row_shr:8
-  x = r >= 8 ? x + y : x;
-  y = dpp_move<0x142>(x);   // row_bcast:15
-  x = (lane & 16) ? x + y : x;
-  y = dpp_move<0x143>(x);   // row_bcast:31
-  x = lane >= 32 ? x + y : x;
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int64_t dpp_or_zero(int64_t x) {
+  const u32x2 v = __builtin_bit_cast(u32x2, x);
+  // the halves moved into one register pair: one 64-bit add per step
+  return __builtin_bit_cast(int64_t, u32x2{dpp_or_zero<CTRL, ROWS>(v.x), dpp_or_zero<CTRL, ROWS>(v.y)});
+}
+
+// Inclusive scan over the 64 lanes: shifts by 1, 2, 4 and 8 within rows of
+// 16 lanes, then row 0's total into row 1 and row 2's into row 3 (row_bcast
+// 15), then rows 0-1's total into rows 2 and 3 (row_bcast 31).
+template <typename X>
+__device__ __forceinline__ X wave_incl_scan_t(X x) {
+  x += dpp_or_zero<0x111, 0xf>(x);   // row_shr:1
+  x += dpp_or_zero<0x112, 0xf>(x);   // row_shr:2
+  x += dpp_or_zero<0x114, 0xf>(x);   // row_shr:4
+  x += dpp_or_zero<0x118, 0xf>(x);   // row_shr:8
+  x += dpp_or_zero<0x142, 0xa>(x);   // row_bcast:15, rows 1 and 3
+  x += dpp_or_zero<0x143, 0xc>(x);   // row_bcast:31, rows 2 and 3
   return x;
 }
 
-template <int CTRL>
-__device__ __forceinline__ uint32_t dpp_move_u32(uint32_t x) {
-  return (uint32_t)__builtin_amdgcn_mov_dpp((int)x, CTRL, 0xf, 0xf, false);
+__device__ __forceinline__ int64_t wave_incl_scan(int64_t x, int lane) {
+  (void)lane;
+  return wave_incl_scan_t<int64_t>(x);
 }
 
 // The same scan for values whose wave total fits 32 bits.
 __device__ __forceinline__ uint32_t wave_incl_scan32(uint32_t x, int lane) {
-  const int r = lane & 15;
-  uint32_t y;
-  y = dpp_move_u32<0x111>(x);
-  x = r >= 1 ? x + y : x;
-  y = dpp_move_u32<0x112>(x);
-  x = r >= 2 ? x + y : x;
-  y = dpp_move_u32<0x114>(x);
-  x = r >= 4 ? x + y : x;
-  y = dpp_move_u32<0x118>(x);
-  x = r >= 8 ? x + y : x;
-  y = dpp_move_u32<0x142>(x);
-  x = (lane & 16) ? x + y : x;
-  y = dpp_move_u32<0x143>(x);
-  x = lane >= 32 ? x + y : x;
-  return x;
+  (void)lane;
+  return wave_incl_scan_t<uint32_t>(x);
 }
 
 // Lane l's 64-bit value, read by every lane (l wave-uniform).

@@ -159,6 +159,32 @@ def test_plan_parity_tiles_beyond_residency(T, B):
     run_plan([16, 64][:T], [0, 1][:T], 1, [1000] * T, lengths, False)
 
 
+@pytest.mark.parametrize("B", [600, 5000])
+def test_plan_parity_wide_tiles(B):
+    """Tiles whose cost reaches 2^32 bytes (64 rows of 256 KiB per bag) take
+    the planner's 64-bit scan; the batch mixes them with tiles that fit 32
+    bits (bags of one row, and a second field of small rows).  600 bags: one
+    tile; 5,000 bags: 20 tiles of 256 bags in one launch."""
+    rng = np.random.default_rng(13)
+    lengths = np.ones((2, B), np.int64)
+    lengths[0, : B * 3 // 5] = 64
+    lengths[1] = rng.integers(0, 6, size=B)
+    for W, flags in ((0, 0), (977, 0), (977, dpi.DPI_FLAG_EXACT_SPLIT), (1, 0)):
+        run_plan([65536, 16], [0, 1], 0, [1000, 1000], lengths, False, W=W, flags=flags)
+
+
+@pytest.mark.parametrize("flags", [0, dpi.DPI_FLAG_EXACT_SPLIT])
+def test_plan_parity_boundary_products_beyond_64_bits(flags):
+    """A batch whose total cost times the wave count exceeds 2^62 (one-row
+    items of cost 2^31 - 1 bytes: S near 2^51, 4,096 waves), so the wave
+    boundaries take the planner's 128-bit quotients instead of the 64-bit
+    ones; then the same bags under 977 waves (64-bit)."""
+    lengths = np.full((1, 4096), 256, np.int64)
+    lengths[0, ::7] = 3
+    for W in (4096, 977):
+        run_plan([16], [0], 0, [1000], lengths, False, C=1, K=2**31 - 1, W=W, flags=flags)
+
+
 @pytest.mark.parametrize("W", [1, 7, 26 * 4096, 1_000_000, 0])
 def test_plan_onehot_closed_form_wave_counts(W):
     """The closed-form one-hot plan against the oracle at wave counts from one
