@@ -149,10 +149,11 @@ def test_plan_parity_many_tiles_multihot():
 
 @pytest.mark.parametrize("T,B", [(1, 1_600_000), (2, 3_000_000)])
 def test_plan_parity_tiles_beyond_residency(T, B):
-    """Batches of more tiles than fit on the device at once but at most 1024
-    (about 390 tiles of 4096 bags, about 730 of 8192): the one-launch
-    planner's first blocks sum the tiles of the blocks that start later.  Bags
-    of 0..5 ids, split bags under a tight wave count, then the default one."""
+    """One-launch plans of many tiles: about 390 tiles of 4,096 bags (every
+    block resident at once), and about 730 tiles of 8,192 bags, more than the
+    512 blocks of the 32-slab kernel that fit on the device together, so the
+    first blocks sum the tiles of the blocks that start later.  Bags of 0..5
+    ids, split bags under a tight wave count, then the default one."""
     rng = np.random.default_rng(12)
     lengths = rng.integers(0, 6, size=(T, B))
     run_plan([16, 64][:T], [0, 1][:T], 1, [1000] * T, lengths, False, W=50_001, C=2)
