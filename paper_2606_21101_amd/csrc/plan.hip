@@ -378,20 +378,29 @@ __device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk) {
 // on every thread.  UNROLL: groups of slabs unrolled (all of them by default,
 // so that the compiler can issue every group's loads together; fewer keep the
 // registers for a caller that scans afterwards in the same kernel).
-template <int V, int UNROLL = (V < kPlanChunk ? 1 : V / kPlanChunk)>
-__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks, int64_t* sums = nullptr) {
+//
+// KEEP (tiles of one group of slabs): the field bytes and the tile's loaded
+// offsets are the caller's s_f and raw, kept for its scan, which then loads
+// nothing again.
+template <int V, int UNROLL, bool KEEP>
+__device__ __forceinline__ void plan_reduce_block_k(PA pa, int64_t blk, int64_t nblocks, int64_t* sums,
+                                                    FieldBytes* keep_f,
+                                                    SlabRaw<(V < kPlanChunk ? V : kPlanChunk)>* keep_raw) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x;
   constexpr int CH = V < kPlanChunk ? V : kPlanChunk;
+  static_assert(!KEEP || V <= kPlanChunk, "one group of slabs");
   bool bad = false;
 
   int64_t v[4] = {0, 0, 0, 0};   // items, cost, malformed offsets, long bags
   if (p.TB > 0) {
-    __shared__ FieldBytes s_f;
+    __shared__ FieldBytes s_f_own;
+    SlabRaw<CH> raw_own;
+    FieldBytes& s_f = KEEP ? *keep_f : s_f_own;
+    SlabRaw<CH>& raw = KEEP ? *keep_raw : raw_own;
     stage_fields(pa, s_f);
     const int64_t tile0 = blk * (int64_t)kScanThreads * V;
-    SlabRaw<CH> raw;
     slab_load<CH>(pa, tile0 + tid, raw);   // in flight across the setup and the barrier
     bad = plan_setup_block(pa, blk);        // (tile 0: the field info, its loads behind the slabs')
     __syncthreads();
@@ -426,6 +435,11 @@ __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nb
     d.block_sum[nb + blk] = v[1];
     d.block_sum[2 * nb + blk] = flags;
   }
+}
+
+template <int V, int UNROLL = (V < kPlanChunk ? 1 : V / kPlanChunk)>
+__device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks, int64_t* sums = nullptr) {
+  plan_reduce_block_k<V, UNROLL, false>(pa, blk, nblocks, sums, nullptr, nullptr);
 }
 
 // ---------------------------------------------------------------------------
@@ -601,10 +615,20 @@ __device__ __forceinline__ void plan_scan_prologue(PA pa, int64_t blk, FieldByte
   }
 }
 
+// A tile of at most kPlanChunk slabs whose sums fit 32 bits, already scanned
+// inside the tile (local_scan): per slab, each thread's bag's local
+// exclusive item and cost prefixes, items, cost and field.
 template <int V>
+struct LocalSlabs {
+  uint32_t li[V], lc[V], n[V], c[V];
+  int32_t t[V];
+};
+
+template <int V, bool LOCAL = false>
 __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i, int64_t pre_c, int64_t N,
                                                int64_t S, bool err, int64_t nlong, int64_t own_i, int64_t own_c,
-                                               FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw);
+                                               FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw,
+                                               const LocalSlabs<V>* loc = nullptr);
 
 // SINGLE: the whole batch is this block's one group of slabs (V <= kPlanChunk);
 // its sums come straight from the block instead of from plan_reduce, and
@@ -692,10 +716,11 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
 // pre_c cost) and the batch's totals (N items, S cost, malformed offsets,
 // bags longer than kDirectMaxItems items) known.  Block 0 also writes the
 // header and the status words.
-template <int V>
+template <int V, bool LOCAL>
 __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i, int64_t pre_c, int64_t N,
                                                int64_t S, bool err, int64_t nlong, int64_t own_i, int64_t own_c,
-                                               FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw) {
+                                               FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw,
+                                               const LocalSlabs<V>* loc) {
   PPR p = pa->p;
   PDR d = pa->d;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -798,7 +823,29 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     const double margin = (x_hi + 1.0) * 0x1p-45;
     return floor(x_hi + margin) != floor(x_lo - margin);
   };
-  if (own_i >= 0 && own_i <= (int64_t)UINT32_MAX && own_c >= 0 && own_c <= (int64_t)UINT32_MAX) {
+  if constexpr (LOCAL) {
+    // scanned inside the tile before the tile sums were gathered: the tile
+    // prefix added, then the filter
+    (void)raw;
+    (void)own_i;
+    (void)own_c;
+    const double base = (double)pre_c * scale;
+#pragma unroll
+    for (int k = 0; k < V; ++k) {
+      const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
+      const bool valid = bag < p.TB;
+      if (valid && p.prefixes) {
+        d.bib[bag] = pre_i + loc->li[k];
+        d.bcb[bag] = pre_c + loc->lc[k];
+      }
+      if (W == 0) continue;
+      const double x_lo = fma((double)loc->lc[k], scale, base);
+      const double x_hi = fma((double)(loc->lc[k] + loc->c[k]), scale, base);
+      const bool cand = valid && may_hold_target(x_lo, x_hi);
+      collect(cand, bag, pre_i + loc->li[k], pre_c + loc->lc[k], pre_c + loc->lc[k] + loc->c[k], loc->t[k],
+              (int32_t)loc->n[k]);
+    }
+  } else if (own_i >= 0 && own_i <= (int64_t)UINT32_MAX && own_c >= 0 && own_c <= (int64_t)UINT32_MAX) {
     // Narrow tile (block-uniform): every sum inside the tile fits 32 bits, so
     // the costs, scans, wave totals and running sums are 32-bit and a bag's
     // 64-bit prefixes are the tile prefix plus its local ones.  The filter
@@ -1183,6 +1230,44 @@ __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t ta
   own[1] = s_own[1];
 }
 
+// The scan inside a tile of one group of slabs whose sums fit 32 bits, from
+// its loaded offsets: what the narrow scan does before it adds the tile
+// prefix.  Run while the other blocks publish their sums, so that a block
+// polls for them later and its polling loads do not hold up their stores.
+template <int V>
+__device__ __forceinline__ void local_scan(PA pa, const FieldBytes& s_f, const SlabRaw<V>& raw, LocalSlabs<V>& loc) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  __shared__ __align__(16) uint32_t s_w[V][2][kWavesPerBlock];
+  SlabBags32<V> s;
+  slab_cost32<V>(pa, s_f, raw, s);
+  uint32_t xi[V], xc[V];
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    loc.n[k] = s.n[k];
+    loc.c[k] = s.c[k];
+    loc.t[k] = s.t[k];
+    xi[k] = wave_incl_scan32(s.n[k], lane);
+    xc[k] = wave_incl_scan32(s.c[k], lane);
+    if (lane == 63) {
+      s_w[k][0][wv] = xi[k];
+      s_w[k][1][wv] = xc[k];
+    }
+  }
+  __syncthreads();
+  uint32_t run_i = 0, run_c = 0;
+#pragma unroll
+  for (int k = 0; k < V; ++k) {
+    const uint4 wi = *reinterpret_cast<const uint4*>(s_w[k][0]);
+    const uint4 wc = *reinterpret_cast<const uint4*>(s_w[k][1]);
+    const uint32_t bi = (wv > 0 ? wi.x : 0u) + (wv > 1 ? wi.y : 0u) + (wv > 2 ? wi.z : 0u);
+    const uint32_t bc = (wv > 0 ? wc.x : 0u) + (wv > 1 ? wc.y : 0u) + (wv > 2 ? wc.z : 0u);
+    loc.li[k] = run_i + bi + xi[k] - s.n[k];
+    loc.lc[k] = run_c + bc + xc[k] - s.c[k];
+    run_i += wi.x + wi.y + wi.z + wi.w;
+    run_c += wc.x + wc.y + wc.z + wc.w;
+  }
+}
+
 // A block per tile.  SPREAD = false: every block resident at once, each
 // sums its own tile.  SPREAD = true: more tiles than resident blocks; blocks
 // b < p.reduce_blocks (the first to start, all resident together) sum tiles
@@ -1200,11 +1285,21 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
   int64_t* const flags = d.block_sum + 4 * nb + 3;
   const uint64_t tag = (uint64_t)p.plan_id << 32;
 
+  __shared__ FieldBytes s_f;
+  SlabRaw<scan_chunk<V>()> raw;
   // tile sums (tile 0: also the field info), published
+  int64_t mine_i = 0, mine_c = 0;
   if constexpr (!SPREAD) {
     int64_t mine[3];
-    plan_reduce_block<V>(pa, blk, nb, mine);
+    if constexpr (V <= kPlanChunk) {
+      // one group of slabs: the sums' loads and field bytes serve the scan too
+      plan_reduce_block_k<V, 1, true>(pa, blk, nb, mine, &s_f, &raw);
+    } else {
+      plan_reduce_block<V>(pa, blk, nb, mine);
+    }
     if (tid == 0) publish_tile_sums(flags, blk, tag, mine);
+    mine_i = mine[0];
+    mine_c = mine[1];
   } else {
     const int64_t G = p.reduce_blocks;
 #pragma unroll 1
@@ -1216,13 +1311,27 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
     }
   }
 
-  __shared__ FieldBytes s_f;
-  SlabRaw<scan_chunk<V>()> raw;
-  plan_scan_prologue<V>(pa, blk, s_f, raw);   // field bytes, and the first loads of the scan in flight
-  __syncthreads();
-  int64_t v[6], own[2];
-  gather_tile_sums<V>(pa, blk, tag, flags, s_f, v, own);
-  plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], own[0], own[1], s_f, raw);
+  if constexpr (!SPREAD && V <= kPlanChunk) {
+    // the tile's own sums are known (block-uniform): a tile whose sums fit
+    // 32 bits scans now, the rest after the gather as usual
+    const bool narrow = mine_i <= (int64_t)UINT32_MAX && mine_c <= (int64_t)UINT32_MAX;
+    int64_t v[6], own[2];
+    if (narrow) {
+      LocalSlabs<V> loc;
+      local_scan<V>(pa, s_f, raw, loc);
+      gather_tile_sums<V>(pa, blk, tag, flags, s_f, v, own);
+      plan_scan_core<V, true>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], own[0], own[1], s_f, raw, &loc);
+    } else {
+      gather_tile_sums<V>(pa, blk, tag, flags, s_f, v, own);
+      plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], own[0], own[1], s_f, raw);
+    }
+  } else {
+    plan_scan_prologue<V>(pa, blk, s_f, raw);   // field bytes, and the first loads of the scan in flight
+    __syncthreads();
+    int64_t v[6], own[2];
+    gather_tile_sums<V>(pa, blk, tag, flags, s_f, v, own);
+    plan_scan_core<V>(pa, blk, v[0], v[1], v[2], v[3], v[4] != 0, v[5], own[0], own[1], s_f, raw);
+  }
 }
 
 // Blocks of plan_fused_kernel<V, SPREAD> resident at once on the device (0
