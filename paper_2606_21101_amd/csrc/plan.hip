@@ -772,14 +772,18 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
 
   __shared__ Targets g;
   __shared__ BoundaryOut o;
+  // the slow quotients are formed by the first lanes of different waves, so
+  // that their latencies overlap
+  if (tid == kWaveSize) g.scale = W > 0 ? (double)W / (double)S : 0.0;
+  if (tid == 2 * kWaveSize) g.inv_w = W > 0 ? 1.0 / (double)W : 0.0;
+  if (tid == 3 * kWaveSize) {
+    g.slack = W > 0 ? floor_div64((uint64_t)S, 2 * W, (double)S / (double)(2 * W)) : 0;   // S / (2W), exact
+    g.fits64 = mul128(S, W) < ((u128)1 << 62);
+  }
   if (tid == 0) {
     g.W = W;
     g.S = S;
-    g.slack = W > 0 ? S / (2 * W) : 0;
-    g.scale = W > 0 ? (double)W / (double)S : 0.0;
-    g.inv_w = W > 0 ? 1.0 / (double)W : 0.0;
     g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
-    g.fits64 = mul128(S, W) < ((u128)1 << 62);
     o.wib = d.wib;
     o.wave_bag = d.wave_bag;
     o.wbase = d.wbase;
