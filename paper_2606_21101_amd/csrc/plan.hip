@@ -38,6 +38,8 @@
 //   the bag's cost beyond the target is at most floor(S/(2W)).
 // All target arithmetic is exact: comparisons of 128-bit products, with
 // floating point used only for first guesses that are then corrected.
+#include <atomic>
+
 #include "dpi_internal.h"
 #include "wave_scan.h"
 
@@ -1338,20 +1340,24 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
   }
 }
 
-// Blocks of plan_fused_kernel<V, SPREAD> resident at once on the device (0
-// if the runtime cannot say).
+// Blocks of plan_fused_kernel<V, SPREAD> resident at once on the current
+// device (0 if the runtime cannot say), asked once per device.
+constexpr int kCapacityDevices = 64;
 template <int V, bool SPREAD>
 int64_t plan_fused_capacity() {
-  static int64_t cap = -1;
-  if (cap < 0) {
-    int dev = 0, n = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, plan_fused_kernel<V, SPREAD>, kScanThreads, 0) != hipSuccess)
-      n = 0;
-    cap = (int64_t)n * cus;
-  }
-  return cap;
+  static std::atomic<int64_t> cap[kCapacityDevices];   // 0: not asked yet; else capacity + 1
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  std::atomic<int64_t>* slot = dev >= 0 && dev < kCapacityDevices ? &cap[dev] : nullptr;
+  const int64_t known = slot ? slot->load(std::memory_order_relaxed) : 0;
+  if (known > 0) return known - 1;
+  int n = 0, cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, plan_fused_kernel<V, SPREAD>, kScanThreads, 0) != hipSuccess)
+    return 0;   // asked again next time
+  const int64_t c = (int64_t)n * cus;
+  if (slot) slot->store(c + 1, std::memory_order_relaxed);
+  return c;
 }
 
 template <int V>
