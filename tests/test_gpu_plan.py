@@ -313,3 +313,39 @@ def test_bad_offsets_detected_in_multi_tile_batches(T, B, late):
     fl = FusedLookup(tabs)
     plan = fl.plan(torch.from_numpy(offs_np).cuda(), B, total, num_waves=4096)
     assert dpi.dpi_plan_sync_status(plan) == dpi.DPI_ERR_BAD_OFFSETS
+
+
+# Planner fuzz: each case draws a field count, a batch size (so that the tile
+# count lands on one of the planner's paths: one tile, every tile resident,
+# more tiles than resident blocks, beyond 1,024 tiles), a row width and dtype
+# per field, a bag-length law (zeros, Poisson, a few long bags, rows wide
+# enough to make some tiles cost 2^32 bytes), a wave count, chunk size, item
+# cost and the exact-split flag; the plan is compared with the oracle's bit
+# for bit, per-wave arrays included.
+PLAN_FUZZ_BAGS = [1_500, 40_000, 400_000, 1_700_000, 6_000_000, 9_000_000]
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_plan_fuzz(seed):
+    rng = np.random.default_rng(7100 + seed)
+    T = int(rng.integers(1, 9))
+    bags = PLAN_FUZZ_BAGS[seed % len(PLAN_FUZZ_BAGS)]
+    B = max(1, bags // T)
+    dims = [int(rng.choice([4, 16, 64, 128, 1024, 65536 if seed % 4 == 3 else 256])) for _ in range(T)]
+    dtypes = [int(rng.integers(0, 2)) for _ in range(T)]
+    law = seed % 3
+    if law == 0:
+        lengths = rng.integers(0, 4, size=(T, B))
+    elif law == 1:
+        lengths = rng.poisson(float(rng.uniform(1, 30)), size=(T, B)).clip(0, 300)
+    else:
+        lengths = rng.integers(0, 12, size=(T, B))
+        hot = rng.integers(0, T * B, size=8)
+        lengths.reshape(-1)[hot] = rng.integers(500, 5000, size=8)
+    lengths = lengths.astype(np.int64)
+    C = int(rng.choice([0, 1, 8, 32]))
+    K = int(rng.choice([0, 1, 64, 4096]))
+    W = int(rng.choice([0, 1, 977, 65_536, 400_000]))
+    flags = dpi.DPI_FLAG_EXACT_SPLIT if rng.integers(0, 2) else 0
+    print(f"  plan fuzz seed {seed}: T={T} B={B} dims={dims} C={C} K={K} W={W} flags={flags}", flush=True)
+    run_plan(dims, dtypes, int(rng.integers(0, 2)), [1000] * T, lengths, False, C=C, K=K, W=W, flags=flags)
