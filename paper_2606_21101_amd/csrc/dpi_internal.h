@@ -14,7 +14,7 @@ constexpr int kWaveSize = 64;
 constexpr int kBlockThreads = 256;          // 4 independent waves per workgroup
 constexpr int kWavesPerBlock = kBlockThreads / kWaveSize;
 constexpr int kScanThreads = 256;           // plan: threads per block (one bag per thread per slab)
-constexpr int kPlanMaxSlabs = 32;           // most slabs per tile
+constexpr int kPlanMaxSlabs = 64;           // most slabs per tile
 constexpr int kPlanChunk = 8;               // slabs whose offset loads are in flight together
 constexpr int kPlanTargetTiles = 512;       // a tile grows until the batch has at most this many
 constexpr int kPlanDirectTiles = 1024;      // most tiles whose sums every scan block reads itself

@@ -377,9 +377,10 @@ __device__ __forceinline__ bool plan_setup_block(PA pa, int64_t blk) {
 }
 
 // sums (optional): receives the tile's items, cost and malformed | long << 1
-// on every thread.  UNROLL: groups of slabs unrolled (all of them by default,
-// so that the compiler can issue every group's loads together; fewer keep the
-// registers for a caller that scans afterwards in the same kernel).
+// on every thread.  UNROLL: groups of slabs unrolled (by default all of
+// them up to four, so that the compiler can issue those groups' loads
+// together; fewer keep the registers for a caller that scans afterwards in
+// the same kernel).
 //
 // KEEP (tiles of one group of slabs): the field bytes and the tile's loaded
 // offsets are the caller's s_f and raw, kept for its scan, which then loads
@@ -439,7 +440,7 @@ __device__ __forceinline__ void plan_reduce_block_k(PA pa, int64_t blk, int64_t 
   }
 }
 
-template <int V, int UNROLL = (V < kPlanChunk ? 1 : V / kPlanChunk)>
+template <int V, int UNROLL = (V < kPlanChunk ? 1 : (V / kPlanChunk < 4 ? V / kPlanChunk : 4))>
 __device__ __forceinline__ void plan_reduce_block(PA pa, int64_t blk, int64_t nblocks, int64_t* sums = nullptr) {
   plan_reduce_block_k<V, UNROLL, false>(pa, blk, nblocks, sums, nullptr, nullptr);
 }
@@ -1414,6 +1415,7 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
     case 8: return launch_plan_v<8>(a, s);
     case 16: return launch_plan_v<16>(a, s);
     case 32: return launch_plan_v<32>(a, s);
+    case 64: return launch_plan_v<64>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
