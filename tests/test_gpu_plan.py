@@ -125,12 +125,12 @@ def test_plan_parity_large_onehot_batch():
     assert got["header"][9] == 2 * B
 
 
-@pytest.mark.parametrize("T,B", [(1, 1024 * 8192), (1, 1024 * 8192 + 1), (3, 3_000_000)])
+@pytest.mark.parametrize("T,B", [(1, 1024 * 16384), (1, 1024 * 16384 + 1), (3, 6_000_000)])
 def test_plan_parity_tile_counts(T, B):
-    """Batches with explicit unit offsets around the largest tile count whose
-    sums every scan block reads itself (1024 tiles of 8192 bags): at it, one
-    past it, and well beyond it, where a separate launch scans the tile sums.
-    The same batches without offsets take the closed-form one-hot plan."""
+    """Batches with explicit unit offsets around the largest tile count that
+    plans in one launch (1024 tiles of 16,384 bags): at it, one past it, and
+    beyond it, where a separate launch scans the tile sums.  The same batches
+    without offsets take the closed-form one-hot plan."""
     lengths = np.ones((T, B), np.int64)
     for onehot in (False, True):
         got = run_plan([16, 8, 4][:T], [0, 1, 0][:T], 0, [1000] * T, lengths, onehot, W=4099)
@@ -138,20 +138,20 @@ def test_plan_parity_tile_counts(T, B):
 
 
 def test_plan_parity_many_tiles_multihot():
-    """Explicit offsets over 9 M bags (about 1100 tiles): lengths 0..5, some
+    """Explicit offsets over 18 M bags (about 1100 tiles): lengths 0..5, some
     empty bags, the tile-sum launch and split bags under a tight wave count."""
     rng = np.random.default_rng(11)
-    lengths = rng.integers(0, 6, size=(3, 3_000_000))
+    lengths = rng.integers(0, 6, size=(3, 6_000_000))
     run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False, W=70_001, C=2,
              flags=dpi.DPI_FLAG_EXACT_SPLIT)
     run_plan([16, 8, 64], [0, 1, 1], 1, [1000] * 3, lengths, False)
 
 
-@pytest.mark.parametrize("T,B", [(1, 1_600_000), (2, 3_000_000)])
+@pytest.mark.parametrize("T,B", [(1, 1_600_000), (2, 4_500_000)])
 def test_plan_parity_tiles_beyond_residency(T, B):
     """One-launch plans of many tiles: about 390 tiles of 4,096 bags (every
-    block resident at once), and about 730 tiles of 8,192 bags, more than the
-    512 blocks of the 32-slab kernel that fit on the device together, so the
+    block resident at once), and about 550 tiles of 16,384 bags, more than the
+    512 blocks of the 64-slab kernel that fit on the device together, so the
     first blocks sum the tiles of the blocks that start later.  Bags of 0..5
     ids, split bags under a tight wave count, then the default one."""
     rng = np.random.default_rng(12)
@@ -293,12 +293,12 @@ def test_superseded_plan_is_refused():
     assert dpi.dpi_plan_export(second)["header"][2] == 2
 
 
-@pytest.mark.parametrize("T,B,late", [(2, 100_000, False), (1, 9_000_000, False), (1, 6_000_000, False),
-                                      (1, 6_000_000, True)])
+@pytest.mark.parametrize("T,B,late", [(2, 100_000, False), (1, 18_000_000, False), (1, 9_000_000, False),
+                                      (1, 9_000_000, True)])
 def test_bad_offsets_detected_in_multi_tile_batches(T, B, late):
     """Malformed offsets seen by several threads of one tile, in batches planned
-    by one launch (fewer than 1024 tiles; 6 M bags are more tiles than fit on
-    the device at once) and by three (more): the plan must reject them.  (A
+    by one launch (at most 1024 tiles; 9 M bags are more tiles than fit on the
+    device at once) and by three (more): the plan must reject them.  (A
     tile's flag once summed the count of threads that saw a malformed bag into
     its malformed bit, so two such threads cleared it.)  late: the malformed
     bags sit in a tile past the first blocks' own, summed by a block that
@@ -322,7 +322,7 @@ def test_bad_offsets_detected_in_multi_tile_batches(T, B, late):
 # enough to make some tiles cost 2^32 bytes), a wave count, chunk size, item
 # cost and the exact-split flag; the plan is compared with the oracle's bit
 # for bit, per-wave arrays included.
-PLAN_FUZZ_BAGS = [1_500, 40_000, 400_000, 1_700_000, 6_000_000, 9_000_000]
+PLAN_FUZZ_BAGS = [1_500, 40_000, 400_000, 1_700_000, 9_000_000, 18_000_000]
 
 
 @pytest.mark.parametrize("seed", range(12))
