@@ -76,7 +76,7 @@ Layout make_layout(int64_t T, int64_t B, int64_t total_ids, const dpi_plan_opts&
   L.tinfo = take(T * sizeof(TableInfo));
   L.col_base = take((T + 1) * sizeof(int64_t));
   L.id_base = take((T + 1) * sizeof(int64_t));
-  L.block_sum = take((10 * nblk + 3) * sizeof(int64_t));
+  L.block_sum = take((12 * nblk + 3) * sizeof(int64_t));
   L.bib = take(prefixes ? (TB + 1) * sizeof(int64_t) : 0);
   L.bcb = take(prefixes ? (TB + 1) * sizeof(int64_t) : 0);
   L.wib = take((waves_req + 1) * sizeof(int64_t));

@@ -85,9 +85,10 @@ struct PlanDev {
   TableInfo* tinfo;      // [T]
   int64_t* col_base;     // [T+1]
   int64_t* id_base;      // [T+1]
-  int64_t* block_sum;    // [10 * nblk + 3]: per tile items, then costs, then malformed-offset flags; three
+  int64_t* block_sum;    // [12 * nblk + 3]: per tile items, then costs, then malformed-offset flags; three
                          // totals (when the tiles are scanned by their own launch); per tile split bags;
-                         // per tile six words of published sums (one-launch planning)
+                         // published sums (one-launch planning): per tile a pair of words, then per
+                         // tile six words of the long form
   int64_t* bib;          // bag_item_base [TB+1]
   int64_t* bcb;          // bag_cost_base [TB+1]
   int64_t* wib;          // wave_item_begin [Wreq+1]

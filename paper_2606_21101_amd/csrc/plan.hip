@@ -55,6 +55,13 @@ typedef const __attribute__((address_space(4))) PlanDev& PDR;
 
 __device__ __forceinline__ u128 mul128(int64_t a, int64_t b) { return (u128)(uint64_t)a * (uint64_t)b; }
 
+// A value every lane of the wave holds, moved to scalar registers.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+  return (int64_t)((uint64_t)hi << 32 | lo);
+}
+
 // A double near a 128-bit value (two roundings; callers only use it as a
 // first guess and then correct with exact comparisons).
 __device__ __forceinline__ double approx_u128(u128 x) {
@@ -313,17 +320,31 @@ __device__ __forceinline__ void slab_cost32(PA pa, const FieldBytes& f, const Sl
   PPR p = pa->p;
   const uint32_t C = (uint32_t)p.C, K = (uint32_t)p.K;
   const int32_t sh = p.c_shift;
+  uint32_t row[CH], out[CH], L[CH], n[CH];
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {   // as slab_cost: reads together, no branch around them
+    row[k] = (uint32_t)f.row[r.t[k]];
+    out[k] = (uint32_t)f.out[r.t[k]];
+  }
 #pragma unroll
   for (int k = 0; k < CH; ++k) {
     const bool bad = (r.first[k] & (r.lo[k] != 0)) | (r.hi[k] < r.lo[k]);
-    const uint32_t L = bad ? 0u : (uint32_t)(r.hi[k] - r.lo[k]);
-    const uint32_t up = L + C - 1u;
-    uint32_t n = sh >= 0 ? up >> sh : up / C;
-    n = n < 1u ? 1u : n;
-    const int t = r.t[k];
-    s.t[k] = t;
-    s.n[k] = r.ok[k] ? n : 0u;
-    s.c[k] = r.ok[k] ? L * (uint32_t)f.row[t] + (uint32_t)f.out[t] + n * K : 0u;
+    L[k] = bad ? 0u : (uint32_t)(r.hi[k] - r.lo[k]);
+  }
+  if (sh >= 0) {
+#pragma unroll
+    for (int k = 0; k < CH; ++k) n[k] = (L[k] + C - 1u) >> sh;
+  } else {
+#pragma unroll
+    for (int k = 0; k < CH; ++k) n[k] = (L[k] + C - 1u) / C;
+  }
+#pragma unroll
+  for (int k = 0; k < CH; ++k) {
+    n[k] = n[k] < 1u ? 1u : n[k];
+    const uint32_t m = 0u - (uint32_t)r.ok[k];
+    s.t[k] = r.t[k];
+    s.n[k] = n[k] & m;
+    s.c[k] = (L[k] * row[k] + out[k] + n[k] * K) & m;
   }
 }
 
@@ -599,7 +620,7 @@ __device__ __forceinline__ void resolve_candidates(BoundaryOut& o, const Targets
   const bool split = lane < count && (g.fits64 ? bag_boundaries<true>(o, g, f, list[lane])
                                                : bag_boundaries<false>(o, g, f, list[lane]));
   const uint64_t m = __ballot(split);
-  if (m != 0 && lane == 0) atomicAdd(&o.splits, (unsigned long long)__popcll(m));
+  o.splits += (unsigned long long)__popcll(m);   // wave-uniform
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   __builtin_amdgcn_wave_barrier();
 }
@@ -704,6 +725,7 @@ __device__ __forceinline__ void plan_scan_block(PA pa, int64_t blk, bool setup_b
     own_c = bs[nb + blk];
   } else {
     // plan_tiles left exclusive prefixes in place and the totals after them
+    __syncthreads();   // field bytes
     pre_i = bs[blk];
     pre_c = bs[nb + blk];
     N = bs[3 * nb];
@@ -773,32 +795,39 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     return;
   }
 
-  __shared__ Targets g;
-  __shared__ BoundaryOut o;
-  // the slow quotients are formed by the first lanes of different waves, so
-  // that their latencies overlap
-  if (tid == kWaveSize) g.scale = W > 0 ? (double)W / (double)S : 0.0;
-  if (tid == 2 * kWaveSize) g.inv_w = W > 0 ? 1.0 / (double)W : 0.0;
-  if (tid == 3 * kWaveSize) {
-    g.slack = W > 0 ? floor_div64((uint64_t)S, 2 * W, (double)S / (double)(2 * W)) : 0;   // S / (2W), exact
-    g.fits64 = mul128(S, W) < ((u128)1 << 62);
+  // The targets' quotients and the output pointers, per wave: no barrier
+  // before the filter (every caller has published the field bytes with a
+  // barrier of its own).  S and W are block-uniform; read once per wave.
+  const int64_t Su = uniform64(S), Wu = uniform64(W);
+  Targets g;
+  g.W = Wu;
+  g.S = Su;
+  g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
+  {
+    // three independent divisions, no branch between them (W > 0 implies
+    // S > 0: every bag costs at least its output row)
+    const bool any = Wu > 0;
+    const int64_t Sd = any ? Su : 1, Wd = any ? Wu : 1;
+    const double scale = (double)Wu / (double)Sd;   // 0 when W = 0
+    const double inv_w = 1.0 / (double)Wd;
+    const double half = (double)Sd / (double)(2 * Wd);
+    const int64_t slack = floor_div64((uint64_t)Sd, 2 * Wd, half);   // S / (2W), exact
+    g.scale = scale;
+    g.inv_w = any ? inv_w : 0.0;
+    g.slack = any ? slack : 0;
   }
-  if (tid == 0) {
-    g.W = W;
-    g.S = S;
-    g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
-    o.wib = d.wib;
-    o.wave_bag = d.wave_bag;
-    o.wbase = d.wbase;
-    o.head_first = d.head_first;
-    o.split_pieces = d.split_pieces;
-    o.split_last = d.split_last;
-    o.tickets = d.tickets;
-    o.C = p.C;
-    o.K = p.K;
-    o.splits = 0;
-  }
-  __syncthreads();   // publishes the field bytes, g and o
+  g.fits64 = mul128(Su, Wu) < ((u128)1 << 62);
+  BoundaryOut o;
+  o.wib = d.wib;
+  o.wave_bag = d.wave_bag;
+  o.wbase = d.wbase;
+  o.head_first = d.head_first;
+  o.split_pieces = d.split_pieces;
+  o.split_last = d.split_last;
+  o.tickets = d.tickets;
+  o.C = p.C;
+  o.K = p.K;
+  o.splits = 0;   // this wave's split bags
   const double scale = g.scale;
   __shared__ Cand s_cand[kWavesPerBlock][kWaveSize];
   int ncand = 0;   // collected candidates of this wave (wave-uniform)
@@ -837,20 +866,30 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     (void)own_i;
     (void)own_c;
     const double base = (double)pre_c * scale;
+    const int64_t TB = p.TB;
+    if (p.prefixes) {   // block-uniform
 #pragma unroll
-    for (int k = 0; k < V; ++k) {
-      const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
-      const bool valid = bag < p.TB;
-      if (valid && p.prefixes) {
-        d.bib[bag] = pre_i + loc->li[k];
-        d.bcb[bag] = pre_c + loc->lc[k];
+      for (int k = 0; k < V; ++k) {
+        const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
+        if (bag < TB) {
+          d.bib[bag] = pre_i + loc->li[k];
+          d.bcb[bag] = pre_c + loc->lc[k];
+        }
       }
-      if (W == 0) continue;
-      const double x_lo = fma((double)loc->lc[k], scale, base);
-      const double x_hi = fma((double)(loc->lc[k] + loc->c[k]), scale, base);
-      const bool cand = valid && may_hold_target(x_lo, x_hi);
-      collect(cand, bag, pre_i + loc->li[k], pre_c + loc->lc[k], pre_c + loc->lc[k] + loc->c[k], loc->t[k],
-              (int32_t)loc->n[k]);
+    }
+    if (W > 0) {
+      // every slab's filter first (straight-line), then the collection
+      bool cand[V];
+#pragma unroll
+      for (int k = 0; k < V; ++k) {
+        const double x_lo = fma((double)loc->lc[k], scale, base);
+        const double x_hi = fma((double)(loc->lc[k] + loc->c[k]), scale, base);
+        cand[k] = tile0 + (int64_t)k * kScanThreads + tid < TB && may_hold_target(x_lo, x_hi);
+      }
+#pragma unroll
+      for (int k = 0; k < V; ++k)
+        collect(cand[k], tile0 + (int64_t)k * kScanThreads + tid, pre_i + loc->li[k], pre_c + loc->lc[k],
+                pre_c + loc->lc[k] + loc->c[k], loc->t[k], (int32_t)loc->n[k]);
     }
   } else if (own_i >= 0 && own_i <= (int64_t)UINT32_MAX && own_c >= 0 && own_c <= (int64_t)UINT32_MAX) {
     // Narrow tile (block-uniform): every sum inside the tile fits 32 bits, so
@@ -860,6 +899,8 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     // size 2^-53, inside the same bound.
     __shared__ __align__(16) uint32_t s_w32[V][2][kWavesPerBlock];
     const double base = (double)pre_c * scale;
+    const int64_t TB = p.TB;
+    const bool prefixes = p.prefixes != 0;
     uint32_t run_i = 0, run_c = 0;
 #pragma unroll 1
     for (int c0 = 0; c0 < V; c0 += CH) {
@@ -877,26 +918,38 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
         }
       }
       __syncthreads();   // every slab of the group has its own LDS slots: one barrier per group
+      // the group's prefixes and filters in straight-line code, then the
+      // prefix stores and the collection
+      uint32_t li[CH], lc[CH];
+      bool cand[CH];
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
         const uint4 wi = *reinterpret_cast<const uint4*>(s_w32[c0 + k][0]);
         const uint4 wc = *reinterpret_cast<const uint4*>(s_w32[c0 + k][1]);
         const uint32_t bi = (wv > 0 ? wi.x : 0u) + (wv > 1 ? wi.y : 0u) + (wv > 2 ? wi.z : 0u);
         const uint32_t bc = (wv > 0 ? wc.x : 0u) + (wv > 1 ? wc.y : 0u) + (wv > 2 ? wc.z : 0u);
-        const uint32_t li = run_i + bi + xi[k] - s.n[k];   // local exclusive prefixes
-        const uint32_t lc = run_c + bc + xc[k] - s.c[k];
+        li[k] = run_i + bi + xi[k] - s.n[k];   // local exclusive prefixes
+        lc[k] = run_c + bc + xc[k] - s.c[k];
         run_i += wi.x + wi.y + wi.z + wi.w;
         run_c += wc.x + wc.y + wc.z + wc.w;
-        const int64_t bag = tile0 + (int64_t)(c0 + k) * kScanThreads + tid;
-        const bool valid = bag < p.TB;
-        if (valid && p.prefixes) {
-          d.bib[bag] = pre_i + li;
-          d.bcb[bag] = pre_c + lc;
+        const double x_lo = fma((double)lc[k], scale, base), x_hi = fma((double)(lc[k] + s.c[k]), scale, base);
+        cand[k] = tile0 + (int64_t)(c0 + k) * kScanThreads + tid < TB && may_hold_target(x_lo, x_hi);
+      }
+      if (prefixes) {   // block-uniform
+#pragma unroll
+        for (int k = 0; k < CH; ++k) {
+          const int64_t bag = tile0 + (int64_t)(c0 + k) * kScanThreads + tid;
+          if (bag < TB) {
+            d.bib[bag] = pre_i + li[k];
+            d.bcb[bag] = pre_c + lc[k];
+          }
         }
-        if (W == 0) continue;
-        const double x_lo = fma((double)lc, scale, base), x_hi = fma((double)(lc + s.c[k]), scale, base);
-        const bool cand = valid && may_hold_target(x_lo, x_hi);
-        collect(cand, bag, pre_i + li, pre_c + lc, pre_c + lc + s.c[k], s.t[k], (int32_t)s.n[k]);
+      }
+      if (W > 0) {
+#pragma unroll
+        for (int k = 0; k < CH; ++k)
+          collect(cand[k], tile0 + (int64_t)(c0 + k) * kScanThreads + tid, pre_i + li[k], pre_c + lc[k],
+                  pre_c + lc[k] + s.c[k], s.t[k], (int32_t)s.n[k]);
       }
     }
   } else {
@@ -945,8 +998,15 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     }
   }
   if (ncand > 0) resolve_candidates(o, g, s_f, s_cand[wv], ncand, lane);
+  __shared__ unsigned long long s_splits[kWavesPerBlock];
+  if (lane == 0) s_splits[wv] = o.splits;
   __syncthreads();
-  if (tid == 0) tile_splits[blk] = (int64_t)o.splits;
+  if (tid == 0) {
+    unsigned long long n = 0;
+#pragma unroll
+    for (int w = 0; w < kWavesPerBlock; ++w) n += s_splits[w];
+    tile_splits[blk] = (int64_t)n;
+  }
 }
 
 template <int V>
@@ -956,7 +1016,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_reduce_kernel(const PlanArg
 }
 
 template <int V>
-__global__ __launch_bounds__(kScanThreads) void plan_scan_kernel(const PlanArgs args) {
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2))) void plan_scan_kernel(const PlanArgs args) {
   (void)args;
   const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
   __shared__ FieldBytes s_f;
@@ -1097,7 +1157,6 @@ __global__ __launch_bounds__(kScanThreads) void plan_onehot_kernel(const PlanArg
 // relies on another block's writes other than the published sums: the header
 // and each per-wave entry have a single writer.
 // ---------------------------------------------------------------------------
-constexpr int kTileWords = 6;   // items, cost, malformed | long << 1: two words each
 constexpr int kPlanSpinLimit = 4096;   // polls of a tile's flag before summing the tile here
 
 // Sums of tile j computed by one thread: items, cost, and the malformed and
@@ -1138,27 +1197,43 @@ __device__ int64_t tile_sums_serial(PA pa, const FieldBytes& f, int64_t j, int64
 }
 
 // Publishes tile blk's sums (items, cost, malformed | long << 1) as tagged
-// words; one thread.
-__device__ __forceinline__ void publish_tile_sums(int64_t* flags, int64_t blk, uint64_t tag,
+// words (one thread).  Short form, the usual case: one pair of words,
+// items and cost, when the items fit 32 bits, the cost 31 bits and the
+// flags are clear.  Otherwise the long form: six words (each sum's two
+// halves), after every tile's pair, and a pair whose cost word has bit 31
+// set.  A reader of the pair reads the long form only when it sees that bit.
+constexpr int kTileWords = 6;             // long form
+constexpr uint32_t kLongForm = 0x80000000u;
+
+__device__ __forceinline__ void publish_tile_sums(int64_t* flags, int64_t nb, int64_t blk, uint64_t tag,
                                                   const int64_t (&mine)[3]) {
-  uint64_t* w = reinterpret_cast<uint64_t*>(flags) + blk * kTileWords;
+  uint64_t* const pair = reinterpret_cast<uint64_t*>(flags) + 2 * blk;
+  const bool shrt = (uint64_t)mine[0] <= 0xffffffffu && (uint64_t)mine[1] < kLongForm && mine[2] == 0;
+  if (!shrt) {
+    uint64_t* const w = reinterpret_cast<uint64_t*>(flags) + 2 * nb + blk * kTileWords;
 #pragma unroll
-  for (int q = 0; q < 3; ++q) {
-    __hip_atomic_store(w + 2 * q, tag | ((uint64_t)mine[q] & 0xffffffffu), __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-    __hip_atomic_store(w + 2 * q + 1, tag | ((uint64_t)mine[q] >> 32), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    for (int q = 0; q < 3; ++q) {
+      __hip_atomic_store(w + 2 * q, tag | ((uint64_t)mine[q] & 0xffffffffu), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(w + 2 * q + 1, tag | ((uint64_t)mine[q] >> 32), __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
   }
+  __hip_atomic_store(pair, tag | (shrt ? (uint64_t)mine[0] : 0u), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __hip_atomic_store(pair + 1, tag | (shrt ? (uint64_t)mine[1] : (uint64_t)kLongForm), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Every tile's published sums, gathered for tile blk (thread i takes tiles i,
 // i + 256, ...): v = prefix items, prefix cost, items, cost, malformed tiles,
 // long bags, block-reduced on every thread; own = tile blk's items and cost.
-// A thread requests all of its tiles' words at once, three 16-byte loads per
+// A thread requests all of its tiles' pairs at once, one 16-byte load per
 // tile at agent scope (sc1: served past the XCD's L2, as an agent-scope
-// atomic load is; every 8-byte word carries its own tag, so a pair need not
-// be read atomically), so the usual case -- every tile published -- costs one
-// round trip, and each further polling round one more for all of the
-// thread's tiles still missing.
+// atomic load is; every 8-byte word carries its own tag, so the pair need not
+// be read atomically), so the usual case -- every tile published in the short
+// form -- costs one round trip, and each further polling round one more for
+// all of the thread's tiles still missing.  A long form is polled by its
+// thread alone.
 template <int V>
 __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t tag, const int64_t* flags,
                                                  const FieldBytes& s_f, int64_t (&v)[6], int64_t (&own)[2]) {
@@ -1167,27 +1242,20 @@ __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t ta
   const int tid = threadIdx.x;
   const int64_t nb = pa->p.nblk;
   constexpr int kPer = kPlanDirectTiles / kScanThreads;
+  const uint32_t tag_hi = (uint32_t)(tag >> 32);
   __shared__ int64_t s_own[2];
   const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<int64_t*>(flags), (short)0, (int)(nb * kTileWords * 8), 0x00020000);
-  i32x4 raw_w[kPer][kTileWords / 2];
+      const_cast<int64_t*>(flags), (short)0, (int)(nb * (2 + kTileWords) * 8), 0x00020000);
+  i32x4 pr[kPer];
   bool ready[kPer];
-  auto load_tile = [&](int m) {
+  auto load_pair = [&](int m) {
     const int64_t j = min(tid + (int64_t)m * kScanThreads, nb - 1);
-#pragma unroll
-    for (int q = 0; q < kTileWords / 2; ++q)
-      raw_w[m][q] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)(j * kTileWords * 8 + 16 * q), 0, kSc1);
+    pr[m] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, (int)(j * 16), 0, kSc1);
   };
-  auto tagged = [&](int m) {
-    bool ok = true;
-#pragma unroll
-    for (int q = 0; q < kTileWords / 2; ++q) ok &= (uint32_t)raw_w[m][q].y == (uint32_t)(tag >> 32) &&
-                                                   (uint32_t)raw_w[m][q].w == (uint32_t)(tag >> 32);
-    return ok;
-  };
+  auto tagged = [&](int m) { return (uint32_t)pr[m].y == tag_hi && (uint32_t)pr[m].w == tag_hi; };
 #pragma unroll
   for (int m = 0; m < kPer; ++m)
-    if ((int64_t)m * kScanThreads < nb) load_tile(m);   // block-uniform
+    if ((int64_t)m * kScanThreads < nb) load_pair(m);   // block-uniform
 #pragma unroll
   for (int m = 0; m < kPer; ++m) ready[m] = tid + (int64_t)m * kScanThreads >= nb || tagged(m);
   // tiles not yet published: every missing tile of the thread polled again
@@ -1200,7 +1268,7 @@ __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t ta
     __builtin_amdgcn_s_sleep(1);
 #pragma unroll
     for (int m = 0; m < kPer; ++m)
-      if (!ready[m]) load_tile(m);
+      if (!ready[m]) load_pair(m);
 #pragma unroll
     for (int m = 0; m < kPer; ++m) ready[m] = ready[m] || tagged(m);
   }
@@ -1211,15 +1279,27 @@ __device__ __forceinline__ void gather_tile_sums(PA pa, int64_t blk, uint64_t ta
     if ((int64_t)m * kScanThreads >= nb) break;
     const int64_t j = tid + (int64_t)m * kScanThreads;
     if (j >= nb) continue;
-    int64_t si, sc, se;
-    if (ready[m]) {
-      const i32x4 r0 = raw_w[m][0], r1 = raw_w[m][1], r2 = raw_w[m][2];
-      si = (int64_t)((uint64_t)(uint32_t)r0.x | (uint64_t)(uint32_t)r0.z << 32);
-      sc = (int64_t)((uint64_t)(uint32_t)r1.x | (uint64_t)(uint32_t)r1.z << 32);
-      se = (int64_t)((uint64_t)(uint32_t)r2.x | (uint64_t)(uint32_t)r2.z << 32);
-    } else {
-      se = tile_sums_serial<V>(pa, s_f, j, si, sc);   // not published in time: summed here
+    int64_t si = (uint32_t)pr[m].x, sc = (uint32_t)pr[m].z, se = 0;
+    bool have = ready[m] && ((uint32_t)pr[m].z & kLongForm) == 0;
+    if (ready[m] && !have) {
+      // the long form (bounded poll; its words may land after the pair)
+      const int base = (int)((2 * nb + j * kTileWords) * 8);
+      for (int spin = 0; spin < kPlanSpinLimit && !have; ++spin) {
+        const i32x4 r0 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, base, 0, kSc1);
+        const i32x4 r1 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, base + 16, 0, kSc1);
+        const i32x4 r2 = __builtin_amdgcn_raw_buffer_load_b128(rsrc, base + 32, 0, kSc1);
+        have = (uint32_t)r0.y == tag_hi && (uint32_t)r0.w == tag_hi && (uint32_t)r1.y == tag_hi &&
+               (uint32_t)r1.w == tag_hi && (uint32_t)r2.y == tag_hi && (uint32_t)r2.w == tag_hi;
+        if (have) {
+          si = (int64_t)((uint64_t)(uint32_t)r0.x | (uint64_t)(uint32_t)r0.z << 32);
+          sc = (int64_t)((uint64_t)(uint32_t)r1.x | (uint64_t)(uint32_t)r1.z << 32);
+          se = (int64_t)((uint64_t)(uint32_t)r2.x | (uint64_t)(uint32_t)r2.z << 32);
+        } else {
+          __builtin_amdgcn_s_sleep(1);
+        }
+      }
     }
+    if (!have) se = tile_sums_serial<V>(pa, s_f, j, si, sc);   // not published in time: summed here
     v[0] += j < blk ? si : 0;
     v[1] += j < blk ? sc : 0;
     v[2] += si;
@@ -1280,9 +1360,10 @@ __device__ __forceinline__ void local_scan(PA pa, const FieldBytes& s_f, const S
 // b < p.reduce_blocks (the first to start, all resident together) sum tiles
 // b, b + reduce_blocks, ... and publish all of them before any block waits,
 // and the later blocks, which start as the first ones finish, only gather
-// and scan.
+// and scan.  At least two waves per SIMD, so that every tile count the
+// planner picks (at most 512 tiles) stays resident.
 template <int V, bool SPREAD>
-__global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs args) {
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(2))) void plan_fused_kernel(const PlanArgs args) {
   (void)args;
   const PA pa = (PA)__builtin_amdgcn_kernarg_segment_ptr();
   PPR p = pa->p;
@@ -1304,7 +1385,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
     } else {
       plan_reduce_block<V>(pa, blk, nb, mine);
     }
-    if (tid == 0) publish_tile_sums(flags, blk, tag, mine);
+    if (tid == 0) publish_tile_sums(flags, nb, blk, tag, mine);
     mine_i = mine[0];
     mine_c = mine[1];
   } else {
@@ -1313,7 +1394,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_fused_kernel(const PlanArgs
     for (int64_t j = blk; blk < G && j < nb; j += G) {
       int64_t mine[3];
       plan_reduce_block<V, 1>(pa, j, nb, mine);
-      if (tid == 0) publish_tile_sums(flags, j, tag, mine);
+      if (tid == 0) publish_tile_sums(flags, nb, j, tag, mine);
       __syncthreads();   // the next tile's sums reuse the block's LDS
     }
   }

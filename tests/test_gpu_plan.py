@@ -174,6 +174,20 @@ def test_plan_parity_wide_tiles(B):
         run_plan([65536, 16], [0, 1], 0, [1000, 1000], lengths, False, W=W, flags=flags)
 
 
+@pytest.mark.parametrize("W", [0, 977])
+def test_plan_parity_long_form_tile_sums(W):
+    """Tiles whose cost lies between 2^31 and 2^32 bytes (40 rows of 256 KiB
+    per bag, 256 bags per tile): their scan stays 32-bit, but their sums do
+    not fit the short published form and take the long one, beside tiles in
+    the short form (a second field of small rows), in one launch of 40 tiles."""
+    rng = np.random.default_rng(17)
+    B = 5000
+    lengths = np.empty((2, B), np.int64)
+    lengths[0] = 40
+    lengths[1] = rng.integers(0, 6, size=B)
+    run_plan([65536, 16], [0, 1], 0, [1000, 1000], lengths, False, W=W)
+
+
 @pytest.mark.parametrize("flags", [0, dpi.DPI_FLAG_EXACT_SPLIT])
 def test_plan_parity_boundary_products_beyond_64_bits(flags):
     """A batch whose total cost times the wave count exceeds 2^62 (one-row
