@@ -237,7 +237,7 @@ struct SlabBags {
 };
 
 template <int CH>
-__device__ __forceinline__ void slab_load(PA pa, int64_t first, SlabRaw<CH>& r) {
+__device__ __forceinline__ void slab_load(PA pa, int64_t first, SlabRaw<CH>& r, double inv_b) {
   PPR p = pa->p;
   const int64_t TB = p.TB, B = p.B;
   int64_t lc[CH];   // clamped bag number
@@ -247,7 +247,6 @@ __device__ __forceinline__ void slab_load(PA pa, int64_t first, SlabRaw<CH>& r) 
     r.ok[k] = l < TB;
     lc[k] = r.ok[k] ? l : TB - 1;
   }
-  const double inv_b = 1.0 / (double)B;
   if (B >= kScanThreads) {
     // consecutive slabs of a lane cross at most one field start
     int32_t t = field_of(lc[0], B, inv_b);
@@ -301,8 +300,9 @@ __device__ __forceinline__ void slab_cost(PA pa, const FieldBytes& f, const Slab
     const int t = r.t[k];
     const int64_t c = (int64_t)L * f.row[t] + f.out[t] + (int64_t)n * p.K;
     s.t[k] = t;
-    s.n[k] = r.ok[k] ? (int32_t)n : 0;
-    s.c[k] = r.ok[k] ? c : 0;
+    // masked, not selected: a select would become a branch around the reads
+    s.n[k] = (int32_t)n & -(int32_t)r.ok[k];
+    s.c[k] = c & -(int64_t)r.ok[k];
   }
 }
 
@@ -425,14 +425,15 @@ __device__ __forceinline__ void plan_reduce_block_k(PA pa, int64_t blk, int64_t 
     SlabRaw<CH>& raw = KEEP ? *keep_raw : raw_own;
     stage_fields(pa, s_f);
     const int64_t tile0 = blk * (int64_t)kScanThreads * V;
-    slab_load<CH>(pa, tile0 + tid, raw);   // in flight across the setup and the barrier
+    const double inv_b = 1.0 / (double)p.B;   // (once: the loop below reuses it)
+    slab_load<CH>(pa, tile0 + tid, raw, inv_b);   // in flight across the setup and the barrier
     bad = plan_setup_block(pa, blk);        // (tile 0: the field info, its loads behind the slabs')
     __syncthreads();
 #pragma unroll UNROLL
     for (int c0 = 0; c0 < V; c0 += CH) {
       SlabBags<CH> s;
       slab_cost<CH>(pa, s_f, raw, s);
-      if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw);
+      if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw, inv_b);
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
         v[0] += s.n[k];
@@ -635,7 +636,7 @@ template <int V>
 __device__ __forceinline__ void plan_scan_prologue(PA pa, int64_t blk, FieldBytes& s_f, SlabRaw<scan_chunk<V>()>& raw) {
   if (pa->p.TB > 0) {
     stage_fields(pa, s_f);
-    slab_load<scan_chunk<V>()>(pa, blk * (int64_t)kScanThreads * V + threadIdx.x, raw);
+    slab_load<scan_chunk<V>()>(pa, blk * (int64_t)kScanThreads * V + threadIdx.x, raw, 1.0 / (double)pa->p.B);
   }
 }
 
@@ -901,12 +902,13 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     const double base = (double)pre_c * scale;
     const int64_t TB = p.TB;
     const bool prefixes = p.prefixes != 0;
+    const double inv_b = 1.0 / (double)p.B;   // (once, not per group)
     uint32_t run_i = 0, run_c = 0;
 #pragma unroll 1
     for (int c0 = 0; c0 < V; c0 += CH) {
       SlabBags32<CH> s;
       slab_cost32<CH>(pa, s_f, raw, s);
-      if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw);   // next group
+      if (c0 + CH < V) slab_load<CH>(pa, tile0 + (int64_t)(c0 + CH) * kScanThreads + tid, raw, inv_b);   // next group
       uint32_t xi[CH], xc[CH];
 #pragma unroll
       for (int k = 0; k < CH; ++k) {
@@ -959,11 +961,12 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
     // path does not cost the narrow one occupancy.
     __shared__ int64_t s_wt[2][kWavesPerBlock];
     int64_t run_i = pre_i, run_c = pre_c;
+    const double inv_b = 1.0 / (double)p.B;
 #pragma unroll 1
     for (int k = 0; k < V; ++k) {
       const int64_t bag = tile0 + (int64_t)k * kScanThreads + tid;
       SlabRaw<1> r1;
-      slab_load<1>(pa, bag, r1);
+      slab_load<1>(pa, bag, r1, inv_b);
       SlabBags<1> s1;
       slab_cost<1>(pa, s_f, r1, s1);
       const int64_t xi = wave_incl_scan(s1.n[0], lane), xc = wave_incl_scan(s1.c[0], lane);
