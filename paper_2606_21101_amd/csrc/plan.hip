@@ -122,6 +122,10 @@ template <> struct Quot<false> {
   static __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t den, double inv) {
     return ceil_div128((u128)(uint64_t)num, den, inv);
   }
+  // a * b <= c (a, b, c >= 0)
+  static __device__ __forceinline__ bool mul_le(int64_t a, int64_t b, int64_t c) {
+    return mul128(a, b) <= (u128)(uint64_t)c;
+  }
 };
 template <> struct Quot<true> {
   static __device__ __forceinline__ int64_t floor_mul_div(int64_t a, int64_t b, int64_t den, double g) {
@@ -132,6 +136,9 @@ template <> struct Quot<true> {
   }
   static __device__ __forceinline__ int64_t ceil_div(int64_t num, int64_t den, double inv) {
     return ceil_div64((uint64_t)num, den, inv);
+  }
+  static __device__ __forceinline__ bool mul_le(int64_t a, int64_t b, int64_t c) {
+    return mul64(a, b) <= (uint64_t)c;
   }
 };
 
@@ -525,7 +532,7 @@ __global__ __launch_bounds__(kScanThreads) void plan_tiles_kernel(const PlanArgs
 // ---------------------------------------------------------------------------
 // Wave targets of a plan: c_w = ceil(w*S/W) for w = 1..W (shared by a block).
 struct Targets {
-  int64_t W, S, slack;
+  int64_t W, S;
   double scale;     // W / S
   double inv_w;     // 1 / W
   bool exact;       // no snapping of starts to bag ends
@@ -581,7 +588,10 @@ __device__ __forceinline__ bool bag_boundaries(const BoundaryOut& o, const Targe
     if (j > n - 1) j = n;
     bool inside = j < n;
     int64_t begin = cd.ibase + j;
-    if (inside && !g.exact && E_hi - c <= g.slack) {
+    // snapped to the bag's end when that lies within half a wave's cost:
+    // E_hi - c <= floor(S / 2W), i.e. (E_hi - c) * 2W <= S (c <= E_hi, and
+    // with 64-bit quotients (E_hi - c) * 2W <= 2SW < 2^63)
+    if (inside && !g.exact && Q::mul_le(E_hi - c, 2 * W, S)) {
       inside = false;
       begin = cd.ibase + n;
     }
@@ -805,17 +815,13 @@ __device__ __forceinline__ void plan_scan_core(PA pa, int64_t blk, int64_t pre_i
   g.S = Su;
   g.exact = (p.flags & DPI_FLAG_EXACT_SPLIT) != 0;
   {
-    // three independent divisions, no branch between them (W > 0 implies
+    // two independent divisions, no branch between them (W > 0 implies
     // S > 0: every bag costs at least its output row)
     const bool any = Wu > 0;
-    const int64_t Sd = any ? Su : 1, Wd = any ? Wu : 1;
-    const double scale = (double)Wu / (double)Sd;   // 0 when W = 0
-    const double inv_w = 1.0 / (double)Wd;
-    const double half = (double)Sd / (double)(2 * Wd);
-    const int64_t slack = floor_div64((uint64_t)Sd, 2 * Wd, half);   // S / (2W), exact
+    const double scale = (double)Wu / (double)(any ? Su : 1);   // 0 when W = 0
+    const double inv_w = 1.0 / (double)(any ? Wu : 1);
     g.scale = scale;
     g.inv_w = any ? inv_w : 0.0;
-    g.slack = any ? slack : 0;
   }
   g.fits64 = mul128(Su, Wu) < ((u128)1 << 62);
   BoundaryOut o;
