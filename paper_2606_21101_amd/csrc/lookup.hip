@@ -121,8 +121,17 @@ __device__ __forceinline__ int pool_bags_coop(KA a, int64_t t, int64_t b_lo, int
 // buffer range check instead of a branch per row, ids are checked once per
 // group, and mean bags divide by reciprocal and correction; the other kernels
 // keep the branch-per-row form, which holds their registers lower.
-template <typename TIN, typename TOUT, int LPR, bool BUF, bool LEAN = false, int U = kUnroll>
+//
+// SPAN (LEAN only): a group runs on past the end of the current bag into the
+// next one (never beyond it), so that a slot keeps up to U rows in flight
+// across bag ends; each row is added to the accumulator of its bag (the
+// current one, or the next one's, which becomes current when the bag closes).
+// Used for 8-lane rows (bags of about ten rows, where groups cut at bag ends
+// held five rows on average); it doubles the adds, which costs more than it
+// gains where the adds already bound the kernel (16-lane rows).
+template <typename TIN, typename TOUT, int LPR, bool BUF, bool LEAN = false, int U = kUnroll, bool SPAN = false>
 __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
+  static_assert(!SPAN || LEAN, "spanning groups need the single-row-class kernel's masked loads");
   constexpr int EPL = In<TIN>::EPL;
   constexpr int G = kWaveSize / LPR;
   a = uni(a);
@@ -174,10 +183,14 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
     const int32_t r_end = off[endb];
     int32_t bstart = r;
     int32_t bend = cur < endb ? off[cur + 1] : r;
+    // SPAN: the end of the bag after cur (bend when cur is the slot's last)
+    int32_t bnext = SPAN ? (cur + 1 < endb ? off[cur + 2] : bend) : 0;
     TOUT* optr = out_lane + (tb0 + cur) * ostride;   // output row of bag cur
-    float acc[EPL];
+    float acc[EPL], acc2[SPAN ? EPL : 1];
 #pragma unroll
     for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
+#pragma unroll
+    for (int q = 0; q < (SPAN ? EPL : 1); ++q) acc2[q] = 0.f;
 
     // close the current bag (pool, store, reset) and every empty bag after it
     // until the stream position r lies inside a bag; the bound on cur only
@@ -195,12 +208,26 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
           }
         }
         if (col) store_lane<TOUT, EPL>(LEAN ? optr : out_lane + (tb0 + cur) * ostride, acc, vec);
+        if constexpr (SPAN) {
+          // the next bag's rows summed so far become the current sum
 #pragma unroll
-        for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
+          for (int q = 0; q < EPL; ++q) {
+            acc[q] = acc2[q];
+            acc2[q] = 0.f;
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < EPL; ++q) acc[q] = 0.f;
+        }
         ++cur;
         if constexpr (LEAN) optr += ostride;
         bstart = bend;
-        if (cur < endb) bend = off[cur + 1];
+        if constexpr (SPAN) {
+          bend = bnext;
+          if (cur + 1 < endb) bnext = off[cur + 2];
+        } else {
+          if (cur < endb) bend = off[cur + 1];
+        }
       }
     };
 
@@ -228,7 +255,8 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
       // finds every id outside the table
       // rows of this group; positions are below 2^31, so unsigned sums of a
       // position and at most U cannot overflow
-      const int32_t n_in = (int32_t)(min((uint32_t)r + U, (uint32_t)bend) - (uint32_t)r);
+      // (SPAN: up to the end of the next bag; bnext >= bend > r)
+      const int32_t n_in = (int32_t)(min((uint32_t)r + U, (uint32_t)(SPAN ? bnext : bend)) - (uint32_t)r);
       raw16_t raw[U];
       if constexpr (LEAN) {
         static_assert(BUF, "the single-row-class kernel reads tables through buffer descriptors");
@@ -289,8 +317,27 @@ __device__ __forceinline__ int pool_segment_fast(KA a, int64_t t, int64_t b_lo, 
       } else {
         fetch_ids(ge);
       }
+      if constexpr (SPAN) {
+        // rows [0, split) of the group belong to bag cur, the rest to the next
+        const int32_t split = bend - r;
 #pragma unroll
-      for (int u = 0; u < U; ++u) accumulate<TIN, EPL>(acc, raw[u]);
+        for (int u = 0; u < U; ++u) {
+          // each row's bytes go to one accumulator, zeros to the other (a
+          // select of the raw bits: a row's infinities or NaNs stay in its bag)
+          const bool mine = u < split;
+          raw16_t here, next;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            here[q] = mine ? raw[u][q] : 0;
+            next[q] = mine ? 0 : raw[u][q];
+          }
+          accumulate<TIN, EPL>(acc, here);
+          accumulate<TIN, EPL>(acc2, next);
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < U; ++u) accumulate<TIN, EPL>(acc, raw[u]);
+      }
       r = ge;
       close_bags();
     }
@@ -437,7 +484,7 @@ __device__ __forceinline__ void finish_piece(KA a, int64_t w_first, int64_t bag,
 template <typename TIN, typename TOUT, int LPR, int U = kUnroll>
 struct Uniform {
   static __device__ __forceinline__ int segment(KA a, int64_t t, int64_t b_lo, int64_t b_hi, int lane) {
-    return pool_segment_fast<TIN, TOUT, LPR, true, true, U>(a, t, b_lo, b_hi, lane);
+    return pool_segment_fast<TIN, TOUT, LPR, true, true, U, LPR == 8>(a, t, b_lo, b_hi, lane);
   }
   static __device__ __forceinline__ int partial(KA a, int64_t t, int64_t b, int64_t lo, int64_t hi, int64_t slot,
                                                 int lane) {

@@ -255,3 +255,44 @@ def test_largest_buffer_table_masked_rows_read_zeros(dim, dtype):
     check_outputs(out.double().cpu().numpy(), ref, mag, dtype == torch.float16, False)
     del store, table
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("dim,dtype", [(64, 1), (32, 0)])
+def test_row_groups_across_bag_ends(dim, dtype):
+    """128-byte rows (eight lanes per row), whose row groups run on past a bag's
+    end into the next bag: short bags (0..12 rows, many empty or of one row),
+    sum and mean fields, explicit wave counts (the single-row-class kernel);
+    then a row holding +inf in one column, which must reach exactly the bags
+    that pool that row and leave every other output bit unchanged."""
+    rng = np.random.default_rng(90 + dim)
+    T, B, rows = 3, 3000, 200
+    dims, dtypes = [dim] * T, [dtype] * T
+    tables = [(rng.standard_normal((rows, dim)) * 0.01).astype(np.float16 if dtype else np.float32)
+              for _ in range(T)]
+    lens = rng.integers(0, 13, size=(T, B))
+    lens[rng.random((T, B)) < 0.15] = 0
+    lens[rng.random((T, B)) < 0.10] = 1
+    offs = np.zeros((T, B + 1), np.int32)
+    offs[:, 1:] = np.cumsum(lens, axis=1)
+    ids = np.concatenate([rng.integers(0, rows, size=int(offs[t, -1])) for t in range(T)]).astype(np.int32)
+    pool = [0, 1, 0]
+    for W in (97, 3001):
+        for od in (torch.float32, torch.float16):
+            out, st, _, _ = run_case(tables, ids, offs, pool, B, od, num_waves=W)
+            assert st == dpi.DPI_OK
+            check(tables, ids, offs, pool, B, out)
+    base, _, _, _ = run_case(tables, ids, offs, pool, B, torch.float32, num_waves=97)
+    hot_row, col = 5, 3
+    tables_inf = [t.copy() for t in tables]
+    tables_inf[1][hot_row, col] = np.inf
+    out, st, _, _ = run_case(tables_inf, ids, offs, pool, B, torch.float32, num_waves=97)
+    assert st == dpi.DPI_OK
+    got, ref = out.cpu().numpy(), base.cpu().numpy()
+    lo = int(offs[0, -1])
+    seg = ids[lo: lo + int(offs[1, -1])]
+    has = np.array([np.any(seg[offs[1, b]: offs[1, b + 1]] == hot_row) for b in range(B)])
+    c = dim + col                     # field 1's column
+    assert has.any() and np.all(np.isposinf(got[has, c]))
+    keep = np.ones(got.shape, bool)
+    keep[has, c] = False
+    assert np.array_equal(got[keep], ref[keep])
