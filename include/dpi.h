@@ -87,8 +87,9 @@ typedef enum { DPI_X_F32 = 0, DPI_X_I64 = 1, DPI_X_I32 = 2 } dpi_x_dtype;   /* h
 enum {
   DPI_FLAG_EXACT_SPLIT = 1u << 1,  /* never move a wave boundary to a bag's end (many split bags) */
   DPI_FLAG_LINEAR_BLOCKS = 1u << 2, /* workgroup i takes waves 4i..4i+3 (default: each XCD of the
-                                       chip takes a contiguous range of waves, so one field's rows
-                                       meet in one L2) */
+                                       chip, or each pair of XCDs when every row is at most 128
+                                       bytes, takes a contiguous range of waves, so one field's
+                                       rows meet in few L2s) */
   DPI_FLAG_INPUT_FIRST = 1u << 3    /* dpi_lookup allocates one lane per bag (the input-first
                                        alternative of §IV-C) instead of the plan's waves; same
                                        results, kept for comparison */

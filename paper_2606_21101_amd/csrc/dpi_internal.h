@@ -155,7 +155,7 @@ struct LookupArgs {
   int32_t C;
   int32_t dmax;
   int32_t out_f16;
-  int32_t xcd_affine;
+  int32_t xcd_affine;      // XCDs per contiguous range of blocks (1 or 2), 0: linear order
   int32_t uniform_class;   // TableInfo class bits shared by every field, or -1
   int32_t input_first;     // one lane per bag instead of the plan's waves
   int32_t onehot;          // no offsets: every bag holds one id

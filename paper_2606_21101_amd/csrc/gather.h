@@ -201,11 +201,16 @@ __device__ __forceinline__ bool use_buffer(const TableInfo& ti) {
   return ti.num_rows * (int64_t)ti.row_bytes <= (int64_t)0xffffffffLL;
 }
 
-__device__ __forceinline__ int64_t xcd_affine_block(int64_t g, int64_t n) {
-  // workgroups are dispatched round-robin over 8 XCDs; give XCD x the
-  // contiguous logical range of its round-robin share
+// Workgroups are dispatched round-robin over 8 XCDs.  group = 1: XCD x takes
+// the contiguous logical range of its round-robin share.  group = 2: XCDs 2p
+// and 2p + 1 share one contiguous range, alternating blocks (a bijection on
+// [0, n) either way: the group's blocks in dispatch order, after the blocks
+// of the XCDs before it).
+__device__ __forceinline__ int64_t xcd_affine_block(int64_t g, int64_t n, int32_t group) {
   const int64_t x = g & 7, i = g >> 3, q = n >> 3, r = n & 7;
-  return x < r ? x * (q + 1) + i : r * (q + 1) + (x - r) * q + i;
+  const int64_t lo = group == 2 ? (x & ~(int64_t)1) : x;   // first XCD of x's group
+  const int64_t m = x - lo;
+  return lo * q + min(lo, r) + i * group + m;
 }
 
 #define DPI_FOR_LPR(MACRO) \

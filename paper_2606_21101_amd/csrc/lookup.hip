@@ -590,7 +590,7 @@ template <typename P>
 __device__ __forceinline__ void wave_body(KA a) {
   const int lane = threadIdx.x & (kWaveSize - 1);
   int64_t blk = blockIdx.x;
-  if (a->xcd_affine) blk = xcd_affine_block(blk, gridDim.x);
+  if (a->xcd_affine) blk = xcd_affine_block(blk, gridDim.x, a->xcd_affine);
   const int64_t w = blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   if (w >= a->grid_waves) return;
   // the plan's wave count and verdict and this wave's range, requested
@@ -663,7 +663,7 @@ void lookup_onehot_kernel(const LookupArgs args) {
   constexpr int64_t kRowsPerWave = (int64_t)(kWaveSize / LPR) * kOneHotRows;
   const KA a = (KA)__builtin_amdgcn_kernarg_segment_ptr();
   const int lane = threadIdx.x & (kWaveSize - 1);
-  const int64_t blk = a->xcd_affine ? xcd_affine_block(blockIdx.x, gridDim.x) : (int64_t)blockIdx.x;
+  const int64_t blk = a->xcd_affine ? xcd_affine_block(blockIdx.x, gridDim.x, a->xcd_affine) : (int64_t)blockIdx.x;
   const int64_t per_field = (a->B + kRowsPerWave - 1) / kRowsPerWave;
   const int64_t gw = blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   if (gw >= per_field * a->T) return;

@@ -363,7 +363,7 @@ void lookup_small_onehot_kernel(const SmallArgs args) {
   constexpr int64_t kRowsPerWave = (int64_t)(kWaveSize / LPR) * kOneHotRows;
   const KS a = (KS)__builtin_amdgcn_kernarg_segment_ptr();
   const int lane = threadIdx.x & (kWaveSize - 1);
-  const int64_t blk = a->xcd_affine ? xcd_affine_block(blockIdx.x, gridDim.x) : (int64_t)blockIdx.x;
+  const int64_t blk = a->xcd_affine ? xcd_affine_block(blockIdx.x, gridDim.x, a->xcd_affine) : (int64_t)blockIdx.x;
   const int64_t per_field = (a->B + kRowsPerWave - 1) / kRowsPerWave;
   const int64_t gw = blk * kWavesPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x / kWaveSize);
   if (gw >= per_field * a->T) return;
