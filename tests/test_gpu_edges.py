@@ -262,6 +262,7 @@ def test_row_groups_across_bag_ends(dim, dtype):
     """128-byte rows (eight lanes per row), whose row groups run on past a bag's
     end into the next bag: short bags (0..12 rows, many empty or of one row),
     sum and mean fields, explicit wave counts (the single-row-class kernel);
+    the linear block order bit for bit against the default (pairs of XCDs);
     then a row holding +inf in one column, which must reach exactly the bags
     that pool that row and leave every other output bit unchanged."""
     rng = np.random.default_rng(90 + dim)
@@ -282,6 +283,11 @@ def test_row_groups_across_bag_ends(dim, dtype):
             assert st == dpi.DPI_OK
             check(tables, ids, offs, pool, B, out)
     base, _, _, _ = run_case(tables, ids, offs, pool, B, torch.float32, num_waves=97)
+    # rows of at most 128 bytes: pairs of XCDs share each range of waves; the
+    # linear block order must give the same bits
+    lin, st, _, _ = run_case(tables, ids, offs, pool, B, torch.float32, num_waves=97,
+                             flags=dpi.DPI_FLAG_LINEAR_BLOCKS)
+    assert st == dpi.DPI_OK and torch.equal(lin, base)
     hot_row, col = 5, 3
     tables_inf = [t.copy() for t in tables]
     tables_inf[1][hot_row, col] = np.inf
